@@ -1,0 +1,149 @@
+/*
+ * convsel -- forward 2-D convolution for AMD MI355X (gfx950) with a per-call
+ * choice of algorithm.
+ *
+ * The operation is the forward pass of a convolution layer as PyTorch's Conv2d
+ * defines it (the paper, Sec. IV, requires every algorithm to reproduce that
+ * output).  With G groups, Cg = C/G and Kg = K/G:
+ *
+ *   P = floor((H + 2*pad_h - dil_h*(R-1) - 1) / stride_h) + 1
+ *   Q = floor((W + 2*pad_w - dil_w*(S-1) - 1) / stride_w) + 1
+ *   y[n,k,p,q] = b[k] + sum_{c<Cg, r<R, s<S}
+ *                x[n, (k/Kg)*Cg + c, p*stride_h - pad_h + r*dil_h,
+ *                                    q*stride_w - pad_w + s*dil_w] * w[k,c,r,s]
+ *
+ * where x reads as zero outside the image (cross-correlation, no filter flip),
+ * optionally followed by max(0, .) (the ReLU that follows convolutions in the
+ * paper's example networks, Sec. IV Listing 1).
+ *
+ * The algorithms are those the paper lets a user pick per layer (Sec. II-B and
+ * Sec. V-B): direct convolution, implicit GEMM (no column matrix is formed),
+ * IM2COL + GEMM (the column matrix is formed in a workspace, then multiplied),
+ * and Winograd minimal filtering F(2x2, 3x3) for 3x3 stride-1 layers.  All of
+ * them compute the same function; they differ in speed and workspace.
+ *
+ * Conventions shared by every entry point:
+ *  - Layouts: x is N x C x H x W, w is K x Cg x R x S, b is K values, y is
+ *    N x K x P x Q; all dense row-major (NCHW / KCRS), device memory.
+ *  - x, w, b and y share one element type (conv_dtype_t).  bf16 data is
+ *    multiplied exactly and accumulated in fp32; outputs are rounded to the
+ *    element type (round to nearest even for bf16).
+ *  - Ownership: the caller owns every buffer (inputs, output, workspace).  The
+ *    library allocates no device memory inside any entry point and keeps no
+ *    per-call state; the only process state is a lazily filled, thread-safe
+ *    table of device properties.
+ *  - Streams: `stream` is a hipStream_t passed as void* (NULL = the default
+ *    stream).  Work is enqueued and the call returns without synchronising.
+ *  - Errors: status codes only.  Every argument, shape, support and workspace
+ *    check runs on the host before the first HIP call, so those errors leave
+ *    the device untouched.  A failed HIP call (no device, wrong architecture,
+ *    launch failure) returns CONV_ERR_DEVICE with the HIP error cleared.
+ *  - N == 0 is a valid no-op.  P < 1 or Q < 1 is CONV_ERR_INVALID_ARG.
+ */
+#ifndef CONVSEL_H
+#define CONVSEL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum conv_status {
+  CONV_OK = 0,
+  CONV_ERR_INVALID_ARG = 1,  /* bad descriptor, NULL pointer, overlap, empty output */
+  CONV_ERR_UNSUPPORTED = 2,  /* the algorithm is not defined for this layer */
+  CONV_ERR_WORKSPACE = 3,    /* workspace smaller than conv2d_workspace_bytes() */
+  CONV_ERR_DEVICE = 4        /* a HIP call failed */
+} conv_status_t;
+
+typedef enum conv_algo {
+  CONV_ALGO_DEFAULT = 0,        /* the library's own pick, conv2d_default_algo() */
+  CONV_ALGO_DIRECT = 1,         /* paper Sec. II-B item (d) */
+  CONV_ALGO_IMPLICIT_GEMM = 2,  /* paper Sec. V-B item (b) */
+  CONV_ALGO_IM2COL_GEMM = 3,    /* paper Sec. II-B item (a), Sec. V-B item (c) */
+  CONV_ALGO_WINOGRAD = 4        /* paper Sec. V-B item (d): F(2x2,3x3) */
+} conv_algo_t;
+
+typedef enum conv_dtype {
+  CONV_F32 = 0,
+  CONV_BF16 = 1
+} conv_dtype_t;
+
+/* One layer.  Sizes are element counts; w holds K x (C/groups) x R x S. */
+typedef struct conv2d_desc {
+  int64_t n, c, h, w;
+  int64_t k, r, s;
+  int32_t stride_h, stride_w;
+  int32_t pad_h, pad_w;
+  int32_t dil_h, dil_w;
+  int32_t groups;
+  int32_t dtype;      /* conv_dtype_t */
+  int32_t has_bias;   /* 0: b must be NULL; 1: b holds K values */
+  int32_t fuse_relu;  /* 1: y = max(0, conv + bias) */
+} conv2d_desc_t;
+
+/* Output height and width of the layer (formula above).  INVALID_ARG for a
+ * malformed descriptor (non-positive sizes, stride or dilation < 1, negative
+ * padding, C or K not divisible by groups, unknown dtype) or an empty output. */
+conv_status_t conv2d_output_shape(const conv2d_desc_t* desc, int64_t* p, int64_t* q);
+
+/* OK if `algo` can run this layer; UNSUPPORTED if the algorithm is not defined
+ * for it (Winograd needs R = S = 3, stride 1, dilation 1, groups 1);
+ * INVALID_ARG as conv2d_output_shape, or for an unknown algo value. */
+conv_status_t conv2d_check(const conv2d_desc_t* desc, conv_algo_t algo);
+
+/* Device workspace, in bytes, that conv2d() needs for this layer and algo
+ * (0 for direct and implicit GEMM).  The column matrix and the Winograd
+ * buffers are processed in batches of images, so the figure is capped near
+ * 1 GiB unless one image alone needs more.  Same errors as conv2d_check. */
+conv_status_t conv2d_workspace_bytes(const conv2d_desc_t* desc, conv_algo_t algo, size_t* bytes);
+
+/* The concrete algorithm CONV_ALGO_DEFAULT resolves to for this layer (a fixed
+ * rule on the layer shape; the paper's "default" selector, Sec. IV).  Returns
+ * CONV_ALGO_DEFAULT itself only for an invalid descriptor. */
+conv_algo_t conv2d_default_algo(const conv2d_desc_t* desc);
+
+/* y = conv(x, w) (+ b) (then ReLU) with the chosen algorithm, enqueued on
+ * `stream`.  x, w, y (and b when has_bias) must be non-NULL device pointers;
+ * y must not overlap x, w, b or the workspace.  workspace may be NULL when
+ * workspace_bytes is 0.  Returns INVALID_ARG / UNSUPPORTED / WORKSPACE before
+ * touching the device, DEVICE if a HIP call fails. */
+conv_status_t conv2d(const void* x, const void* w, const void* b, void* y, const conv2d_desc_t* desc,
+                     conv_algo_t algo, void* workspace, size_t workspace_bytes, void* stream);
+
+/* The column matrix of the IM2COL + GEMM algorithm for all N images: col is
+ * N x G x (P*Q) x (Cg*R*S), element [n][g][p*Q+q][(c*R + r)*S + s] =
+ * x[n, g*Cg + c, p*stride_h - pad_h + r*dil_h, q*stride_w - pad_w + s*dil_w]
+ * (zero outside the image), in the layer's dtype.  A pure gather: results
+ * are bit-exact copies of input elements.  Same argument rules as conv2d. */
+conv_status_t conv2d_im2col(const void* x, void* col, const conv2d_desc_t* desc, void* stream);
+
+/* Winograd F(2x2,3x3) transforms (Lavin and Gray 2016, the algorithm the
+ * paper's Winograd variant names, Sec. V-B item (d)).  Only for layers where
+ * conv2d_check(desc, CONV_ALGO_WINOGRAD) is OK.
+ *  - filter: U is 16 x K x C, U[xi*4+nu][k][c] = (G w[k,c] G^T)[xi][nu],
+ *    computed in fp32 and stored in the layer's dtype.
+ *  - input:  V is 16 x T x C with T = N*ceil(P/2)*ceil(Q/2) tiles,
+ *    tile t = (n*ceil(P/2) + tp)*ceil(Q/2) + tq, V[xi*4+nu][t][c] =
+ *    (B^T d B)[xi][nu] where d is the 4x4 input patch at row 2tp - pad_h,
+ *    column 2tq - pad_w (zero outside the image); fp32 math, layer dtype. */
+conv_status_t conv2d_winograd_filter_transform(const void* w, void* u, const conv2d_desc_t* desc,
+                                               void* stream);
+conv_status_t conv2d_winograd_input_transform(const void* x, void* v, const conv2d_desc_t* desc,
+                                              void* stream);
+
+/* Static strings; never NULL ("unknown" for values outside the enums). */
+const char* conv2d_status_string(conv_status_t status);
+const char* conv2d_algo_name(conv_algo_t algo);
+
+/* Parses "default", "direct", "implicit_gemm", "im2col_gemm" (alias "gemm"),
+ * "winograd".  INVALID_ARG for NULL or any other name. */
+conv_status_t conv2d_algo_from_name(const char* name, conv_algo_t* algo);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CONVSEL_H */

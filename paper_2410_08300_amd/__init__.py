@@ -1,0 +1,15 @@
+"""Forward 2-D convolution for AMD MI355X (gfx950) with per-layer choice of
+algorithm -- direct, implicit GEMM, IM2COL + GEMM and Winograd F(2x2,3x3) --
+after the framework of "A Framework to Enable Algorithmic Design Choice
+Exploration in DNNs" (arXiv 2410.08300).
+
+The compute runs in hand-written HIP kernels behind a C ABI
+(include/convsel.h, libconvsel.so); PyTorch supplies device memory and
+streams.
+"""
+from ._lib import Conv2dError, ALGOS
+from .conv import conv2d, im2col, winograd_filter_transform, winograd_input_transform
+from .selection import AlgoTable, Conv2dSwap, swap_conv2d, select_fastest, tune, time_conv, supported_algos
+
+__all__ = ["Conv2dError", "ALGOS", "conv2d", "im2col", "winograd_filter_transform", "winograd_input_transform",
+           "AlgoTable", "Conv2dSwap", "swap_conv2d", "select_fastest", "tune", "time_conv", "supported_algos"]

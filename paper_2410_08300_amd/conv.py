@@ -1,0 +1,107 @@
+"""Torch-facing convolution call: marshals tensors into the C ABI.
+
+PyTorch supplies device memory (caching allocator) and the current stream;
+the convolution itself runs in the HIP library.  Inputs must be CUDA (HIP)
+tensors: there is no CPU path.
+"""
+import torch
+
+from . import _lib
+
+_TORCH_DTYPES = {torch.float32: "f32", torch.bfloat16: "bf16"}
+
+
+def _desc_for(x, w, b, stride, padding, dilation, groups, relu):
+    if x.dim() != 4 or w.dim() != 4:
+        raise ValueError("conv2d expects a 4-D NCHW input and a 4-D KCRS weight")
+    if x.dtype != w.dtype or (b is not None and b.dtype != x.dtype):
+        raise ValueError("input, weight and bias must share one dtype")
+    if x.dtype not in _TORCH_DTYPES:
+        raise ValueError("unsupported dtype %s (float32 or bfloat16)" % x.dtype)
+    N, C, H, W = x.shape
+    K, Cg, R, S = w.shape
+    if Cg * groups != C:
+        raise ValueError("weight expects %d input channels per group but input has %d channels and groups=%d"
+                         % (Cg, C, groups))
+    if b is not None and (b.dim() != 1 or b.shape[0] != K):
+        raise ValueError("bias must hold K=%d values" % K)
+    return _lib.make_desc(N, C, H, W, K, R, S, stride, padding, dilation, groups, _TORCH_DTYPES[x.dtype],
+                          b is not None, relu)
+
+
+def conv2d(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, algo="default", relu=False,
+           out=None):
+    """Forward 2-D convolution with the chosen algorithm.
+
+    Same semantics as ``torch.nn.functional.conv2d`` (zero padding given as
+    an int or a pair), plus ``algo`` ("default", "direct", "implicit_gemm",
+    "im2col_gemm" / "gemm", "winograd") and an optional fused ReLU.  Raises
+    ``Conv2dError`` for any non-OK library status.
+    """
+    if not (x.is_cuda and w.is_cuda and (b is None or b.is_cuda)):
+        raise ValueError("conv2d runs on the GPU only: move input, weight and bias to a HIP device")
+    desc = _desc_for(x, w, b, stride, padding, dilation, groups, relu)
+    x = x.contiguous()
+    w = w.contiguous()
+    b = None if b is None else b.contiguous()
+    P, Q = _lib.output_shape(desc)
+    algo_i = _lib.algo_id(algo)
+    with torch.cuda.device(x.device):
+        if out is None:
+            out = torch.empty((x.shape[0], w.shape[0], P, Q), device=x.device, dtype=x.dtype)
+        elif (out.shape != (x.shape[0], w.shape[0], P, Q) or out.dtype != x.dtype or not out.is_contiguous()
+              or out.device != x.device):
+            raise ValueError("out must be a contiguous %s tensor of shape %s on %s"
+                             % (x.dtype, (x.shape[0], w.shape[0], P, Q), x.device))
+        nws = _lib.workspace_bytes(desc, algo_i)
+        ws = torch.empty(nws, dtype=torch.uint8, device=x.device) if nws else None
+        stream = torch.cuda.current_stream(x.device).cuda_stream
+        st = _lib.conv2d_raw(x.data_ptr(), w.data_ptr(), None if b is None else b.data_ptr(), out.data_ptr(),
+                             desc, algo_i, None if ws is None else ws.data_ptr(), nws, stream)
+    if st != _lib.CONV_OK:
+        raise _lib.Conv2dError(st, "conv2d(algo=%s)" % _lib.algo_name(algo_i))
+    return out
+
+
+def im2col(x, kernel_size, stride=1, padding=0, dilation=1, groups=1):
+    """The column matrix of the IM2COL algorithm, [N][G][P*Q][Cg*R*S]."""
+    R, S = _lib._pair(kernel_size)
+    N, C, H, W = x.shape
+    desc = _lib.make_desc(N, C, H, W, groups, R, S, stride, padding, dilation, groups,
+                          _TORCH_DTYPES[x.dtype])
+    P, Q = _lib.output_shape(desc)
+    x = x.contiguous()
+    with torch.cuda.device(x.device):
+        col = torch.empty((N, groups, P * Q, (C // groups) * R * S), device=x.device, dtype=x.dtype)
+        st = _lib.im2col_raw(x.data_ptr(), col.data_ptr(), desc, torch.cuda.current_stream(x.device).cuda_stream)
+    if st != _lib.CONV_OK:
+        raise _lib.Conv2dError(st, "conv2d_im2col")
+    return col
+
+
+def winograd_filter_transform(w):
+    """U[16][K][C] of F(2x2,3x3) for 3x3 filters w[K][C][3][3]."""
+    K, C, R, S = w.shape
+    desc = _lib.make_desc(1, C, 4, 4, K, R, S, 1, 1, 1, 1, _TORCH_DTYPES[w.dtype])
+    w = w.contiguous()
+    with torch.cuda.device(w.device):
+        u = torch.empty((16, K, C), device=w.device, dtype=w.dtype)
+        st = _lib.wino_filter_raw(w.data_ptr(), u.data_ptr(), desc, torch.cuda.current_stream(w.device).cuda_stream)
+    if st != _lib.CONV_OK:
+        raise _lib.Conv2dError(st, "conv2d_winograd_filter_transform")
+    return u
+
+
+def winograd_input_transform(x, padding=1):
+    """V[16][T][C] of F(2x2,3x3) for input x (3x3 filter, stride 1)."""
+    N, C, H, W = x.shape
+    desc = _lib.make_desc(N, C, H, W, 1, 3, 3, 1, padding, 1, 1, _TORCH_DTYPES[x.dtype])
+    P, Q = _lib.output_shape(desc)
+    T = N * ((P + 1) // 2) * ((Q + 1) // 2)
+    x = x.contiguous()
+    with torch.cuda.device(x.device):
+        v = torch.empty((16, T, C), device=x.device, dtype=x.dtype)
+        st = _lib.wino_input_raw(x.data_ptr(), v.data_ptr(), desc, torch.cuda.current_stream(x.device).cuda_stream)
+    if st != _lib.CONV_OK:
+        raise _lib.Conv2dError(st, "conv2d_winograd_input_transform")
+    return v

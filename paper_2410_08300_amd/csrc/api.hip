@@ -1,0 +1,380 @@
+// C ABI of the library (declared in include/convsel.h): descriptor
+// validation, algorithm support, workspace sizes, the default-algorithm rule
+// and dispatch to the kernel launchers.  All checks run on the host before
+// the first HIP call.
+#include <mutex>
+#include <string.h>
+
+#include "../../include/convsel.h"
+#include "kernels.hpp"
+
+namespace convsel {
+bool implicit_gemm_fits(const Shape& s);
+}
+
+using convsel::Shape;
+
+namespace {
+
+constexpr int64_t kInt31 = (int64_t)1 << 31;
+constexpr size_t kWorkspaceCap = (size_t)1 << 30;  // batch the column matrix / Winograd buffers near 1 GiB
+
+int64_t out_extent(int64_t in, int64_t pad, int64_t dil, int64_t ker, int64_t stride) {
+  const int64_t span = in + 2 * pad - dil * (ker - 1) - 1;
+  if (span < 0) return 0;
+  return span / stride + 1;
+}
+
+conv_status_t validate(const conv2d_desc_t* d, Shape* s) {
+  if (!d) return CONV_ERR_INVALID_ARG;
+  if (d->n < 0 || d->c < 1 || d->h < 1 || d->w < 1 || d->k < 1 || d->r < 1 || d->s < 1) return CONV_ERR_INVALID_ARG;
+  if (d->stride_h < 1 || d->stride_w < 1 || d->dil_h < 1 || d->dil_w < 1) return CONV_ERR_INVALID_ARG;
+  if (d->pad_h < 0 || d->pad_w < 0 || d->groups < 1) return CONV_ERR_INVALID_ARG;
+  if (d->c % d->groups != 0 || d->k % d->groups != 0) return CONV_ERR_INVALID_ARG;
+  if (d->dtype != CONV_F32 && d->dtype != CONV_BF16) return CONV_ERR_INVALID_ARG;
+  if ((d->has_bias != 0 && d->has_bias != 1) || (d->fuse_relu != 0 && d->fuse_relu != 1)) return CONV_ERR_INVALID_ARG;
+  const int64_t P = out_extent(d->h, d->pad_h, d->dil_h, d->r, d->stride_h);
+  const int64_t Q = out_extent(d->w, d->pad_w, d->dil_w, d->s, d->stride_w);
+  if (P < 1 || Q < 1) return CONV_ERR_INVALID_ARG;
+  // Every tensor, and the pixel count N*P*Q, must stay below 2^31 elements
+  // (the kernels index within a tensor in 32 bits where it is cheaper).
+  if (d->c > kInt31 / d->h || d->c * d->h > kInt31 / d->w) return CONV_ERR_INVALID_ARG;
+  const int64_t chw = d->c * d->h * d->w;
+  if (d->n > 0 && d->n > (kInt31 - 1) / chw) return CONV_ERR_INVALID_ARG;
+  const int64_t Cg = d->c / d->groups;
+  if (d->r > kInt31 / d->s || Cg > kInt31 / (d->r * d->s) || d->k > kInt31 / (Cg * d->r * d->s))
+    return CONV_ERR_INVALID_ARG;
+  if (P > kInt31 / Q || d->k > kInt31 / (P * Q)) return CONV_ERR_INVALID_ARG;
+  if (d->n > 0 && d->n > (kInt31 - 1) / (d->k * P * Q)) return CONV_ERR_INVALID_ARG;
+  if (s) {
+    s->N = d->n; s->C = d->c; s->H = d->h; s->W = d->w; s->K = d->k; s->R = d->r; s->S = d->s;
+    s->P = P; s->Q = Q;
+    s->G = d->groups; s->Cg = Cg; s->Kg = d->k / d->groups;
+    s->sh = d->stride_h; s->sw = d->stride_w; s->ph = d->pad_h; s->pw = d->pad_w;
+    s->dh = d->dil_h; s->dw = d->dil_w;
+    s->dtype = d->dtype == CONV_F32 ? convsel::DT_F32 : convsel::DT_BF16;
+    s->bias = d->has_bias != 0;
+    s->relu = d->fuse_relu != 0;
+  }
+  return CONV_OK;
+}
+
+bool winograd_ok(const Shape& s) {
+  return s.R == 3 && s.S == 3 && s.sh == 1 && s.sw == 1 && s.dh == 1 && s.dw == 1 && s.G == 1;
+}
+
+conv_status_t support(const Shape& s, conv_algo_t algo) {
+  switch (algo) {
+    case CONV_ALGO_DIRECT:
+    case CONV_ALGO_IM2COL_GEMM:
+      return CONV_OK;
+    case CONV_ALGO_IMPLICIT_GEMM:
+      return convsel::implicit_gemm_fits(s) ? CONV_OK : CONV_ERR_UNSUPPORTED;
+    case CONV_ALGO_WINOGRAD:
+      return winograd_ok(s) ? CONV_OK : CONV_ERR_UNSUPPORTED;
+    default:
+      return CONV_ERR_INVALID_ARG;
+  }
+}
+
+conv_algo_t default_rule(const Shape& s) {
+  // One input channel per group (depthwise): the HBM-bound direct kernel.
+  if (s.Cg == 1) return CONV_ALGO_DIRECT;
+  if (convsel::implicit_gemm_fits(s)) return CONV_ALGO_IMPLICIT_GEMM;
+  return CONV_ALGO_IM2COL_GEMM;
+}
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+// Images per batch of the column matrix.
+int64_t im2col_batch(const Shape& s, size_t* bytes) {
+  const size_t per_img = (size_t)s.G * s.P * s.Q * s.Cg * s.R * s.S * s.esize();
+  int64_t nb = (int64_t)(kWorkspaceCap / per_img);
+  if (nb < 1) nb = 1;
+  if (nb > s.N) nb = s.N;
+  if (bytes) *bytes = (size_t)nb * per_img;
+  return nb;
+}
+
+struct WinoLayout {
+  int64_t nb, TPQ;
+  size_t v_off, m_off, total;
+};
+
+WinoLayout wino_layout(const Shape& s) {
+  WinoLayout L;
+  L.TPQ = ((s.P + 1) / 2) * ((s.Q + 1) / 2);
+  const size_t u_bytes = (size_t)16 * s.K * s.C * s.esize();
+  const size_t v_img = (size_t)16 * L.TPQ * s.C * s.esize();
+  const size_t m_img = (size_t)16 * s.K * L.TPQ * 4;
+  int64_t nb = (int64_t)(kWorkspaceCap / (v_img + m_img));
+  if (nb < 1) nb = 1;
+  if (nb > s.N) nb = s.N;
+  L.nb = nb;
+  L.v_off = align256(u_bytes);
+  L.m_off = align256(L.v_off + nb * v_img);
+  L.total = L.m_off + nb * m_img;
+  return L;
+}
+
+size_t workspace_for(const Shape& s, conv_algo_t algo) {
+  if (s.N == 0) return 0;
+  if (algo == CONV_ALGO_IM2COL_GEMM) {
+    size_t b = 0;
+    im2col_batch(s, &b);
+    return b;
+  }
+  if (algo == CONV_ALGO_WINOGRAD) return wino_layout(s).total;
+  return 0;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + nb && b0 < a0 + na;
+}
+
+// Device readiness: a current device that is gfx950.  Cached per device.
+std::mutex g_dev_mu;
+int g_dev_state[64];  // 0 unknown, 1 ok, 2 unusable
+
+conv_status_t ensure_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    (void)hipGetLastError();
+    return CONV_ERR_DEVICE;
+  }
+  std::lock_guard<std::mutex> lock(g_dev_mu);
+  if (g_dev_state[dev] == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return CONV_ERR_DEVICE;
+    }
+    g_dev_state[dev] = strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 2;
+  }
+  return g_dev_state[dev] == 1 ? CONV_OK : CONV_ERR_DEVICE;
+}
+
+conv_status_t from_hip(hipError_t e) {
+  if (e == hipSuccess) return CONV_OK;
+  (void)hipGetLastError();
+  return CONV_ERR_DEVICE;
+}
+
+conv_status_t run(const Shape& s, conv_algo_t algo, const void* x, const void* w, const void* b, void* y,
+                  void* ws, hipStream_t st) {
+  using namespace convsel;
+  switch (algo) {
+    case CONV_ALGO_DIRECT:
+      return from_hip(launch_direct(s, x, w, b, y, st));
+    case CONV_ALGO_IMPLICIT_GEMM:
+      return from_hip(launch_implicit_gemm(s, x, w, b, y, st));
+    case CONV_ALGO_IM2COL_GEMM: {
+      const int64_t nb = im2col_batch(s, nullptr);
+      const int64_t crs = s.Cg * s.R * s.S, PQ = s.P * s.Q;
+      for (int64_t n0 = 0; n0 < s.N; n0 += nb) {
+        const int64_t cnt = s.N - n0 < nb ? s.N - n0 : nb;
+        hipError_t e = launch_im2col(s, x, ws, n0, cnt, st);
+        if (e != hipSuccess) return from_hip(e);
+        GemmArgs g;
+        g.A = w;
+        g.B = ws;
+        g.C = (char*)y + (size_t)n0 * s.K * PQ * s.esize();
+        g.bias = b;
+        g.M = (int)s.Kg; g.N = (int)PQ; g.Kred = (int)crs;
+        g.lda = crs; g.ldb = crs; g.ldc = PQ;
+        g.batch = (int)(cnt * s.G); g.bdiv = s.G;
+        g.sA0 = 0; g.sA1 = s.Kg * crs;                 // group g's filters
+        g.sB0 = s.G * PQ * crs; g.sB1 = PQ * crs;      // image, group rows of col
+        g.sC0 = s.K * PQ; g.sC1 = s.Kg * PQ;           // image, group planes of y
+        g.sBias1 = s.Kg;                               // group g's biases
+        g.relu = s.relu ? 1 : 0;
+        g.out_f32 = 0;
+        e = launch_gemm_nt(s.dtype, g, st);
+        if (e != hipSuccess) return from_hip(e);
+      }
+      return CONV_OK;
+    }
+    case CONV_ALGO_WINOGRAD: {
+      const WinoLayout L = wino_layout(s);
+      char* base = (char*)ws;
+      void* U = base;
+      void* V = base + L.v_off;
+      float* M = (float*)(base + L.m_off);
+      hipError_t e = launch_wino_filter(s, w, U, st);
+      if (e != hipSuccess) return from_hip(e);
+      for (int64_t n0 = 0; n0 < s.N; n0 += L.nb) {
+        const int64_t cnt = s.N - n0 < L.nb ? s.N - n0 : L.nb;
+        const int64_t Tc = cnt * L.TPQ;
+        e = launch_wino_input(s, x, V, n0, cnt, st);
+        if (e != hipSuccess) return from_hip(e);
+        GemmArgs g;
+        g.A = U; g.B = V; g.C = M; g.bias = nullptr;
+        g.M = (int)s.K; g.N = (int)Tc; g.Kred = (int)s.C;
+        g.lda = s.C; g.ldb = s.C; g.ldc = Tc;
+        g.batch = 16; g.bdiv = 1;
+        g.sA0 = s.K * s.C; g.sA1 = 0;
+        g.sB0 = Tc * s.C; g.sB1 = 0;
+        g.sC0 = s.K * Tc; g.sC1 = 0;
+        g.sBias1 = 0;
+        g.relu = 0;
+        g.out_f32 = 1;
+        e = launch_gemm_nt(s.dtype, g, st);
+        if (e != hipSuccess) return from_hip(e);
+        e = launch_wino_output(s, M, b, (char*)y + (size_t)n0 * s.K * s.P * s.Q * s.esize(), 0, cnt, st);
+        if (e != hipSuccess) return from_hip(e);
+      }
+      return CONV_OK;
+    }
+    default:
+      return CONV_ERR_INVALID_ARG;
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+conv_status_t conv2d_output_shape(const conv2d_desc_t* desc, int64_t* p, int64_t* q) {
+  Shape s;
+  const conv_status_t st = validate(desc, &s);
+  if (st != CONV_OK) return st;
+  if (!p || !q) return CONV_ERR_INVALID_ARG;
+  *p = s.P;
+  *q = s.Q;
+  return CONV_OK;
+}
+
+conv_status_t conv2d_check(const conv2d_desc_t* desc, conv_algo_t algo) {
+  Shape s;
+  const conv_status_t st = validate(desc, &s);
+  if (st != CONV_OK) return st;
+  if (algo == CONV_ALGO_DEFAULT) algo = default_rule(s);
+  return support(s, algo);
+}
+
+conv_status_t conv2d_workspace_bytes(const conv2d_desc_t* desc, conv_algo_t algo, size_t* bytes) {
+  Shape s;
+  conv_status_t st = validate(desc, &s);
+  if (st != CONV_OK) return st;
+  if (!bytes) return CONV_ERR_INVALID_ARG;
+  if (algo == CONV_ALGO_DEFAULT) algo = default_rule(s);
+  st = support(s, algo);
+  if (st != CONV_OK) return st;
+  *bytes = workspace_for(s, algo);
+  return CONV_OK;
+}
+
+conv_algo_t conv2d_default_algo(const conv2d_desc_t* desc) {
+  Shape s;
+  if (validate(desc, &s) != CONV_OK) return CONV_ALGO_DEFAULT;
+  return default_rule(s);
+}
+
+conv_status_t conv2d(const void* x, const void* w, const void* b, void* y, const conv2d_desc_t* desc,
+                     conv_algo_t algo, void* workspace, size_t workspace_bytes, void* stream) {
+  Shape s;
+  conv_status_t st = validate(desc, &s);
+  if (st != CONV_OK) return st;
+  if (algo == CONV_ALGO_DEFAULT) algo = default_rule(s);
+  st = support(s, algo);
+  if (st != CONV_OK) return st;
+  if (s.N == 0) return CONV_OK;
+  if (!x || !w || !y || (s.bias != (b != nullptr))) return CONV_ERR_INVALID_ARG;
+  const size_t need = workspace_for(s, algo);
+  if (workspace_bytes < need || (need > 0 && !workspace)) return CONV_ERR_WORKSPACE;
+  const size_t es = (size_t)s.esize();
+  const size_t ybytes = (size_t)s.N * s.K * s.P * s.Q * es;
+  if (overlaps(y, ybytes, x, (size_t)s.N * s.C * s.H * s.W * es) ||
+      overlaps(y, ybytes, w, (size_t)s.K * s.Cg * s.R * s.S * es) ||
+      overlaps(y, ybytes, b, s.bias ? (size_t)s.K * es : 0) ||
+      overlaps(y, ybytes, workspace, need))
+    return CONV_ERR_INVALID_ARG;
+  st = ensure_device();
+  if (st != CONV_OK) return st;
+  return run(s, algo, x, w, b, y, workspace, (hipStream_t)stream);
+}
+
+conv_status_t conv2d_im2col(const void* x, void* col, const conv2d_desc_t* desc, void* stream) {
+  Shape s;
+  conv_status_t st = validate(desc, &s);
+  if (st != CONV_OK) return st;
+  if (s.N == 0) return CONV_OK;
+  if (!x || !col) return CONV_ERR_INVALID_ARG;
+  const size_t es = (size_t)s.esize();
+  if (overlaps(col, (size_t)s.N * s.G * s.P * s.Q * s.Cg * s.R * s.S * es, x, (size_t)s.N * s.C * s.H * s.W * es))
+    return CONV_ERR_INVALID_ARG;
+  st = ensure_device();
+  if (st != CONV_OK) return st;
+  return from_hip(convsel::launch_im2col(s, x, col, 0, s.N, (hipStream_t)stream));
+}
+
+conv_status_t conv2d_winograd_filter_transform(const void* w, void* u, const conv2d_desc_t* desc, void* stream) {
+  Shape s;
+  conv_status_t st = validate(desc, &s);
+  if (st != CONV_OK) return st;
+  if (!winograd_ok(s)) return CONV_ERR_UNSUPPORTED;
+  if (!w || !u) return CONV_ERR_INVALID_ARG;
+  const size_t es = (size_t)s.esize();
+  if (overlaps(u, (size_t)16 * s.K * s.C * es, w, (size_t)s.K * s.C * 9 * es)) return CONV_ERR_INVALID_ARG;
+  st = ensure_device();
+  if (st != CONV_OK) return st;
+  return from_hip(convsel::launch_wino_filter(s, w, u, (hipStream_t)stream));
+}
+
+conv_status_t conv2d_winograd_input_transform(const void* x, void* v, const conv2d_desc_t* desc, void* stream) {
+  Shape s;
+  conv_status_t st = validate(desc, &s);
+  if (st != CONV_OK) return st;
+  if (!winograd_ok(s)) return CONV_ERR_UNSUPPORTED;
+  if (s.N == 0) return CONV_OK;
+  if (!x || !v) return CONV_ERR_INVALID_ARG;
+  const size_t es = (size_t)s.esize();
+  const int64_t T = s.N * ((s.P + 1) / 2) * ((s.Q + 1) / 2);
+  if (T > kInt31 / s.C / 16) return CONV_ERR_INVALID_ARG;
+  if (overlaps(v, (size_t)16 * T * s.C * es, x, (size_t)s.N * s.C * s.H * s.W * es)) return CONV_ERR_INVALID_ARG;
+  st = ensure_device();
+  if (st != CONV_OK) return st;
+  return from_hip(convsel::launch_wino_input(s, x, v, 0, s.N, (hipStream_t)stream));
+}
+
+const char* conv2d_status_string(conv_status_t status) {
+  switch (status) {
+    case CONV_OK: return "ok";
+    case CONV_ERR_INVALID_ARG: return "invalid argument";
+    case CONV_ERR_UNSUPPORTED: return "algorithm not supported for this layer";
+    case CONV_ERR_WORKSPACE: return "workspace too small";
+    case CONV_ERR_DEVICE: return "device error";
+    default: return "unknown";
+  }
+}
+
+const char* conv2d_algo_name(conv_algo_t algo) {
+  switch (algo) {
+    case CONV_ALGO_DEFAULT: return "default";
+    case CONV_ALGO_DIRECT: return "direct";
+    case CONV_ALGO_IMPLICIT_GEMM: return "implicit_gemm";
+    case CONV_ALGO_IM2COL_GEMM: return "im2col_gemm";
+    case CONV_ALGO_WINOGRAD: return "winograd";
+    default: return "unknown";
+  }
+}
+
+conv_status_t conv2d_algo_from_name(const char* name, conv_algo_t* algo) {
+  if (!name || !algo) return CONV_ERR_INVALID_ARG;
+  static const struct {
+    const char* name;
+    conv_algo_t algo;
+  } table[] = {{"default", CONV_ALGO_DEFAULT},         {"direct", CONV_ALGO_DIRECT},
+               {"implicit_gemm", CONV_ALGO_IMPLICIT_GEMM}, {"im2col_gemm", CONV_ALGO_IM2COL_GEMM},
+               {"gemm", CONV_ALGO_IM2COL_GEMM},         {"winograd", CONV_ALGO_WINOGRAD}};
+  for (const auto& e : table)
+    if (strcmp(name, e.name) == 0) {
+      *algo = e.algo;
+      return CONV_OK;
+    }
+  return CONV_ERR_INVALID_ARG;
+}
+
+}  // extern "C"

@@ -1,0 +1,65 @@
+// Host-side interface between the C ABI (api.hip) and the kernel launchers.
+// Every launcher enqueues on `stream` and returns the HIP status of its last
+// launch; shapes are validated by the caller before any launcher runs.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace convsel {
+
+enum { DT_F32 = 0, DT_BF16 = 1 };
+
+// A validated layer with its derived sizes.
+struct Shape {
+  int64_t N, C, H, W, K, R, S, P, Q;
+  int64_t Cg, Kg;
+  int sh, sw, ph, pw, dh, dw, G;
+  int dtype;
+  bool bias, relu;
+  int64_t esize() const { return dtype == DT_F32 ? 4 : 2; }
+};
+
+// Batched "NT" GEMM on MFMA:  C[b][i][j] = sum_k A[b][i][k] * B[b][j][k]
+// (+ bias[b1*sBias1 + i], then ReLU), i < M, j < N, k < Kred.  Both operands
+// are reduction-contiguous (row-major with leading dimensions lda / ldb).
+// Batch b is split as b0 = b / bdiv, b1 = b % bdiv and every operand is
+// offset by b0*s?0 + b1*s?1 elements.  C is stored in the data type, or in
+// fp32 when out_f32 is set.
+struct GemmArgs {
+  const void* A;
+  const void* B;
+  void* C;
+  const void* bias;
+  int M, N, Kred;
+  int64_t lda, ldb, ldc;
+  int batch, bdiv;
+  int64_t sA0, sA1, sB0, sB1, sC0, sC1;
+  int64_t sBias1;
+  int relu;
+  int out_f32;
+};
+
+hipError_t launch_gemm_nt(int dtype, const GemmArgs& g, hipStream_t stream);
+
+// direct convolution (VALU), all N images.
+hipError_t launch_direct(const Shape& s, const void* x, const void* w, const void* b, void* y,
+                         hipStream_t stream);
+
+// implicit GEMM (MFMA), all N images.
+hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, const void* b, void* y,
+                                hipStream_t stream);
+
+// Column matrix [nb][G][P*Q][Cg*R*S] of images n0 .. n0+nb-1.
+hipError_t launch_im2col(const Shape& s, const void* x, void* col, int64_t n0, int64_t nb,
+                         hipStream_t stream);
+
+// Winograd F(2x2,3x3) pieces.  U: 16 x K x C.  V: 16 x Tc x C and M: 16 x K x Tc
+// (fp32) for the Tc = nb*TP*TQ tiles of images n0 .. n0+nb-1.
+hipError_t launch_wino_filter(const Shape& s, const void* w, void* U, hipStream_t stream);
+hipError_t launch_wino_input(const Shape& s, const void* x, void* V, int64_t n0, int64_t nb,
+                             hipStream_t stream);
+hipError_t launch_wino_output(const Shape& s, const float* M, const void* b, void* y, int64_t n0,
+                              int64_t nb, hipStream_t stream);
+
+}  // namespace convsel

@@ -1,0 +1,222 @@
+"""Per-layer algorithm selection (paper, Sec. IV).
+
+* ``AlgoTable``: an ordered map from a convolution module's qualified name to
+  the algorithm it runs.  Swapped modules read it at every call, so editing
+  the table changes the algorithm without touching the model.
+* ``swap_conv2d(model, selector)``: replaces, in place, every
+  ``torch.nn.Conv2d`` with a ``Conv2dSwap`` wrapper.  The selector is one of
+  the paper's three kinds -- a single algorithm name for every layer, a list
+  indexed by the layer's position among the model's Conv2d modules, or a
+  callable that receives the module and returns a name -- or an existing
+  ``AlgoTable`` / dict keyed by qualified name.  "torch" keeps a module as it
+  is; "default" lets the library pick per call.
+* ``select_fastest`` / ``tune``: measured selection -- time every algorithm
+  that supports a layer and record the fastest in the table.
+"""
+import collections
+import json
+
+import torch
+from torch import nn
+
+from . import _lib
+from .conv import conv2d
+
+ALGO_CHOICES = ("default", "direct", "implicit_gemm", "im2col_gemm", "gemm", "winograd", "torch")
+CONCRETE_ALGOS = ("direct", "implicit_gemm", "im2col_gemm", "winograd")
+
+
+def _canonical(name):
+    if not isinstance(name, str) or name not in ALGO_CHOICES:
+        raise ValueError("unknown convolution algorithm %r (choose from %s)" % (name, ", ".join(ALGO_CHOICES)))
+    return "im2col_gemm" if name == "gemm" else name
+
+
+class AlgoTable(collections.OrderedDict):
+    """qualified module name -> algorithm name."""
+
+    def set(self, name, algo):
+        self[name] = _canonical(algo)
+
+    def get_algo(self, name):
+        return self.get(name, "default")
+
+    def to_json(self):
+        return json.dumps(list(self.items()))
+
+    @classmethod
+    def from_json(cls, text):
+        t = cls()
+        for name, algo in json.loads(text):
+            t.set(name, algo)
+        return t
+
+
+def _padding_pair(m):
+    if isinstance(m.padding, str):
+        if m.padding == "valid":
+            return (0, 0)
+        # "same" with stride 1: symmetric only when the dilated extent is odd.
+        pads = []
+        for d, k in zip(m.dilation, m.kernel_size):
+            total = d * (k - 1)
+            if total % 2:
+                raise ValueError("padding='same' with an even filter extent needs asymmetric padding, "
+                                 "which the library does not offer")
+            pads.append(total // 2)
+        return tuple(pads)
+    return tuple(m.padding)
+
+
+def _static_check(name, m, algo):
+    """Reject, at swap time, picks that cannot run whatever the input shape."""
+    if algo in ("torch", "default"):
+        return
+    if m.padding_mode != "zeros":
+        raise ValueError("%s: padding_mode=%r is not supported (zero padding only)" % (name, m.padding_mode))
+    if algo == "winograd":
+        if tuple(m.kernel_size) != (3, 3) or tuple(m.stride) != (1, 1) or tuple(m.dilation) != (1, 1) \
+                or m.groups != 1:
+            raise ValueError("%s: winograd F(2x2,3x3) needs a 3x3 filter, stride 1, dilation 1 and groups 1"
+                             % name)
+
+
+class Conv2dSwap(nn.Module):
+    """Slim replacement of an nn.Conv2d whose forward calls the HIP library
+    with the algorithm the shared ``AlgoTable`` holds for this module."""
+
+    def __init__(self, conv, table, name):
+        super().__init__()
+        self.in_channels, self.out_channels = conv.in_channels, conv.out_channels
+        self.kernel_size, self.stride, self.dilation = conv.kernel_size, conv.stride, conv.dilation
+        self.padding = _padding_pair(conv) if conv.padding_mode == "zeros" else conv.padding
+        self.groups, self.padding_mode = conv.groups, conv.padding_mode
+        self.weight = conv.weight
+        self.bias = conv.bias
+        self.table = table
+        self.name = name
+        # The original module serves the "torch" choice.  It is kept out of
+        # the module tree (its parameters are this module's parameters), so
+        # it is neither listed again as a Conv2d nor moved twice.
+        object.__setattr__(self, "_torch_conv", conv)
+
+    @property
+    def algo(self):
+        return self.table.get_algo(self.name)
+
+    def forward(self, x):
+        algo = self.algo
+        if algo == "torch":
+            return self._torch_conv(x)
+        return conv2d(x, self.weight, self.bias, self.stride, self.padding, self.dilation, self.groups, algo=algo)
+
+    def extra_repr(self):
+        return "%d, %d, kernel_size=%s, stride=%s, padding=%s, groups=%d, algo=%s" % (
+            self.in_channels, self.out_channels, self.kernel_size, self.stride, self.padding, self.groups, self.algo)
+
+
+def _set_submodule(model, name, new):
+    parent = model
+    parts = name.split(".")
+    for p in parts[:-1]:
+        parent = getattr(parent, p)
+    setattr(parent, parts[-1], new)
+
+
+def swap_conv2d(model, selector="default"):
+    """Replace every nn.Conv2d of ``model`` in place; return the AlgoTable.
+
+    Modules already swapped are re-pointed at the new table.
+    """
+    all_convs = [(n, m) for n, m in model.named_modules() if isinstance(m, (nn.Conv2d, Conv2dSwap))]
+    if isinstance(selector, (list, tuple)) and len(selector) != len(all_convs):
+        raise ValueError("selector list has %d entries but the model has %d Conv2d modules"
+                         % (len(selector), len(all_convs)))
+    table = AlgoTable()
+    for idx, (name, m) in enumerate(all_convs):
+        base = m._torch_conv if isinstance(m, Conv2dSwap) else m
+        if isinstance(selector, str):
+            algo = selector
+        elif isinstance(selector, (list, tuple)):
+            algo = selector[idx]
+        elif isinstance(selector, dict):
+            algo = selector.get(name, "default")
+        elif callable(selector):
+            algo = selector(base)
+        else:
+            raise ValueError("selector must be a name, a list of names, a callable or a table")
+        algo = _canonical(algo)
+        _static_check(name, base, algo)
+        table[name] = algo
+    for name, m in all_convs:
+        if isinstance(m, Conv2dSwap):
+            m.table = table
+        else:
+            # Modules left on "torch" are wrapped too: the wrapper runs the
+            # original module while the table says "torch", so a later table
+            # edit can still move them to the library.
+            _set_submodule(model, name, Conv2dSwap(m, table, name))
+    return table
+
+
+def supported_algos(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, relu=False):
+    """Concrete algorithms the library accepts for this layer."""
+    from .conv import _desc_for
+    desc = _desc_for(x, w, b, stride, padding, dilation, groups, relu)
+    return [a for a in CONCRETE_ALGOS if _lib.check(desc, a) == _lib.CONV_OK]
+
+
+def time_conv(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, algo="default", relu=False,
+              warmup=2, reps=5):
+    """Median milliseconds per call (HIP events on the current stream)."""
+    out = conv2d(x, w, b, stride, padding, dilation, groups, algo=algo, relu=relu)
+    for _ in range(warmup):
+        conv2d(x, w, b, stride, padding, dilation, groups, algo=algo, relu=relu, out=out)
+    times = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        conv2d(x, w, b, stride, padding, dilation, groups, algo=algo, relu=relu, out=out)
+        e1.record()
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1))
+    times.sort()
+    return times[len(times) // 2]
+
+
+def select_fastest(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, relu=False, algos=None,
+                   warmup=2, reps=5):
+    """(fastest algorithm, {algorithm: median ms}) over the supported ones."""
+    cands = supported_algos(x, w, b, stride, padding, dilation, groups, relu)
+    if algos is not None:
+        cands = [a for a in cands if a in algos]
+    timings = {a: time_conv(x, w, b, stride, padding, dilation, groups, a, relu, warmup, reps) for a in cands}
+    best = min(timings, key=timings.get)
+    return best, timings
+
+
+def tune(model, example_input, table=None, warmup=2, reps=5):
+    """Measured per-layer selection on a swapped model: capture every
+    Conv2dSwap's input with one forward pass, time each supported algorithm
+    on it and write the fastest into the table.  Returns the table."""
+    mods = [(n, m) for n, m in model.named_modules() if isinstance(m, Conv2dSwap)]
+    if table is None:
+        table = mods[0][1].table if mods else AlgoTable()
+    captured = {}
+    hooks = [m.register_forward_pre_hook(lambda mod, inp, n=n: captured.__setitem__(n, inp[0]))
+             for n, m in mods]
+    try:
+        with torch.no_grad():
+            model(example_input)
+    finally:
+        for h in hooks:
+            h.remove()
+    with torch.no_grad():
+        for n, m in mods:
+            if n not in captured or table.get_algo(n) == "torch":
+                continue
+            best, _ = select_fastest(captured[n], m.weight, m.bias, m.stride, m.padding, m.dilation, m.groups,
+                                     warmup=warmup, reps=reps)
+            table[n] = best
+    return table

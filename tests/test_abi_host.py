@@ -1,0 +1,153 @@
+"""Host-side checks of the C ABI: the library loads, exports what the header
+declares, and rejects bad arguments before touching any device.  None of
+these tests launches a kernel."""
+import os
+import re
+
+import pytest
+import torch
+
+import oracle
+from paper_2410_08300_amd import _lib
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "convsel.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(conv2d[a-z_0-9]*)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = header_functions()
+    assert "conv2d" in names and len(names) >= 10
+    L = _lib.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(_lib.EXPORTED) == names
+
+
+def test_desc_struct_matches_header_layout():
+    import ctypes
+    assert ctypes.sizeof(_lib.Desc) == 7 * 8 + 10 * 4
+
+
+def test_algo_names_round_trip():
+    for name, v in _lib.ALGOS.items():
+        assert _lib.algo_id(name) == v
+        assert _lib.algo_name(v) == name
+    assert _lib.algo_id("gemm") == _lib.ALGOS["im2col_gemm"]
+    with pytest.raises(ValueError):
+        _lib.algo_id("smm")
+    assert _lib.algo_name(99) == "unknown"
+    assert _lib.status_string(0) == "ok" and _lib.status_string(42) == "unknown"
+
+
+def test_output_shape_matches_formula():
+    import itertools
+    for H, R, st, pd, dl in itertools.product([1, 5, 7, 32], [1, 3, 5], [1, 2, 3], [0, 1, 2], [1, 2]):
+        P, Q = oracle.output_size(H, H + 1, R, R, st, pd, dl)
+        d = _lib.make_desc(2, 4, H, H + 1, 8, R, R, st, pd, dl)
+        if P < 1 or Q < 1:
+            assert _lib.check(d, "direct") == _lib.CONV_ERR_INVALID_ARG
+        else:
+            assert _lib.output_shape(d) == (P, Q)
+
+
+@pytest.mark.parametrize("kw", [dict(c=0), dict(h=0), dict(k=-1), dict(r=0), dict(groups=3), dict(stride=0),
+                                dict(dilation=0), dict(padding=-1), dict(c=6, groups=4), dict(k=10, groups=4),
+                                dict(h=2, r=5)])
+def test_invalid_descriptors(kw):
+    base = dict(n=2, c=8, h=9, w=9, k=12, r=3, s=3, stride=1, padding=1, dilation=1, groups=2)
+    base.update(kw)
+    if "r" in kw:
+        base["s"] = kw["r"]
+    d = _lib.make_desc(base["n"], base["c"], base["h"], base["w"], base["k"], base["r"], base["s"],
+                       base["stride"], base["padding"], base["dilation"], base["groups"])
+    for a in _lib.ALGOS:
+        assert _lib.check(d, a) == _lib.CONV_ERR_INVALID_ARG
+    with pytest.raises(_lib.Conv2dError):
+        _lib.output_shape(d)
+
+
+def test_bad_dtype_and_flags():
+    d = _lib.make_desc(1, 4, 8, 8, 4, 3, 3)
+    d.dtype = 7
+    assert _lib.check(d, "direct") == _lib.CONV_ERR_INVALID_ARG
+    d = _lib.make_desc(1, 4, 8, 8, 4, 3, 3)
+    d.fuse_relu = 2
+    assert _lib.check(d, "direct") == _lib.CONV_ERR_INVALID_ARG
+    assert _lib.check(_lib.make_desc(1, 4, 8, 8, 4, 3, 3), 17) == _lib.CONV_ERR_INVALID_ARG
+
+
+def test_oversized_tensors_rejected():
+    d = _lib.make_desc(1 << 20, 1024, 64, 64, 8, 1, 1)
+    assert _lib.check(d, "direct") == _lib.CONV_ERR_INVALID_ARG
+
+
+def test_winograd_support_matrix():
+    ok = _lib.make_desc(2, 8, 9, 9, 8, 3, 3, 1, 1, 1, 1)
+    assert _lib.check(ok, "winograd") == _lib.CONV_OK
+    for kw in [dict(r=5), dict(stride=2), dict(dilation=2), dict(groups=2), dict(r=1)]:
+        args = dict(r=3, stride=1, dilation=1, groups=1)
+        args.update(kw)
+        d = _lib.make_desc(2, 8, 9, 9, 8, args["r"], args["r"], args["stride"], 1, args["dilation"], args["groups"])
+        assert _lib.check(d, "winograd") == _lib.CONV_ERR_UNSUPPORTED
+        for a in ("direct", "implicit_gemm", "im2col_gemm"):
+            assert _lib.check(d, a) == _lib.CONV_OK
+
+
+def test_workspace_sizes():
+    d = _lib.make_desc(4, 6, 10, 12, 8, 3, 3, 2, 1, 1, 2, "bf16")
+    P, Q = _lib.output_shape(d)
+    assert _lib.workspace_bytes(d, "direct") == 0
+    assert _lib.workspace_bytes(d, "implicit_gemm") == 0
+    assert _lib.workspace_bytes(d, "im2col_gemm") == 4 * 2 * P * Q * 3 * 9 * 2
+    w = _lib.make_desc(3, 16, 7, 7, 8, 3, 3, 1, 1, 1, 1, "f32")
+    T = 3 * 4 * 4
+    u = 16 * 8 * 16 * 4
+    v_off = (u + 255) // 256 * 256
+    m_off = (v_off + 16 * T * 16 * 4 + 255) // 256 * 256
+    assert _lib.workspace_bytes(w, "winograd") == m_off + 16 * 8 * T * 4
+    # the column matrix is batched near 1 GiB: one 112x112 image of a 512-channel 3x3 bf16 layer
+    big = _lib.make_desc(128, 512, 112, 112, 256, 3, 3, 1, 1, 1, 1, "bf16")
+    per_img = 112 * 112 * 512 * 9 * 2
+    assert _lib.workspace_bytes(big, "im2col_gemm") == (1 << 30) // per_img * per_img
+    assert _lib.workspace_bytes(_lib.make_desc(0, 4, 8, 8, 4, 3, 3), "im2col_gemm") == 0
+
+
+def test_default_rule():
+    assert _lib.default_algo(_lib.make_desc(2, 32, 16, 16, 32, 3, 3, 1, 1, 1, 32)) == "direct"
+    assert _lib.default_algo(_lib.make_desc(2, 32, 16, 16, 64, 3, 3, 1, 1, 1, 1)) == "implicit_gemm"
+
+
+def test_argument_errors_before_any_device_call():
+    d = _lib.make_desc(1, 4, 8, 8, 4, 3, 3, 1, 1, 1, 1, "f32", bias=True)
+    A, B, Bb, Y = 1 << 20, 2 << 20, 3 << 20, 4 << 20
+    # NULL input / weight / output, bias presence mismatch
+    assert _lib.conv2d_raw(None, B, Bb, Y, d, "direct", None, 0, None) == _lib.CONV_ERR_INVALID_ARG
+    assert _lib.conv2d_raw(A, None, Bb, Y, d, "direct", None, 0, None) == _lib.CONV_ERR_INVALID_ARG
+    assert _lib.conv2d_raw(A, B, Bb, None, d, "direct", None, 0, None) == _lib.CONV_ERR_INVALID_ARG
+    assert _lib.conv2d_raw(A, B, None, Y, d, "direct", None, 0, None) == _lib.CONV_ERR_INVALID_ARG
+    # output overlapping the input
+    assert _lib.conv2d_raw(A, B, Bb, A + 64, d, "direct", None, 0, None) == _lib.CONV_ERR_INVALID_ARG
+    # workspace too small
+    need = _lib.workspace_bytes(d, "winograd")
+    assert _lib.conv2d_raw(A, B, Bb, Y, d, "winograd", 5 << 20, need - 1, None) == _lib.CONV_ERR_WORKSPACE
+    assert _lib.conv2d_raw(A, B, Bb, Y, d, "winograd", None, need, None) == _lib.CONV_ERR_WORKSPACE
+    # output overlapping the workspace
+    assert _lib.conv2d_raw(A, B, Bb, Y, d, "winograd", Y + 16, need, None) == _lib.CONV_ERR_INVALID_ARG
+    # unsupported algorithm for the shape
+    d5 = _lib.make_desc(1, 4, 8, 8, 4, 5, 5, 1, 2, 1, 1, "f32", bias=True)
+    assert _lib.conv2d_raw(A, B, Bb, Y, d5, "winograd", None, 0, None) == _lib.CONV_ERR_UNSUPPORTED
+    # an empty batch is a no-op, even with NULL buffers
+    d0 = _lib.make_desc(0, 4, 8, 8, 4, 3, 3, 1, 1, 1, 1, "f32")
+    assert _lib.conv2d_raw(None, None, None, None, d0, "direct", None, 0, None) == _lib.CONV_OK
+
+
+@pytest.mark.skipif(torch.cuda.device_count() > 0, reason="checks the no-device path; a GPU is present")
+def test_valid_call_without_device_reports_device_error():
+    d = _lib.make_desc(1, 4, 8, 8, 4, 3, 3, 1, 1, 1, 1, "f32")
+    assert _lib.conv2d_raw(1 << 20, 2 << 20, None, 4 << 20, d, "direct", None, 0, None) == _lib.CONV_ERR_DEVICE
+    assert _lib.im2col_raw(1 << 20, 4 << 20, d, None) == _lib.CONV_ERR_DEVICE

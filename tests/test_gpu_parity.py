@@ -1,0 +1,174 @@
+"""GPU parity: every algorithm of the HIP library against the fp64 CPU oracle
+on the same seeded inputs (full outputs at small sizes, sampled outputs at
+the workloads' full sizes), plus the intermediate buffers of IM2COL and
+Winograd, determinism and edge cases."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2410_08300_amd as cs
+from paper_2410_08300_amd import workloads as W
+from gpu_util import ALGOS, tolerance, rel_err, f64, supports, say
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+DEV = torch.device("cuda:0")
+TDT = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def check_full(x, w, b, stride, padding, dilation, groups, relu, algos, label):
+    """Run each algorithm on the GPU and compare the whole output."""
+    ref = oracle.conv2d(f64(x), f64(w), f64(b), stride, padding, dilation, groups, relu)
+    R, S = w.shape[2], w.shape[3]
+    xd, wd = x.to(DEV), w.to(DEV)
+    bd = None if b is None else b.to(DEV)
+    for algo in algos:
+        if not supports(algo, R, S, stride, dilation, groups):
+            continue
+        say("case", label, algo)
+        y = cs.conv2d(xd, wd, bd, stride, padding, dilation, groups, algo=algo, relu=relu)
+        torch.cuda.synchronize()
+        assert y.shape == ref.shape
+        err = rel_err(f64(y), ref)
+        tol = tolerance(x.dtype, algo)
+        assert err <= tol, "%s %s: rel err %.3e > %.0e" % (label, algo, err, tol)
+
+
+def test_toy_layer_all_algorithms():
+    L = W.toy()[0]
+    x, w, b = W.make_tensors(L, (0, 0))
+    check_full(x, w, b, 1, 1, 1, 1, False, ALGOS, "toy")
+
+
+def sweep_cases(count, seed):
+    rng = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < count:
+        R = int(rng.choice([1, 2, 3, 3, 3, 5]))
+        S = R if rng.random() < 0.8 else int(rng.choice([1, 3]))
+        st = (int(rng.integers(1, 4)), int(rng.integers(1, 4))) if rng.random() < 0.3 else int(rng.choice([1, 1, 2]))
+        pd = (int(rng.integers(0, 3)), int(rng.integers(0, 3))) if rng.random() < 0.3 else int(rng.integers(0, 3))
+        dl = int(rng.choice([1, 1, 1, 2]))
+        G = int(rng.choice([1, 1, 1, 2, 4]))
+        Cg = int(rng.choice([1, 3, 8, 13, 16, 24, 40]))
+        Kg = int(rng.choice([1, 5, 32, 64, 70, 130]))
+        if G > 1:
+            Kg = min(Kg, 40)
+        N = int(rng.integers(1, 4))
+        H, Wd = int(rng.integers(1, 34)), int(rng.integers(1, 34))
+        P, Q = oracle.output_size(H, Wd, R, S, st, pd, dl)
+        if P < 1 or Q < 1:
+            continue
+        dtype = "bf16" if rng.random() < 0.5 else "f32"
+        bias = bool(rng.random() < 0.5)
+        relu = bool(rng.random() < 0.3)
+        cases.append((N, Cg * G, H, Wd, Kg * G, R, S, st, pd, dl, G, dtype, bias, relu))
+    return cases
+
+
+@pytest.mark.parametrize("case", sweep_cases(48, 2024), ids=lambda c: "x".join(map(str, c[:7])) + "_" + c[11])
+def test_random_shape_sweep(case):
+    N, C, H, Wd, K, R, S, st, pd, dl, G, dtype, bias, relu = case
+    g = torch.Generator().manual_seed(hash(case) & 0xffffffff)
+    x = torch.randn(N, C, H, Wd, generator=g).to(TDT[dtype])
+    w = (torch.randn(K, C // G, R, S, generator=g) * (2.0 / ((C // G) * R * S)) ** 0.5).to(TDT[dtype])
+    b = (torch.randn(K, generator=g) * 0.1).to(TDT[dtype]) if bias else None
+    check_full(x, w, b, st, pd, dl, G, relu, ALGOS, str(case))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_winograd_odd_sizes_and_padding(dtype):
+    g = torch.Generator().manual_seed(5)
+    for (N, C, H, Wd, K, pad) in [(2, 16, 7, 7, 24, 1), (1, 9, 5, 8, 40, 0), (3, 33, 14, 13, 70, 2),
+                                  (1, 64, 28, 28, 64, 1), (1, 8, 1, 1, 8, 1)]:
+        x = torch.randn(N, C, H, Wd, generator=g).to(TDT[dtype])
+        w = (torch.randn(K, C, 3, 3, generator=g) / (3 * C ** 0.5)).to(TDT[dtype])
+        b = (torch.randn(K, generator=g) * 0.1).to(TDT[dtype])
+        check_full(x, w, b, 1, pad, 1, 1, False, ["winograd"], "wino%s" % ((N, C, H, Wd, K, pad),))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_im2col_buffer_is_bit_exact(dtype):
+    g = torch.Generator().manual_seed(6)
+    for (N, C, H, Wd, R, S, st, pd, dl, G) in [(2, 3, 9, 11, 3, 3, 1, 1, 1, 1), (1, 8, 12, 7, 5, 3, 2, (2, 1), 1, 2),
+                                               (2, 6, 10, 10, 3, 3, (1, 2), 2, 2, 3), (1, 4, 5, 5, 1, 1, 1, 0, 1, 4)]:
+        x = torch.randn(N, C, H, Wd, generator=g).to(TDT[dtype])
+        say("case im2col", dtype, (N, C, H, Wd, R, S, st, pd, dl, G))
+        col = cs.im2col(x.to(DEV), (R, S), st, pd, dl, G)
+        torch.cuda.synchronize()
+        ref = oracle.im2col(f64(x), R, S, st, pd, dl, G)
+        assert col.shape == ref.shape
+        assert np.array_equal(f64(col), ref)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_winograd_transforms_match_oracle(dtype):
+    g = torch.Generator().manual_seed(7)
+    x = torch.randn(2, 24, 9, 10, generator=g).to(TDT[dtype])
+    w = torch.randn(16, 24, 3, 3, generator=g).to(TDT[dtype])
+    say("case winograd transforms", dtype)
+    U = cs.winograd_filter_transform(w.to(DEV))
+    V = cs.winograd_input_transform(x.to(DEV), padding=1)
+    torch.cuda.synchronize()
+    Uo = oracle.winograd_filter_transform(f64(w)).reshape(16, 16, 24)
+    Vo = oracle.winograd_input_transform(f64(x), padding=1).reshape(16, -1, 24)
+    # Relative to each buffer's largest entry: fp32 carries only the rounding
+    # of a few adds (< 1e-6); bf16 adds one rounding of each result (2^-8).
+    tol = 1e-6 if dtype == "f32" else 2.0 ** -8
+    eu, ev = rel_err(f64(U), Uo), rel_err(f64(V), Vo)
+    assert eu <= tol, "U rel err %.3e" % eu
+    assert ev <= tol, "V rel err %.3e" % ev
+
+
+def test_reruns_are_bit_identical():
+    g = torch.Generator().manual_seed(8)
+    x = torch.randn(4, 64, 20, 20, generator=g).to(DEV, torch.bfloat16)
+    w = torch.randn(96, 64, 3, 3, generator=g).to(DEV, torch.bfloat16)
+    for algo in ALGOS:
+        say("case determinism", algo)
+        a = cs.conv2d(x, w, None, 1, 1, algo=algo)
+        b = cs.conv2d(x, w, None, 1, 1, algo=algo)
+        torch.cuda.synchronize()
+        assert torch.equal(a, b)
+
+
+def test_edge_cases():
+    g = torch.Generator().manual_seed(9)
+    # empty batch: no-op
+    x = torch.empty(0, 4, 8, 8, device=DEV)
+    w = torch.randn(4, 4, 3, 3, generator=g).to(DEV)
+    for algo in ALGOS:
+        say("case empty batch", algo)
+        y = cs.conv2d(x, w, None, 1, 1, algo=algo)
+        assert y.shape == (0, 4, 8, 8)
+    # 1x1 image with large padding; output larger than input
+    x = torch.randn(2, 5, 1, 1, generator=g)
+    w = torch.randn(7, 5, 3, 3, generator=g)
+    check_full(x, w, None, 1, 2, 1, 1, False, ALGOS, "1x1 image pad 2")
+    # single output pixel, single channels
+    x = torch.randn(1, 1, 3, 3, generator=g)
+    w = torch.randn(1, 1, 3, 3, generator=g)
+    check_full(x, w, torch.randn(1, generator=g), 1, 0, 1, 1, True, ALGOS, "1x1 output")
+    # many output channels: several 128-row tiles plus a ragged tail
+    x = torch.randn(1, 32, 6, 7, generator=g).to(torch.bfloat16)
+    w = (torch.randn(300, 32, 3, 3, generator=g) * 0.1).to(torch.bfloat16)
+    check_full(x, w, None, 1, 1, 1, 1, False, ALGOS, "K=300")
+    # non-contiguous input
+    xt = torch.randn(2, 9, 12, 8, generator=g).transpose(2, 3)
+    check_full(xt.contiguous(), torch.randn(6, 9, 3, 3, generator=g), None, 1, 1, 1, 1, False, ALGOS, "strided")
+    yd = cs.conv2d(xt.to(DEV), torch.randn(6, 9, 3, 3, generator=g).to(DEV), None, 1, 1)
+    assert yd.shape == (2, 6, 8, 12)
+
+
+def test_unsupported_and_invalid_calls_raise():
+    x = torch.randn(1, 4, 8, 8, device=DEV)
+    with pytest.raises(cs.Conv2dError):
+        cs.conv2d(x, torch.randn(4, 4, 5, 5, device=DEV), None, 1, 2, algo="winograd")
+    with pytest.raises(ValueError):
+        cs.conv2d(x, torch.randn(4, 3, 3, 3, device=DEV))
+    with pytest.raises(ValueError):
+        cs.conv2d(x, torch.randn(4, 4, 3, 3, device=DEV, dtype=torch.bfloat16))

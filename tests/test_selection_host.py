@@ -1,0 +1,124 @@
+"""Selector semantics of swap_conv2d / AlgoTable (paper, Sec. IV) on the CPU.
+
+The HIP call is replaced by a fake backend that evaluates the CPU oracle, so
+the swap mechanics are tested without a GPU; the GPU tests run the same
+models through the real library."""
+import numpy as np
+import pytest
+import torch
+from torch import nn
+
+import oracle
+import paper_2410_08300_amd as cs
+from paper_2410_08300_amd import selection
+
+
+class ConvNet(nn.Module):
+    """The toy network of the paper's Listing 1 (two 3x3 convolutions)."""
+
+    def __init__(self):
+        super().__init__()
+        self.conv1 = nn.Conv2d(3, 16, 3, padding=1)
+        self.maxpool = nn.MaxPool2d(2, 2)
+        self.conv2 = nn.Conv2d(16, 32, 3, padding=1)
+
+    def forward(self, x):
+        x = torch.relu(self.conv1(x))
+        x = self.maxpool(x)
+        x = torch.relu(self.conv2(x))
+        return torch.flatten(x, 1)
+
+
+class Deep(nn.Module):
+    def __init__(self):
+        super().__init__()
+        self.stem = nn.Conv2d(3, 8, 5, padding=2)
+        self.block = nn.Sequential(nn.Conv2d(8, 8, 3, padding=1, groups=8), nn.ReLU(), nn.Conv2d(8, 12, 1))
+
+    def forward(self, x):
+        return self.block(self.stem(x))
+
+
+@pytest.fixture
+def fake_backend(monkeypatch):
+    calls = []
+
+    def fake(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, algo="default", relu=False, out=None):
+        calls.append(algo)
+        y = oracle.conv2d(x.detach().double().numpy(), w.detach().double().numpy(),
+                          None if b is None else b.detach().double().numpy(), stride, padding, dilation, groups,
+                          relu)
+        return torch.from_numpy(y).to(x.dtype)
+
+    monkeypatch.setattr(selection, "conv2d", fake)
+    return calls
+
+
+def test_single_name_list_and_callable(fake_backend):
+    torch.manual_seed(0)
+    m = ConvNet()
+    x = torch.randn(2, 3, 16, 16)
+    ref = m(x)
+    t = cs.swap_conv2d(m, "direct")
+    assert list(t.items()) == [("conv1", "direct"), ("conv2", "direct")]
+    assert torch.allclose(m(x), ref, atol=1e-5)
+    t = cs.swap_conv2d(m, ["implicit_gemm", "gemm"])
+    assert list(t.values()) == ["implicit_gemm", "im2col_gemm"]
+    fake_backend.clear()
+    assert torch.allclose(m(x), ref, atol=1e-5)
+    assert fake_backend == ["implicit_gemm", "im2col_gemm"]
+    t = cs.swap_conv2d(m, lambda conv: "winograd" if conv.in_channels > 8 else "direct")
+    assert list(t.values()) == ["direct", "winograd"]
+
+
+def test_table_edit_changes_algorithm_without_reswapping(fake_backend):
+    m = ConvNet()
+    t = cs.swap_conv2d(m, "direct")
+    x = torch.randn(1, 3, 8, 8)
+    t.set("conv2", "winograd")
+    fake_backend.clear()
+    m(x)
+    assert fake_backend == ["direct", "winograd"]
+    t2 = cs.AlgoTable.from_json(t.to_json())
+    assert t2 == t
+
+
+def test_torch_choice_keeps_pytorch_module(fake_backend):
+    torch.manual_seed(1)
+    m = Deep()
+    x = torch.randn(2, 3, 9, 9)
+    ref = m(x)
+    t = cs.swap_conv2d(m, ["torch", "direct", "default"])
+    assert list(t.values()) == ["torch", "direct", "default"]
+    fake_backend.clear()
+    assert torch.allclose(m(x), ref, atol=1e-5)
+    assert fake_backend == ["direct", "default"]
+
+
+def test_dict_selector_and_reswap():
+    m = Deep()
+    t = cs.swap_conv2d(m, {"block.2": "im2col_gemm"})
+    assert t["stem"] == "default" and t["block.0"] == "default" and t["block.2"] == "im2col_gemm"
+    t2 = cs.swap_conv2d(m, "direct")
+    assert all(v == "direct" for v in t2.values())
+    assert all(mod.table is t2 for _, mod in m.named_modules() if isinstance(mod, cs.Conv2dSwap))
+
+
+def test_selector_errors():
+    with pytest.raises(ValueError):
+        cs.swap_conv2d(ConvNet(), ["direct"])                 # list length mismatch
+    with pytest.raises(ValueError):
+        cs.swap_conv2d(ConvNet(), "smm")                      # unknown name
+    with pytest.raises(ValueError):
+        cs.swap_conv2d(Deep(), "winograd")                    # 5x5 stem cannot use F(2x2,3x3)
+    with pytest.raises(ValueError):
+        cs.swap_conv2d(Deep(), lambda c: 42)
+    m = nn.Sequential(nn.Conv2d(3, 4, 3, padding=1, padding_mode="reflect"))
+    with pytest.raises(ValueError):
+        cs.swap_conv2d(m, "direct")
+    assert cs.swap_conv2d(m, "torch")["0"] == "torch"
+
+
+def test_cpu_tensors_are_refused():
+    with pytest.raises(ValueError):
+        cs.conv2d(torch.randn(1, 3, 8, 8), torch.randn(4, 3, 3, 3))
