@@ -96,6 +96,32 @@ __device__ __forceinline__ bf16_t vec16_get<bf16_t>(const vec16& v, int i) {
   return r;
 }
 
+// Raw bits of one element, zero-extended to 32 bits.
+__device__ __forceinline__ uint32_t load_bits(const float* p) { return __float_as_uint(*p); }
+__device__ __forceinline__ uint32_t load_bits(const bf16_t* p) {
+  return static_cast<uint32_t>(*reinterpret_cast<const uint16_t*>(p));
+}
+
+// Packs per16 element bit patterns (low bits of each word) into 16 bytes.
+template <typename T>
+__device__ __forceinline__ void pack16(vec16& v, const uint32_t* e);
+
+template <>
+__device__ __forceinline__ void pack16<float>(vec16& v, const uint32_t* e) {
+  v.d[0] = e[0];
+  v.d[1] = e[1];
+  v.d[2] = e[2];
+  v.d[3] = e[3];
+}
+
+template <>
+__device__ __forceinline__ void pack16<bf16_t>(vec16& v, const uint32_t* e) {
+  v.d[0] = e[0] | (e[1] << 16);
+  v.d[1] = e[2] | (e[3] << 16);
+  v.d[2] = e[4] | (e[5] << 16);
+  v.d[3] = e[6] | (e[7] << 16);
+}
+
 __device__ __forceinline__ vec16 vec16_zero() {
   vec16 v;
   v.d[0] = v.d[1] = v.d[2] = v.d[3] = 0u;

@@ -44,6 +44,32 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_kernel(GemmArgs g, int batch
 
   vec16 ra[UA], rb[UB];
 
+  // One 16-byte unit (UE consecutive reduction elements) of row `row` of a
+  // row-major operand, zero outside rows < nrows and k < Kred.  Loads are
+  // unconditional from a valid address and masked afterwards, so a thread's
+  // loads are all in flight together.
+  auto load_unit = [&](const T* base, int row, int k, int nrows, int64_t ld) -> vec16 {
+    if (VEC) {
+      const bool ok = row < nrows && k < g.Kred;
+      const vec16 v = load16(base + (ok ? row * ld + k : 0));
+      vec16 r;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) r.d[i] = ok ? v.d[i] : 0u;
+      return r;
+    } else {
+      uint32_t e[UE];
+#pragma unroll
+      for (int i = 0; i < UE; ++i) {
+        const bool ok = row < nrows && k + i < g.Kred;
+        const uint32_t bits = load_bits(base + (ok ? row * ld + k + i : 0));
+        e[i] = ok ? bits : 0u;
+      }
+      vec16 r;
+      pack16<T>(r, e);
+      return r;
+    }
+  };
+
   auto fetch = [&](int kt) {
     const int k0 = kt * BK;
 #pragma unroll
@@ -51,38 +77,14 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_kernel(GemmArgs g, int batch
       const int id = tid + u * kThreads;
       const int row = id / UPR, kc = (id % UPR) * UE;
       const int gi = i0 + row, gk = k0 + kc;
-      if (VEC) {
-        ra[u] = (gi < g.M && gk < g.Kred) ? load16(A + gi * g.lda + gk) : vec16_zero();
-      } else {
-        vec16 v = vec16_zero();
-#pragma unroll
-        for (int e = 0; e < UE; ++e) {
-          T val;
-          if (gi < g.M && gk + e < g.Kred) val = A[gi * g.lda + gk + e];
-          else val = elem<T>::from_f32(0.f);
-          vec16_set<T>(v, e, val);
-        }
-        ra[u] = v;
-      }
+      ra[u] = load_unit(A, gi, gk, g.M, g.lda);
     }
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
       const int id = tid + u * kThreads;
       const int row = id / UPR, kc = (id % UPR) * UE;
       const int gj = j0 + row, gk = k0 + kc;
-      if (VEC) {
-        rb[u] = (gj < g.N && gk < g.Kred) ? load16(B + gj * g.ldb + gk) : vec16_zero();
-      } else {
-        vec16 v = vec16_zero();
-#pragma unroll
-        for (int e = 0; e < UE; ++e) {
-          T val;
-          if (gj < g.N && gk + e < g.Kred) val = B[gj * g.ldb + gk + e];
-          else val = elem<T>::from_f32(0.f);
-          vec16_set<T>(v, e, val);
-        }
-        rb[u] = v;
-      }
+      rb[u] = load_unit(B, gj, gk, g.N, g.ldb);
     }
   };
   auto stash = [&]() {

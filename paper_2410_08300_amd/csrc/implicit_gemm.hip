@@ -64,15 +64,21 @@ __device__ __forceinline__ int vrow_of(int j, const IgArgs& a) {
   return n * a.Hv + (pq / a.Q) * a.sh;
 }
 
+// Halo items per thread whose global offsets are computed once per
+// workgroup and whose data are prefetched into registers; items beyond
+// kImax * 256 (very wide images) are staged on the fly.
+constexpr int kImax = 4;
+
 template <typename T, int BM, int NG, int RST>
 __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
   constexpr int UE = elem<T>::per16;
   constexpr int Cc = UE * NG;
   constexpr int MI = BM / 64, NJ = BN / 64;
+  static_assert(BM * NG <= kThreads, "one filter item per thread");
   extern __shared__ __align__(16) vec16 smem[];
   vec16* As = smem;                         // [BM][UR]
   vec16* Xs = smem + BM * a.UR;             // [VR*Wv][PS]
-  int* utab = reinterpret_cast<int*>(Xs + a.xs_units);  // [2*steps]: Xs unit offset per unit
+  int* utab = reinterpret_cast<int*>(Xs + a.xs_units);  // runtime-tap path only
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -83,17 +89,22 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
   const int RS = a.R * a.S;
   const int jl = min(j0 + BN, a.NPQ) - 1;
   const int vr_lo = vrow_of(j0, a);
+  const int HW = a.H * a.W;
 
-  // Unit table: unit u = tap*NG + cg -> Xs offset (tap offset * PS + cg).
-  for (int u = tid; u < 2 * a.steps; u += kThreads) {
-    int off = 0;
-    if (u < a.units) {
-      const int tap = u / NG, cg = u - tap * NG;
-      const int r = tap / a.S, s = tap - r * a.S;
-      off = (r * a.dh * a.Wv + s * a.dw) * a.PS + cg;
+  if constexpr (RST == 0) {
+    for (int u = tid; u < 2 * a.steps; u += kThreads) {
+      int off = 0;
+      if (u < a.units) {
+        const int tap = u / NG, cg = u - tap * NG;
+        const int r = tap / a.S, s = tap - r * a.S;
+        off = (r * a.dh * a.Wv + s * a.dw) * a.PS + cg;
+      }
+      utab[u] = off;
     }
-    utab[u] = off;
   }
+  // The padding unit of an odd unit count holds zero filters (never rewritten).
+  if (a.units & 1)
+    for (int i = tid; i < BM; i += kThreads) As[i * a.UR + a.units] = vec16_zero();
 
   // Per-lane pixel offsets into the halo and output base offsets.
   int pofs[NJ];
@@ -112,10 +123,138 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
       ybase[nj] = static_cast<int64_t>(n) * a.K * PQ + pq;
     }
   }
+  // Tap offsets in the halo (compile-time tap count only).
+  int tapoff[RST > 0 ? RST : 1];
+#pragma unroll
+  for (int t = 0; t < (RST > 0 ? RST : 1); ++t) {
+    const int r = t / a.S, s = t - r * a.S;
+    tapoff[t] = (r * a.dh * a.Wv + s * a.dw) * a.PS;
+  }
 
   const T* x = reinterpret_cast<const T*>(a.x);
   const T* w = reinterpret_cast<const T*>(a.w) + static_cast<int64_t>(g * a.Kg + k0) * a.Cg * RS;
-  const int64_t HW = static_cast<int64_t>(a.H) * a.W;
+
+  // Halo item it = pix * NG + cg, pix = vrow * Wv + vcol.  goff: element
+  // offset of (image, row, column) in channel 0 of this group, or -1 where
+  // the item reads padding (or does not exist).
+  const int nitems = a.VR * a.Wv * NG;
+  auto item_goff = [&](int it) -> int {
+    if (it >= nitems) return -1;
+    const int pix = it / NG;
+    const int vr = pix / a.Wv, vc = pix - vr * a.Wv;
+    const int v = vr_lo + vr;
+    const int n = v / a.Hv;
+    const int ih = v - n * a.Hv - a.ph, iw = vc - a.pw;
+    if (n >= a.N || ih < 0 || ih >= a.H || iw < 0 || iw >= a.W) return -1;
+    return (n * a.C + g * a.Cg) * HW + ih * a.W + iw;
+  };
+  // gaddr: always a valid element offset (padding items read element 0);
+  // gvalid marks the items whose values are kept.
+  int gaddr[kImax];
+  bool gvalid[kImax];
+#pragma unroll
+  for (int t = 0; t < kImax; ++t) {
+    const int go = item_goff(tid + t * kThreads);
+    gvalid[t] = go >= 0;
+    gaddr[t] = go >= 0 ? go : 0;
+  }
+
+  // Branch-free gather of UE channels at one halo position: every lane
+  // loads from a valid address (element 0 stands in for padding and for
+  // channels past the group) and zeroes those values afterwards, so all
+  // loads are in flight together.
+  auto load_item = [&](int go, int cg, int c0) -> vec16 {
+    const int cb = c0 + cg * UE;
+    uint32_t e[UE];
+#pragma unroll
+    for (int i = 0; i < UE; ++i) {
+      const bool ok = go >= 0 && cb + i < a.Cg;
+      const uint32_t bits = load_bits(x + (ok ? go + (cb + i) * HW : 0));
+      e[i] = ok ? bits : 0u;
+    }
+    vec16 u;
+    pack16<T>(u, e);
+    return u;
+  };
+
+  // Register stage for the next chunk.  fetch() only issues loads into raw
+  // registers; masking and packing wait until stash(), after the MFMAs of the
+  // current chunk, so the load latency overlaps the matrix work.
+  uint32_t xraw[kImax][UE];
+  vec16 wr[RST > 0 ? RST : 1];
+  const int wi = tid / NG, wcg = tid - (tid / NG) * NG;
+  const bool w_item = tid < BM * NG;
+  const bool w_row_ok = w_item && (k0 + wi < a.Kg);
+
+  // Filter row of this thread's item, clamped into the group so that its
+  // address is valid even for rows past Kg (their values are zeroed).
+  const int wrow = w_item ? min(wi, a.Kg - k0 - 1) : 0;
+  const T* wsrc = w + static_cast<int64_t>(wrow) * a.Cg * RS;
+
+  // Loads only: every address is valid (channels clamped into the group), no
+  // branches, so all of a thread's loads are in flight together.
+  auto fetch = [&](int c0) {
+#pragma unroll
+    for (int t = 0; t < kImax; ++t) {
+      const int cb = c0 + ((tid + t * kThreads) % NG) * UE;
+#pragma unroll
+      for (int i = 0; i < UE; ++i) xraw[t][i] = load_bits(x + gaddr[t] + min(cb + i, a.Cg - 1) * HW);
+    }
+    if constexpr (RST > 0) {
+      const int cb = min(c0 + wcg * UE, a.Cg - UE);
+#pragma unroll
+      for (int m = 0; m < RST; ++m) wr[m] = load16(wsrc + static_cast<int64_t>(cb) * RS + m * UE);
+    }
+  };
+
+  auto stash = [&](int c0) {
+#pragma unroll
+    for (int t = 0; t < kImax; ++t) {
+      const int it = tid + t * kThreads;
+      const int cb = c0 + (it % NG) * UE;
+      uint32_t e[UE];
+#pragma unroll
+      for (int i = 0; i < UE; ++i) e[i] = (gvalid[t] && cb + i < a.Cg) ? xraw[t][i] : 0u;
+      vec16 u;
+      pack16<T>(u, e);
+      if (it < nitems) Xs[(it / NG) * a.PS + it % NG] = u;
+    }
+    for (int it = tid + kImax * kThreads; it < nitems; it += kThreads)
+      Xs[(it / NG) * a.PS + it % NG] = load_item(item_goff(it), it % NG, c0);
+    if (w_item) {
+      if constexpr (RST > 0) {
+        // UE channels x RST taps arrive as RST 16-byte units in (channel,
+        // tap) order; regroup them as RST units of UE channels per tap.
+        const bool ok = w_row_ok && c0 + wcg * UE < a.Cg;
+#pragma unroll
+        for (int tap = 0; tap < RST; ++tap) {
+          uint32_t e[UE];
+#pragma unroll
+          for (int i = 0; i < UE; ++i) {
+            const int f = i * RST + tap;
+            const uint32_t word = wr[f / UE].d[(f % UE) / (4 / elem<T>::bytes > 0 ? (4 / elem<T>::bytes) : 1)];
+            const uint32_t bits = elem<T>::bytes == 2 ? ((f & 1) ? (word >> 16) : (word & 0xffffu)) : word;
+            e[i] = ok ? bits : 0u;
+          }
+          vec16 u;
+          pack16<T>(u, e);
+          As[wi * a.UR + tap * NG + wcg] = u;
+        }
+      } else {
+        const int cb = c0 + wcg * UE;
+        const T* src = w + static_cast<int64_t>(wi) * a.Cg * RS + static_cast<int64_t>(cb) * RS;
+        for (int tap = 0; tap < RS; ++tap) {
+          vec16 u = vec16_zero();
+          if (w_row_ok) {
+#pragma unroll
+            for (int e = 0; e < UE; ++e)
+              if (cb + e < a.Cg) vec16_set<T>(u, e, src[e * RS + tap]);
+          }
+          As[wi * a.UR + tap * NG + wcg] = u;
+        }
+      }
+    }
+  };
 
   f32x16_t acc[MI][NJ];
 #pragma unroll
@@ -123,79 +262,52 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
 #pragma unroll
     for (int nj = 0; nj < NJ; ++nj) acc[mi][nj] = zero16();
 
-  const int halo_items = a.VR * a.Wv * NG;
-  for (int c0 = 0; c0 < a.Cg; c0 += Cc) {
-    // ---- stage the input halo: item = (vrow, vcol, cg) -> UE channels ----
-    for (int it = tid; it < halo_items; it += kThreads) {
-      const int vc = it % a.Wv;
-      const int rest = it / a.Wv;
-      const int vr = rest % a.VR, cg = rest / a.VR;
-      const int v = vr_lo + vr;
-      const int n = v / a.Hv;
-      const int ih = v - n * a.Hv - a.ph, iw = vc - a.pw;
-      vec16 u = vec16_zero();
-      if (n < a.N && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W) {
-        const int cbase = c0 + cg * UE;
-        const T* src = x + (static_cast<int64_t>(n) * a.C + g * a.Cg + cbase) * HW + ih * a.W + iw;
+  const int arow = (wm * (BM / 2) + l32) * a.UR;
+  auto mfma_step = [&](int u, int xo) {
+    vec16 af[MI], bfr[NJ];
 #pragma unroll
-        for (int e = 0; e < UE; ++e)
-          if (cbase + e < a.Cg) vec16_set<T>(u, e, src[e * HW]);
-      }
-      Xs[(vr * a.Wv + vc) * a.PS + cg] = u;
-    }
-    // ---- stage the filters: item = (row i, cg) -> R*S units ----
-    for (int it = tid; it < BM * NG; it += kThreads) {
-      const int i = it / NG, cg = it - i * NG;
-      const int cbase = c0 + cg * UE;
-      const bool row_ok = k0 + i < a.Kg;
-      const T* src = w + static_cast<int64_t>(i) * a.Cg * RS + static_cast<int64_t>(cbase) * RS;
-      if constexpr (RST > 0) {
-        // UE whole channels of RST taps are RST contiguous 16-byte units.
-        vec16 raw[RST > 0 ? RST : 1];
+    for (int mi = 0; mi < MI; ++mi) af[mi] = As[arow + mi * 32 * a.UR + u];
 #pragma unroll
-        for (int m = 0; m < RST; ++m) raw[m] = (row_ok && cbase < a.Cg) ? load16(src + m * UE) : vec16_zero();
+    for (int nj = 0; nj < NJ; ++nj) bfr[nj] = Xs[pofs[nj] + xo];
 #pragma unroll
-        for (int tap = 0; tap < RST; ++tap) {
-          vec16 u = vec16_zero();
+    for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-          for (int e = 0; e < UE; ++e) {
-            const int f = e * RST + tap;  // flat (channel, tap) index in the loaded run
-            vec16_set<T>(u, e, vec16_get<T>(raw[f / UE], f % UE));
-          }
-          As[i * a.UR + tap * NG + cg] = u;
-        }
-      } else {
-        for (int tap = 0; tap < RS; ++tap) {
-          vec16 u = vec16_zero();
-          if (row_ok) {
-#pragma unroll
-            for (int e = 0; e < UE; ++e)
-              if (cbase + e < a.Cg) vec16_set<T>(u, e, src[e * RS + tap]);
-          }
-          As[i * a.UR + tap * NG + cg] = u;
-        }
-      }
-    }
-    // zero the padding unit of an odd unit count
-    if (a.units & 1)
-      for (int i = tid; i < BM; i += kThreads) As[i * a.UR + a.units] = vec16_zero();
-    __syncthreads();
+      for (int nj = 0; nj < NJ; ++nj) mfma_32x32<T>(acc[mi][nj], af[mi], bfr[nj]);
+  };
 
-    // ---- MFMA over the chunk's reduction steps ----
-    for (int st = 0; st < a.steps; ++st) {
-      const int u = 2 * st + half;
-      const int xo = utab[u];
-      vec16 af[MI], bfr[NJ];
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  for (int c0 = 0; c0 < a.Cg; c0 += Cc) {
+    const bool more = c0 + Cc < a.Cg;
+    fetch(more ? c0 + Cc : c0);  // the last chunk's refetch is never stashed
+    // Keep the prefetch loads ahead of the MFMAs (the scheduler would
+    // otherwise sink them to the end of the chunk, exposing their latency).
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (RST > 0) {
+      constexpr int STEPS = (RST * NG + 1) / 2;
 #pragma unroll
-      for (int mi = 0; mi < MI; ++mi) af[mi] = As[(wm * (BM / 2) + mi * 32 + l32) * a.UR + u];
-#pragma unroll
-      for (int nj = 0; nj < NJ; ++nj) bfr[nj] = Xs[pofs[nj] + xo];
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-        for (int nj = 0; nj < NJ; ++nj) mfma_32x32<T>(acc[mi][nj], af[mi], bfr[nj]);
+      for (int st = 0; st < STEPS; ++st) {
+        int xo;
+        if constexpr (NG == 2) {
+          xo = tapoff[st] + half;                      // units 2st, 2st+1: tap st, group = half
+        } else {
+          const int t0 = 2 * st, t1 = 2 * st + 1 < RST ? 2 * st + 1 : RST - 1;
+          xo = half ? tapoff[t1] : tapoff[t0];         // units 2st, 2st+1: taps 2st, 2st+1
+        }
+        mfma_step(2 * st + half, xo);
+      }
+    } else {
+      for (int st = 0; st < a.steps; ++st) {
+        const int u = 2 * st + half;
+        mfma_step(u, utab[u]);
+      }
     }
     __syncthreads();
+    if (more) {
+      stash(c0 + Cc);
+      __syncthreads();
+    }
   }
 
   // ---- epilogue: bias, ReLU, NCHW store ----
