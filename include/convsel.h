@@ -94,10 +94,16 @@ conv_status_t conv2d_output_shape(const conv2d_desc_t* desc, int64_t* p, int64_t
  * INVALID_ARG as conv2d_output_shape, or for an unknown algo value. */
 conv_status_t conv2d_check(const conv2d_desc_t* desc, conv_algo_t algo);
 
-/* Device workspace, in bytes, that conv2d() needs for this layer and algo
- * (0 for direct and implicit GEMM).  The column matrix and the Winograd
- * buffers are processed in batches of images, so the figure is capped near
- * 1 GiB unless one image alone needs more.  Same errors as conv2d_check. */
+/* Device workspace, in bytes, that conv2d() needs for this layer and algo.
+ *  - direct: 0.
+ *  - implicit GEMM: 0, except for layers whose output tiles alone would leave
+ *    compute units idle; those split the channel reduction over S <= 8
+ *    workgroups and need S*N*K*P*Q fp32 partial sums (summed by a second,
+ *    deterministic kernel).
+ *  - IM2COL + GEMM and Winograd: the column matrix / transformed tiles, built
+ *    for batches of images so the figure is capped near 1 GiB unless one
+ *    image alone needs more.
+ * Same errors as conv2d_check. */
 conv_status_t conv2d_workspace_bytes(const conv2d_desc_t* desc, conv_algo_t algo, size_t* bytes);
 
 /* The concrete algorithm CONV_ALGO_DEFAULT resolves to for this layer (a fixed

@@ -161,3 +161,21 @@ def wino_filter_raw(w_ptr, u_ptr, desc, stream):
 
 def wino_input_raw(x_ptr, v_ptr, desc, stream):
     return lib().conv2d_winograd_input_transform(x_ptr, v_ptr, ctypes.byref(desc), stream)
+
+
+class PreparedCall:
+    """A conv2d() call with every argument converted once, for repeated
+    launches with no per-call Python work beyond the foreign call itself."""
+
+    def __init__(self, x_ptr, w_ptr, b_ptr, y_ptr, desc, algo, ws_ptr, ws_bytes, stream):
+        self._fn = lib().conv2d
+        self._desc = desc  # keep alive: passed by reference
+        self._args = (ctypes.c_void_p(x_ptr), ctypes.c_void_p(w_ptr), ctypes.c_void_p(b_ptr or 0),
+                      ctypes.c_void_p(y_ptr), ctypes.byref(desc),
+                      algo_id(algo) if isinstance(algo, str) else int(algo),
+                      ctypes.c_void_p(ws_ptr or 0), ctypes.c_size_t(ws_bytes), ctypes.c_void_p(stream or 0))
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st != CONV_OK:
+            raise Conv2dError(st, "conv2d")

@@ -105,3 +105,28 @@ def winograd_input_transform(x, padding=1):
     if st != _lib.CONV_OK:
         raise _lib.Conv2dError(st, "conv2d_winograd_input_transform")
     return v
+
+
+def prepare(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, algo="default", relu=False, out=None):
+    """(callable, out): a conv2d launch with all arguments marshalled once
+    (output and workspace allocated here), for timing and tight loops.  The
+    tensors must stay alive and unmoved while the callable is used."""
+    if not (x.is_cuda and w.is_cuda and (b is None or b.is_cuda)):
+        raise ValueError("conv2d runs on the GPU only")
+    desc = _desc_for(x, w, b, stride, padding, dilation, groups, relu)
+    if not (x.is_contiguous() and w.is_contiguous() and (b is None or b.is_contiguous())):
+        raise ValueError("prepare() needs contiguous tensors")
+    P, Q = _lib.output_shape(desc)
+    algo_i = _lib.algo_id(algo)
+    st = _lib.check(desc, algo_i)
+    if st != _lib.CONV_OK:
+        raise _lib.Conv2dError(st, "conv2d(algo=%s)" % _lib.algo_name(algo_i))
+    if out is None:
+        out = torch.empty((x.shape[0], w.shape[0], P, Q), device=x.device, dtype=x.dtype)
+    nws = _lib.workspace_bytes(desc, algo_i)
+    ws = torch.empty(nws, dtype=torch.uint8, device=x.device) if nws else None
+    call = _lib.PreparedCall(x.data_ptr(), w.data_ptr(), None if b is None else b.data_ptr(), out.data_ptr(),
+                             desc, algo_i, None if ws is None else ws.data_ptr(), nws,
+                             torch.cuda.current_stream(x.device).cuda_stream)
+    call.workspace = ws  # keep alive
+    return call, out

@@ -8,10 +8,6 @@
 #include "../../include/convsel.h"
 #include "kernels.hpp"
 
-namespace convsel {
-bool implicit_gemm_fits(const Shape& s);
-}
-
 using convsel::Shape;
 
 namespace {
@@ -125,6 +121,7 @@ size_t workspace_for(const Shape& s, conv_algo_t algo) {
     return b;
   }
   if (algo == CONV_ALGO_WINOGRAD) return wino_layout(s).total;
+  if (algo == CONV_ALGO_IMPLICIT_GEMM) return convsel::implicit_gemm_workspace(s);
   return 0;
 }
 
@@ -169,7 +166,7 @@ conv_status_t run(const Shape& s, conv_algo_t algo, const void* x, const void* w
     case CONV_ALGO_DIRECT:
       return from_hip(launch_direct(s, x, w, b, y, st));
     case CONV_ALGO_IMPLICIT_GEMM:
-      return from_hip(launch_implicit_gemm(s, x, w, b, y, st));
+      return from_hip(launch_implicit_gemm(s, x, w, b, y, ws, st));
     case CONV_ALGO_IM2COL_GEMM: {
       const int64_t nb = im2col_batch(s, nullptr);
       const int64_t crs = s.Cg * s.R * s.S, PQ = s.P * s.Q;

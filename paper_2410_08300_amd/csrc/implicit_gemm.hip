@@ -55,6 +55,9 @@ struct IgArgs {
   int PS;             // halo pixel stride in 16-byte units (odd)
   int ktiles;         // ceil(Kg / BM)
   int xs_units;       // VR * Wv * PS
+  int splits;         // workgroups sharing one output tile along the channels
+  int chunks_per_split;
+  float* partial;     // splits > 1: fp32 partial sums, [split][N][K][P][Q]
 };
 
 // Virtual row of the first filter row for pixel j.
@@ -275,11 +278,16 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
       for (int nj = 0; nj < NJ; ++nj) mfma_32x32<T>(acc[mi][nj], af[mi], bfr[nj]);
   };
 
-  fetch(0);
-  stash(0);
+  // This workgroup's channel range (all channels unless split along them).
+  const int split = blockIdx.z;
+  const int c_begin = split * a.chunks_per_split * Cc;
+  const int c_end = min(a.Cg, c_begin + a.chunks_per_split * Cc);
+
+  fetch(c_begin);
+  stash(c_begin);
   __syncthreads();
-  for (int c0 = 0; c0 < a.Cg; c0 += Cc) {
-    const bool more = c0 + Cc < a.Cg;
+  for (int c0 = c_begin; c0 < c_end; c0 += Cc) {
+    const bool more = c0 + Cc < c_end;
     fetch(more ? c0 + Cc : c0);  // the last chunk's refetch is never stashed
     // Keep the prefetch loads ahead of the MFMAs (the scheduler would
     // otherwise sink them to the end of the chunk, exposing their latency).
@@ -311,9 +319,27 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
   }
 
   // ---- epilogue: bias, ReLU, NCHW store ----
+  const int64_t PQ = static_cast<int64_t>(a.P) * a.Q;
+  if (a.splits > 1) {
+    // Raw fp32 partial sums; the reduce kernel adds the splits, the bias and
+    // the ReLU, and rounds to the output type.
+    float* part = a.partial + static_cast<int64_t>(split) * a.N * a.K * PQ;
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int i = k0 + wm * (BM / 2) + mi * 32 + mfma_row(v, lane);
+        if (i >= a.Kg) continue;
+        const int k = g * a.Kg + i;
+#pragma unroll
+        for (int nj = 0; nj < NJ; ++nj)
+          if (jvalid[nj]) part[ybase[nj] + k * PQ] = acc[mi][nj][v];
+      }
+    }
+    return;
+  }
   const T* bias = reinterpret_cast<const T*>(a.b);
   T* y = reinterpret_cast<T*>(a.y);
-  const int64_t PQ = static_cast<int64_t>(a.P) * a.Q;
 #pragma unroll
   for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
@@ -330,6 +356,34 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
         elem<T>::store(y + ybase[nj] + k * PQ, val);
       }
     }
+  }
+}
+
+// Sum of the split partials, plus bias, ReLU, rounding to the output type;
+// four consecutive outputs per thread.
+template <typename T>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, const T* __restrict__ bias,
+                                                            T* __restrict__ y, int64_t total, int64_t PQ, int K,
+                                                            int splits, int relu) {
+  const int64_t i0 = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
+  if (i0 >= total) return;
+  const int n4 = total - i0 < 4 ? static_cast<int>(total - i0) : 4;
+  float sum[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < splits; ++s) {
+    const float* p = part + s * total + i0;
+    if (n4 == 4 && (reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+      const float4 v = *reinterpret_cast<const float4*>(p);
+      sum[0] += v.x; sum[1] += v.y; sum[2] += v.z; sum[3] += v.w;
+    } else {
+      for (int e = 0; e < n4; ++e) sum[e] += p[e];
+    }
+  }
+  for (int e = 0; e < n4; ++e) {
+    const int64_t i = i0 + e;
+    float v = sum[e];
+    if (bias) v += elem<T>::load(bias + static_cast<int>((i / PQ) % K));
+    if (relu) v = fmaxf(v, 0.f);
+    elem<T>::store(y + i, v);
   }
 }
 
@@ -378,6 +432,33 @@ struct IgPlan {
   size_t lds;
 };
 
+// Split the channel chunks over several workgroups when the output tiles
+// alone leave CUs idle: pick the split count S (1..8, at least two chunks per
+// split) that minimises the number of full waves of 256 CUs per unit of work,
+// ceil(tiles*S / 256) / S, plus a small charge per extra split for the
+// partial-sum traffic.
+constexpr int kCUs = 256;
+
+void choose_splits(const Shape& s, IgPlan& pl, int Cc) {
+  IgArgs& a = pl.a;
+  const int64_t tiles = (int64_t)((a.NPQ + BN - 1) / BN) * a.ktiles * s.G;
+  const int nch = (int)((s.Cg + Cc - 1) / Cc);
+  int best = 1;
+  double best_cost = 1e30;
+  if (tiles < kCUs) {
+    for (int S = 1; S <= 8 && S <= (nch + 1) / 2; ++S) {
+      const double waves = (double)((tiles * S + kCUs - 1) / kCUs) / S;
+      const double cost = waves + 0.05 * (S - 1);
+      if (cost < best_cost - 1e-9) {
+        best_cost = cost;
+        best = S;
+      }
+    }
+  }
+  a.chunks_per_split = (nch + best - 1) / best;
+  a.splits = (nch + a.chunks_per_split - 1) / a.chunks_per_split;
+}
+
 template <typename T>
 bool make_plan(const Shape& s, const void* wptr, IgPlan& pl) {
   constexpr int UE = elem<T>::per16;
@@ -409,6 +490,7 @@ bool make_plan(const Shape& s, const void* wptr, IgPlan& pl) {
       if (lds <= limit) {
         pl.NG = ng;
         pl.lds = lds;
+        choose_splits(s, pl, UE * ng);
         return true;
       }
     }
@@ -424,8 +506,15 @@ hipError_t launch_one(const IgPlan& pl, hipStream_t stream) {
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds);
     if (e != hipSuccess) return e;
   }
-  const dim3 grid((pl.a.NPQ + BN - 1) / BN, pl.a.ktiles * (pl.a.K / pl.a.Kg));
+  const dim3 grid((pl.a.NPQ + BN - 1) / BN, pl.a.ktiles * (pl.a.K / pl.a.Kg), pl.a.splits);
   hipLaunchKernelGGL(kern, grid, dim3(kThreads), pl.lds, stream, pl.a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || pl.a.splits == 1) return e;
+  const int64_t total = (int64_t)pl.a.N * pl.a.K * pl.a.P * pl.a.Q;
+  const int64_t blocks = (total + 1023) / 1024;
+  hipLaunchKernelGGL(splitk_reduce_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, stream, pl.a.partial,
+                     reinterpret_cast<const T*>(pl.a.b), reinterpret_cast<T*>(pl.a.y), total,
+                     (int64_t)pl.a.P * pl.a.Q, pl.a.K, pl.a.splits, pl.a.relu);
   return hipGetLastError();
 }
 
@@ -439,11 +528,13 @@ hipError_t launch_rst(const IgPlan& pl, hipStream_t stream) {
 }
 
 template <typename T>
-hipError_t launch_typed(const Shape& s, const void* x, const void* w, const void* b, void* y,
+hipError_t launch_typed(const Shape& s, const void* x, const void* w, const void* b, void* y, void* ws,
                         hipStream_t stream) {
   IgPlan pl;
   if (!make_plan<T>(s, w, pl)) return hipErrorInvalidValue;
   pl.a.x = x; pl.a.w = w; pl.a.b = b; pl.a.y = y;
+  pl.a.partial = reinterpret_cast<float*>(ws);
+  if (pl.a.splits > 1 && !ws) return hipErrorInvalidValue;
   if (pl.BM == 64) return pl.NG == 2 ? launch_rst<T, 64, 2>(pl, stream) : launch_rst<T, 64, 1>(pl, stream);
   return pl.NG == 2 ? launch_rst<T, 128, 2>(pl, stream) : launch_rst<T, 128, 1>(pl, stream);
 }
@@ -456,10 +547,17 @@ bool implicit_gemm_fits(const Shape& s) {
   return make_plan<bf16_t>(s, nullptr, pl);
 }
 
-hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, const void* b, void* y,
+size_t implicit_gemm_workspace(const Shape& s) {
+  IgPlan pl;
+  const bool ok = s.dtype == DT_F32 ? make_plan<float>(s, nullptr, pl) : make_plan<bf16_t>(s, nullptr, pl);
+  if (!ok || pl.a.splits <= 1) return 0;
+  return (size_t)pl.a.splits * s.N * s.K * s.P * s.Q * sizeof(float);
+}
+
+hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, const void* b, void* y, void* ws,
                                 hipStream_t stream) {
-  if (s.dtype == DT_F32) return launch_typed<float>(s, x, w, b, y, stream);
-  return launch_typed<bf16_t>(s, x, w, b, y, stream);
+  if (s.dtype == DT_F32) return launch_typed<float>(s, x, w, b, y, ws, stream);
+  return launch_typed<bf16_t>(s, x, w, b, y, ws, stream);
 }
 
 }  // namespace convsel

@@ -46,8 +46,12 @@ hipError_t launch_gemm_nt(int dtype, const GemmArgs& g, hipStream_t stream);
 hipError_t launch_direct(const Shape& s, const void* x, const void* w, const void* b, void* y,
                          hipStream_t stream);
 
-// implicit GEMM (MFMA), all N images.
-hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, const void* b, void* y,
+// implicit GEMM (MFMA), all N images.  Layers whose output tiles alone
+// would leave CUs idle split the channel reduction over several workgroups;
+// they need implicit_gemm_workspace(s) bytes of fp32 partial sums in ws.
+bool implicit_gemm_fits(const Shape& s);
+size_t implicit_gemm_workspace(const Shape& s);
+hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, const void* b, void* y, void* ws,
                                 hipStream_t stream);
 
 // Column matrix [nb][G][P*Q][Cg*R*S] of images n0 .. n0+nb-1.

@@ -20,7 +20,7 @@ import torch
 from torch import nn
 
 from . import _lib
-from .conv import conv2d
+from .conv import conv2d, prepare
 
 ALGO_CHOICES = ("default", "direct", "implicit_gemm", "im2col_gemm", "gemm", "winograd", "torch")
 CONCRETE_ALGOS = ("direct", "implicit_gemm", "im2col_gemm", "winograd")
@@ -167,20 +167,25 @@ def supported_algos(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, rel
 
 
 def time_conv(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, algo="default", relu=False,
-              warmup=2, reps=5):
-    """Median milliseconds per call (HIP events on the current stream)."""
-    out = conv2d(x, w, b, stride, padding, dilation, groups, algo=algo, relu=relu)
+              warmup=2, reps=5, launches=10):
+    """Median milliseconds per call: ``launches`` back-to-back launches
+    between two HIP events on the current stream (prebuilt arguments, so
+    the queue stays ahead of the GPU), median over ``reps`` trials."""
+    x, w = x.contiguous(), w.contiguous()
+    b = None if b is None else b.contiguous()
+    call, out = prepare(x, w, b, stride, padding, dilation, groups, algo=algo, relu=relu)
     for _ in range(warmup):
-        conv2d(x, w, b, stride, padding, dilation, groups, algo=algo, relu=relu, out=out)
+        call()
     times = []
     for _ in range(reps):
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record()
-        conv2d(x, w, b, stride, padding, dilation, groups, algo=algo, relu=relu, out=out)
+        for _ in range(launches):
+            call()
         e1.record()
         e1.synchronize()
-        times.append(e0.elapsed_time(e1))
+        times.append(e0.elapsed_time(e1) / launches)
     times.sort()
     return times[len(times) // 2]
 

@@ -115,6 +115,13 @@ def test_workspace_sizes():
     per_img = 112 * 112 * 512 * 9 * 2
     assert _lib.workspace_bytes(big, "im2col_gemm") == (1 << 30) // per_img * per_img
     assert _lib.workspace_bytes(_lib.make_desc(0, 4, 8, 8, 4, 3, 3), "im2col_gemm") == 0
+    # implicit GEMM: a 512-channel 7x7 layer at batch 32 has 13 x 4 output
+    # tiles of 128 x 128 for 256 CUs, so its channel reduction is split four
+    # ways (32 chunks of 16 channels, 8 per split) with fp32 partial sums.
+    small = _lib.make_desc(32, 512, 7, 7, 512, 3, 3, 1, 1, 1, 1, "bf16")
+    assert _lib.workspace_bytes(small, "implicit_gemm") == 4 * 32 * 512 * 49 * 4
+    large = _lib.make_desc(32, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, "bf16")
+    assert _lib.workspace_bytes(large, "implicit_gemm") == 0
 
 
 def test_default_rule():
