@@ -96,10 +96,11 @@ conv_status_t conv2d_check(const conv2d_desc_t* desc, conv_algo_t algo);
 
 /* Device workspace, in bytes, that conv2d() needs for this layer and algo.
  *  - direct: 0.
- *  - implicit GEMM: 0, except for layers whose output tiles alone would leave
- *    compute units idle; those split the channel reduction over S <= 8
- *    workgroups and need S*N*K*P*Q fp32 partial sums (summed by a second,
- *    deterministic kernel).
+ *  - implicit GEMM: the filters repacked per call into the kernel's layout
+ *    (K padded to the tile, channels padded to the chunk: at most a few MB
+ *    for common layers), plus, for layers whose output tiles alone would
+ *    leave compute units idle, S*N*K*P*Q fp32 partial sums of a channel
+ *    split over S <= 8 workgroups (summed by a second, deterministic kernel).
  *  - IM2COL + GEMM and Winograd: the column matrix / transformed tiles, built
  *    for batches of images so the figure is capped near 1 GiB unless one
  *    image alone needs more.

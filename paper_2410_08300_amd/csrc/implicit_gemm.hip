@@ -5,30 +5,38 @@
 //
 // Pixels are the flattened (n, p, q) output positions; a workgroup owns BN =
 // 128 consecutive pixels and BM (64 or 128) output channels of one group.  The
-// reduction is walked in chunks of Cc input channels; for each chunk:
+// reduction is walked in chunks of Cc input channels (Cc = 8*NG bf16 or
+// 4*NG fp32, i.e. NG 16-byte units per pixel):
 //
+//  * Filters are first repacked (one small kernel per call) into
+//        Wp[group][chunk][k (padded to BM)][tap][NG units of UE channels]
+//    with zeros in the padding, so one chunk's filter tile of a workgroup is
+//    a single contiguous block, staged in LDS as As[i][tap*NG + cg] by plain
+//    16-byte copies.
 //  * Input halo.  The input is viewed as a stack of zero-padded images in
 //    "virtual rows": pixel (n, p) with filter row r reads virtual row
 //    n*Hv + p*sh + r*dh, Hv = (P-1)*sh + (R-1)*dh + 1, and virtual column
 //    q*sw + s*dw (real row = virtual row mod Hv - pad_h, real column =
 //    virtual column - pad_w).  The workgroup's pixels read one contiguous
-//    range of VR virtual rows, each Wv columns wide.  That range is staged
-//    once per chunk in LDS with the channels innermost:
-//        Xs[(vrow * Wv + vcol) * PS + cg]   (16-byte units of UE channels)
-//    so every filter tap of every pixel is a 16-byte LDS read, and each input
-//    element is fetched from global memory once per chunk instead of R*S
-//    times.  Global reads of the halo are coalesced along the image row.
-//  * Filters.  The chunk's taps of the BM filters are staged as
-//        As[i * UR + (tap * NG + cg)]       (16-byte units)
-//    i.e. transposed from (c, r, s) to (tap, c) order so that a 16-byte unit
-//    holds UE consecutive channels of one tap, matching the input units.
-//  * MFMA.  One reduction step consumes two 16-byte units per lane (the two
-//    halves of the wave take units 2*step and 2*step+1), i.e. 16 bf16 or 8
-//    fp32 reduction terms; a unit table in LDS maps each unit to its LDS
-//    offset in Xs.  A padding unit (odd unit count) has zero filter values.
+//    range of VR virtual rows, each Wv columns wide, staged once per chunk
+//    with the channels innermost:  Xs[(vrow * Wv + vcol) * PS + cg], so
+//    every filter tap of every pixel is one 16-byte LDS read and each input
+//    element is fetched once per chunk instead of R*S times.
+//  * Loads are AMD buffer loads: the per-lane offset of a halo element is
+//    fixed for the whole kernel, the channel offset is a scalar, and reads
+//    outside the buffer return zero -- padding and channels past the group
+//    are mapped there, so no lane needs a select or a branch.
+//  * The next chunk is fetched into registers while the MFMAs of the current
+//    one run; one reduction step consumes two 16-byte units per lane (the
+//    two halves of the wave take units 2*step and 2*step+1: 16 bf16 or 8 fp32
+//    reduction terms); a padding unit (odd unit count) has zero filters.
+//  * Layers whose output tiles leave CUs idle split the chunks over several
+//    workgroups (fp32 partial sums, then a reduce kernel).
 //
 // Row strides in LDS (UR and PS units of 16 bytes) are odd, so the 16-byte
-// reads of 32 consecutive rows / pixels map to distinct bank groups.
+// reads of 32 consecutive rows / pixels map to distinct bank groups; stores
+// are arranged so that consecutive lanes write consecutive or odd-strided
+// units.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -38,26 +46,33 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int BN = 128;
+constexpr uint32_t kRsrcWord3 = 0x00020000u;  // raw buffer, 32-bit data format (gfx9 family)
+
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 
 struct IgArgs {
-  const void* x;
-  const void* w;
+  const void* x;       // first image of this launch
+  const void* wp;      // packed filters
   const void* b;
-  void* y;
+  void* y;             // first image of this launch
+  uint32_t x_bytes;    // extent of the input buffer of this launch
+  uint32_t wp_bytes;
   int N, C, H, W, K, R, S, P, Q;
   int sh, sw, ph, pw, dh, dw;
-  int Cg, Kg, relu;
-  int Hv, Wv, VR;     // virtual rows per image, halo width, halo rows
+  int Cg, Kg, G, relu;
+  int Hv, Wv, VR;      // virtual rows per image, halo width, halo rows
   int NPQ;
-  int units;          // R*S*NG
-  int steps;          // ceil(units / 2)
-  int UR;             // filter row stride in 16-byte units (odd)
-  int PS;             // halo pixel stride in 16-byte units (odd)
-  int ktiles;         // ceil(Kg / BM)
-  int xs_units;       // VR * Wv * PS
-  int splits;         // workgroups sharing one output tile along the channels
+  int units;           // R*S*NG: 16-byte units per filter row and chunk
+  int steps;           // ceil(units / 2)
+  int UR;              // filter row stride in 16-byte units (odd)
+  int PS;              // halo pixel stride in 16-byte units (odd)
+  int ktiles;          // ceil(Kg / BM)
+  int Kpad;            // ktiles * BM
+  int nch;             // channel chunks per group
+  int xs_units;        // VR * Wv * PS
+  int splits;          // workgroups sharing one output tile along the channels
   int chunks_per_split;
-  float* partial;     // splits > 1: fp32 partial sums, [split][N][K][P][Q]
+  float* partial;      // splits > 1: fp32 partial sums, [split][N][K][P][Q]
 };
 
 // Virtual row of the first filter row for pixel j.
@@ -67,17 +82,42 @@ __device__ __forceinline__ int vrow_of(int j, const IgArgs& a) {
   return n * a.Hv + (pq / a.Q) * a.sh;
 }
 
-// Halo items per thread whose global offsets are computed once per
-// workgroup and whose data are prefetched into registers; items beyond
-// kImax * 256 (very wide images) are staged on the fly.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, (int)kRsrcWord3);
+}
+
+__device__ __forceinline__ uint32_t buf_load_elem(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, float*) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+}
+__device__ __forceinline__ uint32_t buf_load_elem(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, bf16_t*) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
+}
+__device__ __forceinline__ vec16 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+  vec16 o;
+  o.d[0] = v[0];
+  o.d[1] = v[1];
+  o.d[2] = v[2];
+  o.d[3] = v[3];
+  return o;
+}
+
+// Halo items per thread kept in registers (offsets computed once, data
+// prefetched one chunk ahead); items beyond kImax * 256 (very wide images)
+// are loaded when stashed.
 constexpr int kImax = 4;
+// Filter units per thread prefetched for compile-time tap counts.
+template <int RST, int BM, int NG>
+struct WUnits {
+  static constexpr int value = RST > 0 ? (BM * RST * NG + kThreads - 1) / kThreads : 1;
+};
 
 template <typename T, int BM, int NG, int RST>
 __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
   constexpr int UE = elem<T>::per16;
-  constexpr int Cc = UE * NG;
+  constexpr int ES = elem<T>::bytes;
   constexpr int MI = BM / 64, NJ = BN / 64;
-  static_assert(BM * NG <= kThreads, "one filter item per thread");
+  constexpr int WU = WUnits<RST, BM, NG>::value;
   extern __shared__ __align__(16) vec16 smem[];
   vec16* As = smem;                         // [BM][UR]
   vec16* Xs = smem + BM * a.UR;             // [VR*Wv][PS]
@@ -88,16 +128,20 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
   const int half = lane >> 5, l32 = lane & 31;
   const int j0 = blockIdx.x * BN;
   const int g = blockIdx.y / a.ktiles;
-  const int k0 = (blockIdx.y - g * a.ktiles) * BM;
-  const int RS = a.R * a.S;
+  const int kt = blockIdx.y - g * a.ktiles;
+  const int k0 = kt * BM;
   const int jl = min(j0 + BN, a.NPQ) - 1;
   const int vr_lo = vrow_of(j0, a);
   const int HW = a.H * a.W;
+  const int units = a.units;
+
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.wp, a.wp_bytes);
 
   if constexpr (RST == 0) {
     for (int u = tid; u < 2 * a.steps; u += kThreads) {
       int off = 0;
-      if (u < a.units) {
+      if (u < units) {
         const int tap = u / NG, cg = u - tap * NG;
         const int r = tap / a.S, s = tap - r * a.S;
         off = (r * a.dh * a.Wv + s * a.dw) * a.PS + cg;
@@ -106,8 +150,8 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
     }
   }
   // The padding unit of an odd unit count holds zero filters (never rewritten).
-  if (a.units & 1)
-    for (int i = tid; i < BM; i += kThreads) As[i * a.UR + a.units] = vec16_zero();
+  if (units & 1)
+    for (int i = tid; i < BM; i += kThreads) As[i * a.UR + units] = vec16_zero();
 
   // Per-lane pixel offsets into the halo and output base offsets.
   int pofs[NJ];
@@ -134,128 +178,108 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
     tapoff[t] = (r * a.dh * a.Wv + s * a.dw) * a.PS;
   }
 
-  const T* x = reinterpret_cast<const T*>(a.x);
-  const T* w = reinterpret_cast<const T*>(a.w) + static_cast<int64_t>(g * a.Kg + k0) * a.Cg * RS;
-
-  // Halo item it = pix * NG + cg, pix = vrow * Wv + vcol.  goff: element
-  // offset of (image, row, column) in channel 0 of this group, or -1 where
-  // the item reads padding (or does not exist).
-  const int nitems = a.VR * a.Wv * NG;
-  auto item_goff = [&](int it) -> int {
-    if (it >= nitems) return -1;
-    const int pix = it / NG;
+  // Halo item it = cg * (VR*Wv) + pix, pix = vrow * Wv + vcol: consecutive
+  // lanes take consecutive pixels of one channel group (coalesced global
+  // reads; LDS stores at the odd stride PS).  Item offset: bytes to channel 0
+  // of the group at that position, or x_bytes (out of range: reads zero) for
+  // padding and missing items.
+  const int npix = a.VR * a.Wv;
+  const int nitems = npix * NG;
+  auto item_off = [&](int it) -> uint32_t {
+    if (it >= nitems) return a.x_bytes;
+    const int cg = it / npix, pix = it - cg * npix;
     const int vr = pix / a.Wv, vc = pix - vr * a.Wv;
     const int v = vr_lo + vr;
     const int n = v / a.Hv;
     const int ih = v - n * a.Hv - a.ph, iw = vc - a.pw;
-    if (n >= a.N || ih < 0 || ih >= a.H || iw < 0 || iw >= a.W) return -1;
-    return (n * a.C + g * a.Cg) * HW + ih * a.W + iw;
+    if (n >= a.N || ih < 0 || ih >= a.H || iw < 0 || iw >= a.W) return a.x_bytes;
+    return static_cast<uint32_t>(((n * a.C + g * a.Cg + cg * UE) * HW + ih * a.W + iw) * ES);
   };
-  // gaddr: always a valid element offset (padding items read element 0);
-  // gvalid marks the items whose values are kept.
-  int gaddr[kImax];
-  bool gvalid[kImax];
+  auto item_lds = [&](int it) -> int {
+    const int cg = it / npix, pix = it - cg * npix;
+    return pix * a.PS + cg;
+  };
+  uint32_t xoff[kImax];
+  int xlds[kImax];
 #pragma unroll
   for (int t = 0; t < kImax; ++t) {
-    const int go = item_goff(tid + t * kThreads);
-    gvalid[t] = go >= 0;
-    gaddr[t] = go >= 0 ? go : 0;
+    const int it = tid + t * kThreads;
+    xoff[t] = item_off(it);
+    xlds[t] = it < nitems ? item_lds(it) : -1;
   }
-
-  // Branch-free gather of UE channels at one halo position: every lane
-  // loads from a valid address (element 0 stands in for padding and for
-  // channels past the group) and zeroes those values afterwards, so all
-  // loads are in flight together.
-  auto load_item = [&](int go, int cg, int c0) -> vec16 {
-    const int cb = c0 + cg * UE;
-    uint32_t e[UE];
-#pragma unroll
-    for (int i = 0; i < UE; ++i) {
-      const bool ok = go >= 0 && cb + i < a.Cg;
-      const uint32_t bits = load_bits(x + (ok ? go + (cb + i) * HW : 0));
-      e[i] = ok ? bits : 0u;
-    }
-    vec16 u;
-    pack16<T>(u, e);
-    return u;
+  // Element e of the unit loaded for chunk offset c0: scalar (wave-uniform)
+  // channel offset c0 + e; in the tail chunk, where the unit may run past the
+  // group's channels, lanes past it use the out-of-range offset (zero).
+  auto load_unit_elem = [&](uint32_t voff, int cgb, int c0, int e) -> uint32_t {
+    const uint32_t so = static_cast<uint32_t>((c0 + e) * HW * ES);
+    const bool tail = c0 + UE * NG > a.Cg;  // uniform
+    const uint32_t vo = (tail && cgb + c0 + e >= a.Cg) ? a.x_bytes : voff;
+    return buf_load_elem(xr, vo, so, (T*)nullptr);
   };
 
-  // Register stage for the next chunk.  fetch() only issues loads into raw
-  // registers; masking and packing wait until stash(), after the MFMAs of the
-  // current chunk, so the load latency overlaps the matrix work.
+  // Filter units of this workgroup's tile: unit f = i*units + u.
+  uint32_t wvoff[WU];
+  int wlds[WU];
+#pragma unroll
+  for (int t = 0; t < WU; ++t) {
+    const int f = tid + t * kThreads;
+    const bool ok = f < BM * units;
+    const int i = ok ? f / units : 0, u = ok ? f - (f / units) * units : 0;
+    wvoff[t] = ok ? static_cast<uint32_t>(f * 16) : a.wp_bytes;
+    wlds[t] = ok ? i * a.UR + u : -1;
+  }
+  // Packed-filter byte offset of chunk ch of this tile.
+  auto wtile_soff = [&](int ch) -> uint32_t {
+    return static_cast<uint32_t>((static_cast<int64_t>(g * a.nch + ch) * a.Kpad + k0) * units * 16);
+  };
+
+  // Register stage for the next chunk.
   uint32_t xraw[kImax][UE];
-  vec16 wr[RST > 0 ? RST : 1];
-  const int wi = tid / NG, wcg = tid - (tid / NG) * NG;
-  const bool w_item = tid < BM * NG;
-  const bool w_row_ok = w_item && (k0 + wi < a.Kg);
+  vec16 wreg[WU];
 
-  // Filter row of this thread's item, clamped into the group so that its
-  // address is valid even for rows past Kg (their values are zeroed).
-  const int wrow = w_item ? min(wi, a.Kg - k0 - 1) : 0;
-  const T* wsrc = w + static_cast<int64_t>(wrow) * a.Cg * RS;
-
-  // Loads only: every address is valid (channels clamped into the group), no
-  // branches, so all of a thread's loads are in flight together.
-  auto fetch = [&](int c0) {
+  auto fetch = [&](int ch) {
+    const int c0 = ch * UE * NG;
 #pragma unroll
     for (int t = 0; t < kImax; ++t) {
-      const int cb = c0 + ((tid + t * kThreads) % NG) * UE;
+      const int cgb = ((tid + t * kThreads) / npix) * UE;
 #pragma unroll
-      for (int i = 0; i < UE; ++i) xraw[t][i] = load_bits(x + gaddr[t] + min(cb + i, a.Cg - 1) * HW);
+      for (int e = 0; e < UE; ++e) xraw[t][e] = load_unit_elem(xoff[t], cgb, c0, e);
     }
     if constexpr (RST > 0) {
-      const int cb = min(c0 + wcg * UE, a.Cg - UE);
+      const uint32_t so = wtile_soff(ch);
 #pragma unroll
-      for (int m = 0; m < RST; ++m) wr[m] = load16(wsrc + static_cast<int64_t>(cb) * RS + m * UE);
+      for (int t = 0; t < WU; ++t) wreg[t] = buf_load16(wr, wvoff[t], so);
     }
   };
 
-  auto stash = [&](int c0) {
+  auto stash = [&](int ch) {
 #pragma unroll
     for (int t = 0; t < kImax; ++t) {
-      const int it = tid + t * kThreads;
-      const int cb = c0 + (it % NG) * UE;
-      uint32_t e[UE];
-#pragma unroll
-      for (int i = 0; i < UE; ++i) e[i] = (gvalid[t] && cb + i < a.Cg) ? xraw[t][i] : 0u;
       vec16 u;
-      pack16<T>(u, e);
-      if (it < nitems) Xs[(it / NG) * a.PS + it % NG] = u;
+      pack16<T>(u, xraw[t]);
+      if (xlds[t] >= 0) Xs[xlds[t]] = u;
     }
-    for (int it = tid + kImax * kThreads; it < nitems; it += kThreads)
-      Xs[(it / NG) * a.PS + it % NG] = load_item(item_goff(it), it % NG, c0);
-    if (w_item) {
-      if constexpr (RST > 0) {
-        // UE channels x RST taps arrive as RST 16-byte units in (channel,
-        // tap) order; regroup them as RST units of UE channels per tap.
-        const bool ok = w_row_ok && c0 + wcg * UE < a.Cg;
+    if (nitems > kImax * kThreads) {
+      const int c0 = ch * UE * NG;
+      for (int it = tid + kImax * kThreads; it < nitems; it += kThreads) {
+        const uint32_t off = item_off(it);
+        const int cgb = (it / npix) * UE;
+        uint32_t e[UE];
 #pragma unroll
-        for (int tap = 0; tap < RST; ++tap) {
-          uint32_t e[UE];
-#pragma unroll
-          for (int i = 0; i < UE; ++i) {
-            const int f = i * RST + tap;
-            const uint32_t word = wr[f / UE].d[(f % UE) / (4 / elem<T>::bytes > 0 ? (4 / elem<T>::bytes) : 1)];
-            const uint32_t bits = elem<T>::bytes == 2 ? ((f & 1) ? (word >> 16) : (word & 0xffffu)) : word;
-            e[i] = ok ? bits : 0u;
-          }
-          vec16 u;
-          pack16<T>(u, e);
-          As[wi * a.UR + tap * NG + wcg] = u;
-        }
-      } else {
-        const int cb = c0 + wcg * UE;
-        const T* src = w + static_cast<int64_t>(wi) * a.Cg * RS + static_cast<int64_t>(cb) * RS;
-        for (int tap = 0; tap < RS; ++tap) {
-          vec16 u = vec16_zero();
-          if (w_row_ok) {
-#pragma unroll
-            for (int e = 0; e < UE; ++e)
-              if (cb + e < a.Cg) vec16_set<T>(u, e, src[e * RS + tap]);
-          }
-          As[wi * a.UR + tap * NG + wcg] = u;
-        }
+        for (int i = 0; i < UE; ++i) e[i] = load_unit_elem(off, cgb, c0, i);
+        vec16 u;
+        pack16<T>(u, e);
+        Xs[item_lds(it)] = u;
       }
+    }
+    if constexpr (RST > 0) {
+#pragma unroll
+      for (int t = 0; t < WU; ++t)
+        if (wlds[t] >= 0) As[wlds[t]] = wreg[t];
+    } else {
+      const uint32_t so = wtile_soff(ch);
+      for (int f = tid; f < BM * units; f += kThreads)
+        As[(f / units) * a.UR + f % units] = buf_load16(wr, static_cast<uint32_t>(f * 16), so);
     }
   };
 
@@ -278,17 +302,17 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
       for (int nj = 0; nj < NJ; ++nj) mfma_32x32<T>(acc[mi][nj], af[mi], bfr[nj]);
   };
 
-  // This workgroup's channel range (all channels unless split along them).
+  // This workgroup's chunk range (all chunks unless split along them).
   const int split = blockIdx.z;
-  const int c_begin = split * a.chunks_per_split * Cc;
-  const int c_end = min(a.Cg, c_begin + a.chunks_per_split * Cc);
+  const int ch_begin = split * a.chunks_per_split;
+  const int ch_end = min(a.nch, ch_begin + a.chunks_per_split);
 
-  fetch(c_begin);
-  stash(c_begin);
+  fetch(ch_begin);
+  stash(ch_begin);
   __syncthreads();
-  for (int c0 = c_begin; c0 < c_end; c0 += Cc) {
-    const bool more = c0 + Cc < c_end;
-    fetch(more ? c0 + Cc : c0);  // the last chunk's refetch is never stashed
+  for (int ch = ch_begin; ch < ch_end; ++ch) {
+    const bool more = ch + 1 < ch_end;
+    fetch(more ? ch + 1 : ch);  // the last chunk's refetch is never stashed
     // Keep the prefetch loads ahead of the MFMAs (the scheduler would
     // otherwise sink them to the end of the chunk, exposing their latency).
     __builtin_amdgcn_sched_barrier(0);
@@ -313,7 +337,7 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
     }
     __syncthreads();
     if (more) {
-      stash(c0 + Cc);
+      stash(ch + 1);
       __syncthreads();
     }
   }
@@ -359,6 +383,30 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
   }
 }
 
+// Wp[g][ch][kp][tap][cg][e] = w[g*Kg + kp][ch*Cc + cg*UE + e][tap], zero past
+// Kg rows or Cg channels.  One thread per packed element (coalesced stores).
+template <typename T>
+__global__ __launch_bounds__(256) void pack_filters_kernel(const T* __restrict__ w, T* __restrict__ wp, int64_t total,
+                                                           int Kg, int Cg, int RS, int NG, int nch, int Kpad) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= total) return;
+  constexpr int UE = elem<T>::per16;
+  const int e = static_cast<int>(idx % UE);
+  int64_t r = idx / UE;
+  const int cg = static_cast<int>(r % NG);
+  r /= NG;
+  const int tap = static_cast<int>(r % RS);
+  r /= RS;
+  const int kp = static_cast<int>(r % Kpad);
+  r /= Kpad;
+  const int ch = static_cast<int>(r % nch);
+  const int g = static_cast<int>(r / nch);
+  const int c = ch * UE * NG + cg * UE + e;
+  T v = elem<T>::from_f32(0.f);
+  if (kp < Kg && c < Cg) v = w[(static_cast<int64_t>(g * Kg + kp) * Cg + c) * RS + tap];
+  wp[idx] = v;
+}
+
 // Sum of the split partials, plus bias, ReLU, rounding to the output type;
 // four consecutive outputs per thread.
 template <typename T>
@@ -387,11 +435,11 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   }
 }
 
-// Largest halo span (in virtual rows) over all pixel tiles.  The span of a
-// tile depends only on where it starts within an image, which repeats every
-// PQ / gcd(BN, PQ) tiles, so one period is scanned.
-int halo_rows(const Shape& s, int Hv) {
-  const int64_t PQ = s.P * s.Q, NPQ = s.N * PQ;
+// Largest halo span (in virtual rows) over all pixel tiles of N images.  The
+// span of a tile depends only on where it starts within an image, which
+// repeats every PQ / gcd(BN, PQ) tiles, so one period is scanned.
+int halo_rows(const Shape& s, int64_t N, int Hv) {
+  const int64_t PQ = s.P * s.Q, NPQ = N * PQ;
   const int64_t tiles = (NPQ + BN - 1) / BN;
   int64_t a = BN, b = PQ;
   while (b) {
@@ -425,9 +473,17 @@ int halo_rows(const Shape& s, int Hv) {
 // 160 KiB a workgroup may hold.
 constexpr size_t kLdsPreferred = 80 * 1024;
 constexpr size_t kLdsLimit = 160 * 1024;
+// Each launch reads at most 1 GiB of input, so a buffer offset (at most the
+// buffer size, which marks out-of-range lanes) plus a channel offset stays
+// within 32 bits.
+constexpr int64_t kMaxLaunchBytes = (int64_t)1 << 30;
+constexpr int kCUs = 256;
 
 struct IgPlan {
   int BM, NG, RST;
+  int64_t images_per_launch;
+  size_t wp_bytes;      // packed filters
+  size_t part_bytes;    // split-K partial sums (per launch)
   IgArgs a;
   size_t lds;
 };
@@ -437,16 +493,13 @@ struct IgPlan {
 // split) that minimises the number of full waves of 256 CUs per unit of work,
 // ceil(tiles*S / 256) / S, plus a small charge per extra split for the
 // partial-sum traffic.
-constexpr int kCUs = 256;
-
-void choose_splits(const Shape& s, IgPlan& pl, int Cc) {
+void choose_splits(const Shape& s, IgPlan& pl) {
   IgArgs& a = pl.a;
   const int64_t tiles = (int64_t)((a.NPQ + BN - 1) / BN) * a.ktiles * s.G;
-  const int nch = (int)((s.Cg + Cc - 1) / Cc);
   int best = 1;
   double best_cost = 1e30;
   if (tiles < kCUs) {
-    for (int S = 1; S <= 8 && S <= (nch + 1) / 2; ++S) {
+    for (int S = 1; S <= 8 && S <= (a.nch + 1) / 2; ++S) {
       const double waves = (double)((tiles * S + kCUs - 1) / kCUs) / S;
       const double cost = waves + 0.05 * (S - 1);
       if (cost < best_cost - 1e-9) {
@@ -455,30 +508,39 @@ void choose_splits(const Shape& s, IgPlan& pl, int Cc) {
       }
     }
   }
-  a.chunks_per_split = (nch + best - 1) / best;
-  a.splits = (nch + a.chunks_per_split - 1) / a.chunks_per_split;
+  a.chunks_per_split = (a.nch + best - 1) / best;
+  a.splits = (a.nch + a.chunks_per_split - 1) / a.chunks_per_split;
 }
 
+// Plan for `N1` images per launch (all of them unless the input exceeds the
+// per-launch limit).
 template <typename T>
-bool make_plan(const Shape& s, const void* wptr, IgPlan& pl) {
+bool make_plan(const Shape& s, IgPlan& pl, int64_t N1 = -1) {
   constexpr int UE = elem<T>::per16;
+  const int64_t img_bytes = s.C * s.H * s.W * s.esize();
+  if (img_bytes > kMaxLaunchBytes) return false;
+  if (N1 < 0) {
+    N1 = kMaxLaunchBytes / img_bytes;
+    if (N1 > s.N) N1 = s.N;
+    if (N1 < 1) N1 = 1;
+  }
+  pl.images_per_launch = N1;
   IgArgs& a = pl.a;
-  a.N = (int)s.N; a.C = (int)s.C; a.H = (int)s.H; a.W = (int)s.W; a.K = (int)s.K;
+  a.N = (int)N1; a.C = (int)s.C; a.H = (int)s.H; a.W = (int)s.W; a.K = (int)s.K;
   a.R = (int)s.R; a.S = (int)s.S; a.P = (int)s.P; a.Q = (int)s.Q;
   a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw; a.dh = s.dh; a.dw = s.dw;
-  a.Cg = (int)s.Cg; a.Kg = (int)s.Kg; a.relu = s.relu ? 1 : 0;
+  a.Cg = (int)s.Cg; a.Kg = (int)s.Kg; a.G = s.G; a.relu = s.relu ? 1 : 0;
   a.Hv = (int)((s.P - 1) * s.sh + (s.R - 1) * s.dh + 1);
   a.Wv = (int)((s.Q - 1) * s.sw + (s.S - 1) * s.dw + 1);
-  a.VR = halo_rows(s, a.Hv);
-  a.NPQ = (int)(s.N * s.P * s.Q);
+  a.VR = halo_rows(s, N1, a.Hv);
+  a.NPQ = (int)(N1 * s.P * s.Q);
   const int RS = a.R * a.S;
   pl.BM = s.Kg <= 64 ? 64 : 128;
   a.ktiles = (a.Kg + pl.BM - 1) / pl.BM;
-  const bool aligned = reinterpret_cast<uintptr_t>(wptr) % 16 == 0;
-  const bool vec_w = aligned && s.Cg % UE == 0;
+  a.Kpad = a.ktiles * pl.BM;
   pl.RST = 0;
-  if (vec_w && RS == 1) pl.RST = 1;
-  if (vec_w && RS == 9) pl.RST = 9;
+  if (RS == 1) pl.RST = 1;
+  if (RS == 9) pl.RST = 9;
   for (size_t limit : {kLdsPreferred, kLdsLimit}) {
     for (int ng = (s.Cg > UE ? 2 : 1); ng >= 1; --ng) {
       a.units = RS * ng;
@@ -487,43 +549,48 @@ bool make_plan(const Shape& s, const void* wptr, IgPlan& pl) {
       a.PS = ng | 1;
       a.xs_units = a.VR * a.Wv * a.PS;
       const size_t lds = ((size_t)pl.BM * a.UR + (size_t)a.xs_units) * 16 + (size_t)2 * a.steps * 4;
-      if (lds <= limit) {
-        pl.NG = ng;
-        pl.lds = lds;
-        choose_splits(s, pl, UE * ng);
-        return true;
-      }
+      if (lds > limit) continue;
+      pl.NG = ng;
+      pl.lds = lds;
+      a.nch = (int)((s.Cg + UE * ng - 1) / (UE * ng));
+      pl.wp_bytes = (size_t)s.G * a.nch * a.Kpad * a.units * 16;
+      if (pl.wp_bytes > (size_t)kMaxLaunchBytes) return false;
+      choose_splits(s, pl);
+      pl.part_bytes = a.splits > 1 ? (size_t)a.splits * N1 * s.K * s.P * s.Q * sizeof(float) : 0;
+      return true;
     }
   }
   return false;
 }
 
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
 template <typename T, int BM, int NG, int RST>
-hipError_t launch_one(const IgPlan& pl, hipStream_t stream) {
+hipError_t launch_one(const IgPlan& pl, const IgArgs& a, hipStream_t stream) {
   const auto kern = implicit_gemm_kernel<T, BM, NG, RST>;
   if (pl.lds > 64 * 1024) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds);
     if (e != hipSuccess) return e;
   }
-  const dim3 grid((pl.a.NPQ + BN - 1) / BN, pl.a.ktiles * (pl.a.K / pl.a.Kg), pl.a.splits);
-  hipLaunchKernelGGL(kern, grid, dim3(kThreads), pl.lds, stream, pl.a);
+  const dim3 grid((a.NPQ + BN - 1) / BN, a.ktiles * a.G, a.splits);
+  hipLaunchKernelGGL(kern, grid, dim3(kThreads), pl.lds, stream, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || pl.a.splits == 1) return e;
-  const int64_t total = (int64_t)pl.a.N * pl.a.K * pl.a.P * pl.a.Q;
+  if (e != hipSuccess || a.splits == 1) return e;
+  const int64_t total = (int64_t)a.N * a.K * a.P * a.Q;
   const int64_t blocks = (total + 1023) / 1024;
-  hipLaunchKernelGGL(splitk_reduce_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, stream, pl.a.partial,
-                     reinterpret_cast<const T*>(pl.a.b), reinterpret_cast<T*>(pl.a.y), total,
-                     (int64_t)pl.a.P * pl.a.Q, pl.a.K, pl.a.splits, pl.a.relu);
+  hipLaunchKernelGGL(splitk_reduce_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, stream, a.partial,
+                     reinterpret_cast<const T*>(a.b), reinterpret_cast<T*>(a.y), total, (int64_t)a.P * a.Q, a.K,
+                     a.splits, a.relu);
   return hipGetLastError();
 }
 
 template <typename T, int BM, int NG>
-hipError_t launch_rst(const IgPlan& pl, hipStream_t stream) {
+hipError_t launch_rst(const IgPlan& pl, const IgArgs& a, hipStream_t stream) {
   switch (pl.RST) {
-    case 1: return launch_one<T, BM, NG, 1>(pl, stream);
-    case 9: return launch_one<T, BM, NG, 9>(pl, stream);
-    default: return launch_one<T, BM, NG, 0>(pl, stream);
+    case 1: return launch_one<T, BM, NG, 1>(pl, a, stream);
+    case 9: return launch_one<T, BM, NG, 9>(pl, a, stream);
+    default: return launch_one<T, BM, NG, 0>(pl, a, stream);
   }
 }
 
@@ -531,27 +598,66 @@ template <typename T>
 hipError_t launch_typed(const Shape& s, const void* x, const void* w, const void* b, void* y, void* ws,
                         hipStream_t stream) {
   IgPlan pl;
-  if (!make_plan<T>(s, w, pl)) return hipErrorInvalidValue;
-  pl.a.x = x; pl.a.w = w; pl.a.b = b; pl.a.y = y;
-  pl.a.partial = reinterpret_cast<float*>(ws);
-  if (pl.a.splits > 1 && !ws) return hipErrorInvalidValue;
-  if (pl.BM == 64) return pl.NG == 2 ? launch_rst<T, 64, 2>(pl, stream) : launch_rst<T, 64, 1>(pl, stream);
-  return pl.NG == 2 ? launch_rst<T, 128, 2>(pl, stream) : launch_rst<T, 128, 1>(pl, stream);
+  if (!make_plan<T>(s, pl) || !ws) return hipErrorInvalidValue;
+  T* wp = reinterpret_cast<T*>(ws);
+  float* part = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + align256(pl.wp_bytes));
+  {
+    const int64_t total = (int64_t)(pl.wp_bytes / sizeof(T));
+    hipLaunchKernelGGL(pack_filters_kernel<T>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
+                       reinterpret_cast<const T*>(w), wp, total, (int)s.Kg, (int)s.Cg, (int)(s.R * s.S), pl.NG,
+                       pl.a.nch, pl.a.Kpad);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const int64_t img_elems = s.C * s.H * s.W, out_elems = s.K * s.P * s.Q;
+  for (int64_t n0 = 0; n0 < s.N; n0 += pl.images_per_launch) {
+    const int64_t cnt = s.N - n0 < pl.images_per_launch ? s.N - n0 : pl.images_per_launch;
+    IgPlan cur = pl;
+    // The last, smaller batch of images has its own tiles, halo span and
+    // split count (never more partial sums than the full batch).
+    if (cnt != pl.images_per_launch && !make_plan<T>(s, cur, cnt)) return hipErrorInvalidValue;
+    if (cur.NG != pl.NG || cur.BM != pl.BM) return hipErrorInvalidValue;
+    IgArgs a = cur.a;
+    a.x = reinterpret_cast<const T*>(x) + n0 * img_elems;
+    a.y = reinterpret_cast<T*>(y) + n0 * out_elems;
+    a.x_bytes = (uint32_t)(cnt * img_elems * s.esize());
+    a.wp = wp;
+    a.wp_bytes = (uint32_t)pl.wp_bytes;
+    a.b = b;
+    a.partial = part;
+    hipError_t e;
+    if (pl.BM == 64)
+      e = pl.NG == 2 ? launch_rst<T, 64, 2>(cur, a, stream) : launch_rst<T, 64, 1>(cur, a, stream);
+    else
+      e = pl.NG == 2 ? launch_rst<T, 128, 2>(cur, a, stream) : launch_rst<T, 128, 1>(cur, a, stream);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace
 
 bool implicit_gemm_fits(const Shape& s) {
   IgPlan pl;
-  if (s.dtype == DT_F32) return make_plan<float>(s, nullptr, pl);
-  return make_plan<bf16_t>(s, nullptr, pl);
+  if (s.dtype == DT_F32) return make_plan<float>(s, pl);
+  return make_plan<bf16_t>(s, pl);
+}
+
+template <typename T>
+size_t workspace_typed(const Shape& s) {
+  IgPlan pl;
+  if (!make_plan<T>(s, pl)) return 0;
+  size_t part = pl.part_bytes;
+  const int64_t rem = s.N % pl.images_per_launch;
+  if (rem) {
+    IgPlan last;
+    if (make_plan<T>(s, last, rem) && last.part_bytes > part) part = last.part_bytes;
+  }
+  return align256(pl.wp_bytes) + part;
 }
 
 size_t implicit_gemm_workspace(const Shape& s) {
-  IgPlan pl;
-  const bool ok = s.dtype == DT_F32 ? make_plan<float>(s, nullptr, pl) : make_plan<bf16_t>(s, nullptr, pl);
-  if (!ok || pl.a.splits <= 1) return 0;
-  return (size_t)pl.a.splits * s.N * s.K * s.P * s.Q * sizeof(float);
+  return s.dtype == DT_F32 ? workspace_typed<float>(s) : workspace_typed<bf16_t>(s);
 }
 
 hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, const void* b, void* y, void* ws,

@@ -102,7 +102,6 @@ def test_workspace_sizes():
     d = _lib.make_desc(4, 6, 10, 12, 8, 3, 3, 2, 1, 1, 2, "bf16")
     P, Q = _lib.output_shape(d)
     assert _lib.workspace_bytes(d, "direct") == 0
-    assert _lib.workspace_bytes(d, "implicit_gemm") == 0
     assert _lib.workspace_bytes(d, "im2col_gemm") == 4 * 2 * P * Q * 3 * 9 * 2
     w = _lib.make_desc(3, 16, 7, 7, 8, 3, 3, 1, 1, 1, 1, "f32")
     T = 3 * 4 * 4
@@ -115,13 +114,17 @@ def test_workspace_sizes():
     per_img = 112 * 112 * 512 * 9 * 2
     assert _lib.workspace_bytes(big, "im2col_gemm") == (1 << 30) // per_img * per_img
     assert _lib.workspace_bytes(_lib.make_desc(0, 4, 8, 8, 4, 3, 3), "im2col_gemm") == 0
-    # implicit GEMM: a 512-channel 7x7 layer at batch 32 has 13 x 4 output
-    # tiles of 128 x 128 for 256 CUs, so its channel reduction is split four
-    # ways (32 chunks of 16 channels, 8 per split) with fp32 partial sums.
-    small = _lib.make_desc(32, 512, 7, 7, 512, 3, 3, 1, 1, 1, 1, "bf16")
-    assert _lib.workspace_bytes(small, "implicit_gemm") == 4 * 32 * 512 * 49 * 4
+    # implicit GEMM: the filters repacked as [chunk][K padded to the tile]
+    # [tap][16-byte units], plus fp32 split partial sums for small grids.
+    # 64 -> 64 channels, 56x56, batch 32: 784 tiles of 64 x 128, no split;
+    # 4 chunks of 16 channels x 64 filters x 9 taps x 2 units x 16 bytes.
     large = _lib.make_desc(32, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, "bf16")
-    assert _lib.workspace_bytes(large, "implicit_gemm") == 0
+    assert _lib.workspace_bytes(large, "implicit_gemm") == 4 * 64 * 18 * 16
+    # 512 -> 512 channels, 7x7, batch 32: 13 x 4 tiles of 128 x 128 leave
+    # most of 256 CUs idle, so the 32 chunks are split four ways.
+    small = _lib.make_desc(32, 512, 7, 7, 512, 3, 3, 1, 1, 1, 1, "bf16")
+    packed = 32 * 512 * 18 * 16
+    assert _lib.workspace_bytes(small, "implicit_gemm") == packed + 4 * 32 * 512 * 49 * 4
 
 
 def test_default_rule():
