@@ -113,10 +113,12 @@ conv_status_t conv2d_workspace_bytes(const conv2d_desc_t* desc, conv_algo_t algo
 conv_algo_t conv2d_default_algo(const conv2d_desc_t* desc);
 
 /* y = conv(x, w) (+ b) (then ReLU) with the chosen algorithm, enqueued on
- * `stream`.  x, w, y (and b when has_bias) must be non-NULL device pointers;
- * y must not overlap x, w, b or the workspace.  workspace may be NULL when
- * workspace_bytes is 0.  Returns INVALID_ARG / UNSUPPORTED / WORKSPACE before
- * touching the device, DEVICE if a HIP call fails. */
+ * `stream`.  x, w, y (and b when has_bias) must be non-NULL device pointers
+ * (any element alignment); y must not overlap x, w, b or the workspace.  A
+ * workspace, when one is needed, must be 256-byte aligned (INVALID_ARG
+ * otherwise); it may be NULL when the required size is 0.  Returns
+ * INVALID_ARG / UNSUPPORTED / WORKSPACE before touching the device, DEVICE
+ * if a HIP call fails. */
 conv_status_t conv2d(const void* x, const void* w, const void* b, void* y, const conv2d_desc_t* desc,
                      conv_algo_t algo, void* workspace, size_t workspace_bytes, void* stream);
 

@@ -281,6 +281,7 @@ conv_status_t conv2d(const void* x, const void* w, const void* b, void* y, const
   if (!x || !w || !y || (s.bias != (b != nullptr))) return CONV_ERR_INVALID_ARG;
   const size_t need = workspace_for(s, algo);
   if (workspace_bytes < need || (need > 0 && !workspace)) return CONV_ERR_WORKSPACE;
+  if (need > 0 && reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return CONV_ERR_INVALID_ARG;
   const size_t es = (size_t)s.esize();
   const size_t ybytes = (size_t)s.N * s.K * s.P * s.Q * es;
   if (overlaps(y, ybytes, x, (size_t)s.N * s.C * s.H * s.W * es) ||

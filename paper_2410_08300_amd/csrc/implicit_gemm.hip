@@ -37,6 +37,8 @@
 // reads of 32 consecutive rows / pixels map to distinct bank groups; stores
 // are arranged so that consecutive lanes write consecutive or odd-strided
 // units.
+#include <atomic>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -73,6 +75,8 @@ struct IgArgs {
   int splits;          // workgroups sharing one output tile along the channels
   int chunks_per_split;
   float* partial;      // splits > 1: fp32 partial sums, [split][N][K][P][Q]
+  int slab;            // floats per split of `partial` (N*K*P*Q rounded up to 4)
+  int vec_out;         // P*Q % 8 == 0 and y 16-byte aligned: staged 16-byte stores
 };
 
 // Virtual row of the first filter row for pixel j.
@@ -343,27 +347,72 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
   }
 
   // ---- epilogue: bias, ReLU, NCHW store ----
+  // With P*Q a multiple of 8, every aligned run of 8 tile pixels lies in one
+  // image and starts 16-byte aligned in y, so the accumulators go through
+  // LDS (the chunk buffers are free now) and leave as 16-byte stores of 8
+  // consecutive pixels of one channel.  Otherwise each lane stores its own
+  // values (lanes hold consecutive pixels, so stores still coalesce).
+  // Split workgroups write raw fp32 partial sums instead (summed, biased and
+  // rounded by the reduce kernel).
   const int64_t PQ = static_cast<int64_t>(a.P) * a.Q;
-  if (a.splits > 1) {
-    // Raw fp32 partial sums; the reduce kernel adds the splits, the bias and
-    // the ReLU, and rounds to the output type.
-    float* part = a.partial + static_cast<int64_t>(split) * a.N * a.K * PQ;
+  const bool split_out = a.splits > 1;
+  float* part = split_out ? a.partial + static_cast<int64_t>(split) * a.slab : nullptr;
+  const T* bias = reinterpret_cast<const T*>(a.b);
+  T* y = reinterpret_cast<T*>(a.y);
+  if (a.vec_out) {
+    constexpr int EW = BN / 2;        // pixels per wave row
+    constexpr int ES_ROW = EW + 4;    // staged row stride (floats)
+    float* stage = reinterpret_cast<float*>(smem) + wave * 32 * ES_ROW;
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int i = k0 + wm * (BM / 2) + mi * 32 + mfma_row(v, lane);
-        if (i >= a.Kg) continue;
-        const int k = g * a.Kg + i;
+      for (int nj = 0; nj < NJ; ++nj)
 #pragma unroll
-        for (int nj = 0; nj < NJ; ++nj)
-          if (jvalid[nj]) part[ybase[nj] + k * PQ] = acc[mi][nj][v];
+        for (int v = 0; v < 16; ++v) stage[mfma_row(v, lane) * ES_ROW + nj * 32 + l32] = acc[mi][nj][v];
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+      __builtin_amdgcn_wave_barrier();
+      // 32 rows x EW pixels = 4*EW/8 runs of 8; lane takes runs lane, lane+64, ...
+#pragma unroll
+      for (int it = 0; it < 32 * EW / 8 / 64; ++it) {
+        const int run = lane + 64 * it;
+        const int row = run / (EW / 8), cb = (run % (EW / 8)) * 8;
+        const int i = k0 + wm * (BM / 2) + mi * 32 + row;
+        const int j = j0 + wn * (BN / 2) + cb;
+        if (i >= a.Kg || j >= a.NPQ) continue;
+        const int k = g * a.Kg + i;
+        const int n = j / static_cast<int>(PQ), pq = j - n * static_cast<int>(PQ);
+        const int64_t o = (static_cast<int64_t>(n) * a.K + k) * PQ + pq;
+        const float4 lo = *reinterpret_cast<const float4*>(stage + row * ES_ROW + cb);
+        const float4 hi = *reinterpret_cast<const float4*>(stage + row * ES_ROW + cb + 4);
+        float vals[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        if (split_out) {
+          *reinterpret_cast<float4*>(part + o) = lo;
+          *reinterpret_cast<float4*>(part + o + 4) = hi;
+          continue;
+        }
+        const float bv = bias ? elem<T>::load(bias + k) : 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          vals[e] += bv;
+          if (a.relu) vals[e] = fmaxf(vals[e], 0.f);
+        }
+        if constexpr (sizeof(T) == 2) {
+          uint4 u;
+          u.x = f32x2_to_bf16x2(vals[0], vals[1]);
+          u.y = f32x2_to_bf16x2(vals[2], vals[3]);
+          u.z = f32x2_to_bf16x2(vals[4], vals[5]);
+          u.w = f32x2_to_bf16x2(vals[6], vals[7]);
+          *reinterpret_cast<uint4*>(y + o) = u;
+        } else {
+          *reinterpret_cast<float4*>(reinterpret_cast<float*>(y) + o) = make_float4(vals[0], vals[1], vals[2], vals[3]);
+          *reinterpret_cast<float4*>(reinterpret_cast<float*>(y) + o + 4) =
+              make_float4(vals[4], vals[5], vals[6], vals[7]);
+        }
       }
+      __builtin_amdgcn_wave_barrier();  // the next block reuses this wave's stage
     }
     return;
   }
-  const T* bias = reinterpret_cast<const T*>(a.b);
-  T* y = reinterpret_cast<T*>(a.y);
 #pragma unroll
   for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
@@ -371,10 +420,14 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
       const int i = k0 + wm * (BM / 2) + mi * 32 + mfma_row(v, lane);
       if (i >= a.Kg) continue;
       const int k = g * a.Kg + i;
-      const float bv = bias ? elem<T>::load(bias + k) : 0.f;
+      const float bv = (bias && !split_out) ? elem<T>::load(bias + k) : 0.f;
 #pragma unroll
       for (int nj = 0; nj < NJ; ++nj) {
         if (!jvalid[nj]) continue;
+        if (split_out) {
+          part[ybase[nj] + k * PQ] = acc[mi][nj][v];
+          continue;
+        }
         float val = acc[mi][nj][v] + bv;
         if (a.relu) val = fmaxf(val, 0.f);
         elem<T>::store(y + ybase[nj] + k * PQ, val);
@@ -384,52 +437,52 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
 }
 
 // Wp[g][ch][kp][tap][cg][e] = w[g*Kg + kp][ch*Cc + cg*UE + e][tap], zero past
-// Kg rows or Cg channels.  One thread per packed element (coalesced stores).
+// Kg rows or Cg channels.  One workgroup per packed row (g, ch, kp); its
+// threads write the row's RS*NG*UE elements consecutively.
 template <typename T>
-__global__ __launch_bounds__(256) void pack_filters_kernel(const T* __restrict__ w, T* __restrict__ wp, int64_t total,
-                                                           int Kg, int Cg, int RS, int NG, int nch, int Kpad) {
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (idx >= total) return;
+__global__ __launch_bounds__(256) void pack_filters_kernel(const T* __restrict__ w, T* __restrict__ wp, int Kg,
+                                                           int Cg, int RS, int NG, int nch, int Kpad) {
   constexpr int UE = elem<T>::per16;
-  const int e = static_cast<int>(idx % UE);
-  int64_t r = idx / UE;
-  const int cg = static_cast<int>(r % NG);
-  r /= NG;
-  const int tap = static_cast<int>(r % RS);
-  r /= RS;
-  const int kp = static_cast<int>(r % Kpad);
-  r /= Kpad;
-  const int ch = static_cast<int>(r % nch);
-  const int g = static_cast<int>(r / nch);
-  const int c = ch * UE * NG + cg * UE + e;
-  T v = elem<T>::from_f32(0.f);
-  if (kp < Kg && c < Cg) v = w[(static_cast<int64_t>(g * Kg + kp) * Cg + c) * RS + tap];
-  wp[idx] = v;
+  const int row = blockIdx.x;                 // (g*nch + ch)*Kpad + kp
+  const int kp = row % Kpad, gc = row / Kpad;
+  const int ch = gc % nch, g = gc / nch;
+  const int rowlen = RS * NG * UE;
+  T* dst = wp + static_cast<int64_t>(row) * rowlen;
+  const bool krow = kp < Kg;
+  const T* src = w + static_cast<int64_t>(g * Kg + (krow ? kp : 0)) * Cg * RS;
+  for (int i = threadIdx.x; i < rowlen; i += 256) {
+    const int e = i % UE, rest = i / UE;
+    const int cg = rest % NG, tap = rest / NG;
+    const int c = (ch * NG + cg) * UE + e;
+    T v = elem<T>::from_f32(0.f);
+    if (krow && c < Cg) v = src[c * RS + tap];
+    dst[i] = v;
+  }
 }
 
 // Sum of the split partials, plus bias, ReLU, rounding to the output type;
-// four consecutive outputs per thread.
+// four consecutive outputs per thread (flat index: outputs stay below 2^31).
 template <typename T>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, const T* __restrict__ bias,
-                                                            T* __restrict__ y, int64_t total, int64_t PQ, int K,
+                                                            T* __restrict__ y, int total, int slab, int PQ, int K,
                                                             int splits, int relu) {
-  const int64_t i0 = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
+  const int i0 = (blockIdx.x * 256 + threadIdx.x) * 4;
   if (i0 >= total) return;
-  const int n4 = total - i0 < 4 ? static_cast<int>(total - i0) : 4;
+  const int n4 = total - i0 < 4 ? total - i0 : 4;
   float sum[4] = {0.f, 0.f, 0.f, 0.f};
   for (int s = 0; s < splits; ++s) {
-    const float* p = part + s * total + i0;
-    if (n4 == 4 && (reinterpret_cast<uintptr_t>(p) & 15) == 0) {
-      const float4 v = *reinterpret_cast<const float4*>(p);
+    const float* p = part + static_cast<int64_t>(s) * slab + i0;
+    if (n4 == 4) {
+      const float4 v = *reinterpret_cast<const float4*>(p);  // slabs and i0 are multiples of 4 floats
       sum[0] += v.x; sum[1] += v.y; sum[2] += v.z; sum[3] += v.w;
     } else {
       for (int e = 0; e < n4; ++e) sum[e] += p[e];
     }
   }
   for (int e = 0; e < n4; ++e) {
-    const int64_t i = i0 + e;
+    const int i = i0 + e;
     float v = sum[e];
-    if (bias) v += elem<T>::load(bias + static_cast<int>((i / PQ) % K));
+    if (bias) v += elem<T>::load(bias + (i / PQ) % K);
     if (relu) v = fmaxf(v, 0.f);
     elem<T>::store(y + i, v);
   }
@@ -548,7 +601,9 @@ bool make_plan(const Shape& s, IgPlan& pl, int64_t N1 = -1) {
       a.UR = (2 * a.steps) | 1;
       a.PS = ng | 1;
       a.xs_units = a.VR * a.Wv * a.PS;
-      const size_t lds = ((size_t)pl.BM * a.UR + (size_t)a.xs_units) * 16 + (size_t)2 * a.steps * 4;
+      size_t lds = ((size_t)pl.BM * a.UR + (size_t)a.xs_units) * 16 + (size_t)2 * a.steps * 4;
+      const size_t stage = (size_t)4 * 32 * (BN / 2 + 4) * sizeof(float);  // epilogue staging
+      if (lds < stage) lds = stage;
       if (lds > limit) continue;
       pl.NG = ng;
       pl.lds = lds;
@@ -556,7 +611,8 @@ bool make_plan(const Shape& s, IgPlan& pl, int64_t N1 = -1) {
       pl.wp_bytes = (size_t)s.G * a.nch * a.Kpad * a.units * 16;
       if (pl.wp_bytes > (size_t)kMaxLaunchBytes) return false;
       choose_splits(s, pl);
-      pl.part_bytes = a.splits > 1 ? (size_t)a.splits * N1 * s.K * s.P * s.Q * sizeof(float) : 0;
+      a.slab = (int)((N1 * s.K * s.P * s.Q + 3) & ~(int64_t)3);
+      pl.part_bytes = a.splits > 1 ? (size_t)a.splits * a.slab * sizeof(float) : 0;
       return true;
     }
   }
@@ -568,20 +624,23 @@ size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 template <typename T, int BM, int NG, int RST>
 hipError_t launch_one(const IgPlan& pl, const IgArgs& a, hipStream_t stream) {
   const auto kern = implicit_gemm_kernel<T, BM, NG, RST>;
-  if (pl.lds > 64 * 1024) {
+  // Raise the kernel's dynamic-LDS limit once (not per call, so that calls
+  // can be captured into a graph after the first one).
+  static std::atomic<int> lds_limit{64 * 1024};
+  if ((int)pl.lds > lds_limit.load()) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds);
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsLimit);
     if (e != hipSuccess) return e;
+    lds_limit.store((int)kLdsLimit);
   }
   const dim3 grid((a.NPQ + BN - 1) / BN, a.ktiles * a.G, a.splits);
   hipLaunchKernelGGL(kern, grid, dim3(kThreads), pl.lds, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
-  const int64_t total = (int64_t)a.N * a.K * a.P * a.Q;
-  const int64_t blocks = (total + 1023) / 1024;
-  hipLaunchKernelGGL(splitk_reduce_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, stream, a.partial,
-                     reinterpret_cast<const T*>(a.b), reinterpret_cast<T*>(a.y), total, (int64_t)a.P * a.Q, a.K,
-                     a.splits, a.relu);
+  const int total = a.N * a.K * a.P * a.Q;
+  hipLaunchKernelGGL(splitk_reduce_kernel<T>, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, stream,
+                     a.partial, reinterpret_cast<const T*>(a.b), reinterpret_cast<T*>(a.y), total, a.slab, a.P * a.Q,
+                     a.K, a.splits, a.relu);
   return hipGetLastError();
 }
 
@@ -602,10 +661,9 @@ hipError_t launch_typed(const Shape& s, const void* x, const void* w, const void
   T* wp = reinterpret_cast<T*>(ws);
   float* part = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + align256(pl.wp_bytes));
   {
-    const int64_t total = (int64_t)(pl.wp_bytes / sizeof(T));
-    hipLaunchKernelGGL(pack_filters_kernel<T>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
-                       reinterpret_cast<const T*>(w), wp, total, (int)s.Kg, (int)s.Cg, (int)(s.R * s.S), pl.NG,
-                       pl.a.nch, pl.a.Kpad);
+    const unsigned rows = (unsigned)(s.G * pl.a.nch * pl.a.Kpad);
+    hipLaunchKernelGGL(pack_filters_kernel<T>, dim3(rows), dim3(256), 0, stream, reinterpret_cast<const T*>(w), wp,
+                       (int)s.Kg, (int)s.Cg, (int)(s.R * s.S), pl.NG, pl.a.nch, pl.a.Kpad);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -625,6 +683,7 @@ hipError_t launch_typed(const Shape& s, const void* x, const void* w, const void
     a.wp_bytes = (uint32_t)pl.wp_bytes;
     a.b = b;
     a.partial = part;
+    a.vec_out = (s.P * s.Q) % 8 == 0 && reinterpret_cast<uintptr_t>(a.y) % 16 == 0;
     hipError_t e;
     if (pl.BM == 64)
       e = pl.NG == 2 ? launch_rst<T, 64, 2>(cur, a, stream) : launch_rst<T, 64, 1>(cur, a, stream);

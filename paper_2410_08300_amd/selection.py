@@ -167,25 +167,47 @@ def supported_algos(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, rel
 
 
 def time_conv(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, algo="default", relu=False,
-              warmup=2, reps=5, launches=10):
-    """Median milliseconds per call: ``launches`` back-to-back launches
-    between two HIP events on the current stream (prebuilt arguments, so
-    the queue stays ahead of the GPU), median over ``reps`` trials."""
+              warmup=2, reps=5, launches=10, graph=True):
+    """Median milliseconds per call of the GPU work of one convolution.
+
+    The call's arguments are marshalled once; ``launches`` calls are then
+    captured in a HIP graph and replayed between two HIP events (so host
+    launch overhead is not counted), median over ``reps`` replays.  With
+    ``graph=False`` (or if capture fails) the calls are launched back to back
+    instead, which also counts whatever host time the queue cannot hide.
+    """
     x, w = x.contiguous(), w.contiguous()
     b = None if b is None else b.contiguous()
-    call, out = prepare(x, w, b, stride, padding, dilation, groups, algo=algo, relu=relu)
-    for _ in range(warmup):
-        call()
-    times = []
-    for _ in range(reps):
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(launches):
+    stream = torch.cuda.Stream(x.device)
+    with torch.cuda.stream(stream):
+        call, out = prepare(x, w, b, stride, padding, dilation, groups, algo=algo, relu=relu)
+        for _ in range(warmup):
             call()
-        e1.record()
-        e1.synchronize()
-        times.append(e0.elapsed_time(e1) / launches)
+        stream.synchronize()
+        g = None
+        if graph:
+            try:
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=stream):
+                    for _ in range(launches):
+                        call()
+                g.replay()
+                stream.synchronize()
+            except RuntimeError:
+                g = None
+        times = []
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            if g is not None:
+                g.replay()
+            else:
+                for _ in range(launches):
+                    call()
+            e1.record(stream)
+            e1.synchronize()
+            times.append(e0.elapsed_time(e1) / launches)
     times.sort()
     return times[len(times) // 2]
 

@@ -146,8 +146,9 @@ def test_argument_errors_before_any_device_call():
     need = _lib.workspace_bytes(d, "winograd")
     assert _lib.conv2d_raw(A, B, Bb, Y, d, "winograd", 5 << 20, need - 1, None) == _lib.CONV_ERR_WORKSPACE
     assert _lib.conv2d_raw(A, B, Bb, Y, d, "winograd", None, need, None) == _lib.CONV_ERR_WORKSPACE
-    # output overlapping the workspace
+    # output overlapping the workspace; workspace not 256-byte aligned
     assert _lib.conv2d_raw(A, B, Bb, Y, d, "winograd", Y + 16, need, None) == _lib.CONV_ERR_INVALID_ARG
+    assert _lib.conv2d_raw(A, B, Bb, Y, d, "winograd", (5 << 20) + 16, need, None) == _lib.CONV_ERR_INVALID_ARG
     # unsupported algorithm for the shape
     d5 = _lib.make_desc(1, 4, 8, 8, 4, 5, 5, 1, 2, 1, 1, "f32", bias=True)
     assert _lib.conv2d_raw(A, B, Bb, Y, d5, "winograd", None, 0, None) == _lib.CONV_ERR_UNSUPPORTED

@@ -162,6 +162,18 @@ def test_edge_cases():
     check_full(xt.contiguous(), torch.randn(6, 9, 3, 3, generator=g), None, 1, 1, 1, 1, False, ALGOS, "strided")
     yd = cs.conv2d(xt.to(DEV), torch.randn(6, 9, 3, 3, generator=g).to(DEV), None, 1, 1)
     assert yd.shape == (2, 6, 8, 12)
+    # output written into a view that is not 16-byte aligned (2-byte offset)
+    x = torch.randn(2, 16, 8, 8, generator=g).to(torch.bfloat16)
+    w = (torch.randn(40, 16, 3, 3, generator=g) * 0.2).to(torch.bfloat16)
+    ref = oracle.conv2d(f64(x), f64(w), None, 1, 1)
+    for algo in ALGOS:
+        buf = torch.zeros(2 * 40 * 64 + 1, device=DEV, dtype=torch.bfloat16)
+        out = buf[1:].view(2, 40, 8, 8)
+        say("case unaligned output", algo)
+        cs.conv2d(x.to(DEV), w.to(DEV), None, 1, 1, algo=algo, out=out)
+        torch.cuda.synchronize()
+        assert rel_err(f64(out), ref) <= tolerance("bf16", algo)
+        assert float(buf[0]) == 0.0
 
 
 def test_unsupported_and_invalid_calls_raise():
