@@ -56,27 +56,34 @@ def build_plan(layers, wl_index, device, select, algos_allowed=None):
             else:
                 cache[key] = (select, {})
         algo, timings = cache[key]
+        pk = cs.pack_filters(w, tuple(x.shape), L.stride, L.pad, L.dilation, L.groups, algo, b is not None, L.relu)
         plan.append(dict(layer=L, x=x, w=w, b=b, y=y, desc=desc, algo=algo, algo_id=_lib.algo_id(algo),
-                         ws_bytes=_lib.workspace_bytes(desc, algo), timings=timings))
-    ws_max = max(p["ws_bytes"] for p in plan)
+                         ws_bytes=_lib.workspace_bytes(desc, algo), package=pk,
+                         pk_ws_bytes=_lib.prepacked_workspace_bytes(desc, algo), timings=timings,
+                         describe=_lib.describe(desc, algo)))
+    ws_max = max(max(p["ws_bytes"], p["pk_ws_bytes"]) for p in plan)
     ws = torch.empty(max(ws_max, 1), dtype=torch.uint8, device=device)
     return plan, ws
 
 
-def make_step(plan, ws, stream_ptr):
+def make_step(plan, ws, stream_ptr, prepacked=False):
     """A closure that enqueues every layer through the C ABI with prebuilt
-    arguments (no allocation, no Python-side shape work per call)."""
+    arguments (no allocation, no Python-side shape work per call).  With
+    prepacked=True each layer uses its filter package (conv2d_prepacked);
+    otherwise conv2d() rebuilds the package from the filters every call."""
     import ctypes
     from paper_2410_08300_amd import _lib
 
     L = _lib.lib()
-    fn = L.conv2d
+    fn = L.conv2d_prepacked if prepacked else L.conv2d
     calls = []
     for p in plan:
-        calls.append((ctypes.c_void_p(p["x"].data_ptr()), ctypes.c_void_p(p["w"].data_ptr()),
+        wsrc = p["package"] if prepacked else p["w"]
+        calls.append((ctypes.c_void_p(p["x"].data_ptr()), ctypes.c_void_p(wsrc.data_ptr()),
                       ctypes.c_void_p(p["b"].data_ptr() if p["b"] is not None else 0),
                       ctypes.c_void_p(p["y"].data_ptr()), ctypes.byref(p["desc"]), p["algo_id"],
-                      ctypes.c_void_p(ws.data_ptr()), ctypes.c_size_t(p["ws_bytes"]),
+                      ctypes.c_void_p(ws.data_ptr()),
+                      ctypes.c_size_t(p["pk_ws_bytes"] if prepacked else p["ws_bytes"]),
                       ctypes.c_void_p(stream_ptr)))
 
     def step(events=None):
@@ -154,6 +161,9 @@ def main():
     ap.add_argument("--workload", default="resnet50")
     ap.add_argument("--select", default="measured")
     ap.add_argument("--graph", action="store_true", help="replay the step as a captured HIP graph")
+    ap.add_argument("--prepacked", action="store_true",
+                    help="time the step with filter packages built before timing (conv2d_prepacked); by default "
+                         "every call rebuilds them from the filters")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--sweep", default=None, help="write per-layer, per-algorithm timings to this JSONL file")
@@ -179,63 +189,71 @@ def main():
     layers = W.layers(wl)
     log("bench: workload %s, %d layers, select=%s" % (wl, len(layers), args.select))
     plan, ws = build_plan(layers, W.WORKLOADS.index(wl), dev, args.select)
+    torch.cuda.synchronize()  # filter packages were built on the default stream
     for p in plan:
         L = p["layer"]
         log("  %-24s %-14s %s" % (L.name, p["algo"],
                                   " ".join("%s=%.4f" % kv for kv in sorted(p["timings"].items()))))
+        log("      %s" % p["describe"])
     # Graph capture needs a stream other than the default one; eager runs use
     # the same stream so both modes launch identically.
     stream = torch.cuda.Stream(dev) if args.graph else torch.cuda.current_stream(dev)
     torch.cuda.set_stream(stream)
     step = make_step(plan, ws, stream.cuda_stream)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    graph = None
-    if args.graph:
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph, stream=stream):
-            step()
-        torch.cuda.synchronize()
+    def timed(step_fn):
+        """Warm-up, optional graph capture, then K timed steps bracketed by
+        device synchronisation; per-layer HIP events on the launch stream."""
         for _ in range(args.warmup):
-            graph.replay()
+            step_fn()
         torch.cuda.synchronize()
+        graph = None
+        if args.graph:
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph, stream=stream):
+                step_fn()
+            torch.cuda.synchronize()
+            for _ in range(args.warmup):
+                graph.replay()
+            torch.cuda.synchronize()
+        nl = len(plan)
+        ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(nl)]
+              for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        if graph is not None:
+            for _ in range(args.steps):
+                graph.replay()
+        else:
+            for k in range(args.steps):
+                step_fn(ev[k])
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        ms = (t1 - t0) * 1e3 / args.steps
+        if graph is None:
+            lms = [sum(ev[k][i][0].elapsed_time(ev[k][i][1]) for k in range(args.steps)) / args.steps
+                   for i in range(nl)]
+        else:
+            # graph replay: per-layer times from eager steps with events
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(nl)]
+            lms = [0.0] * nl
+            for _ in range(args.steps):
+                step_fn(evs)
+                torch.cuda.synchronize()
+                for i in range(nl):
+                    lms[i] += evs[i][0].elapsed_time(evs[i][1]) / args.steps
+        return ms, lms
 
-    # Timed region: K whole steps, per-layer HIP events on the launch stream.
-    nl = len(plan)
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(nl)]
-          for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    if graph is not None:
-        for _ in range(args.steps):
-            graph.replay()
+    step_pk = make_step(plan, ws, stream.cuda_stream, prepacked=True)
+    ms_unpk, lms_unpk = timed(step)
+    ms_pk, lms_pk = timed(step_pk)
+    if args.prepacked:
+        ms_per_step, layer_ms, ms_other = ms_pk, lms_pk, ms_unpk
     else:
-        for k in range(args.steps):
-            step(ev[k])
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
+        ms_per_step, layer_ms, ms_other = ms_unpk, lms_unpk, ms_pk
 
     total_flops = sum(p["layer"].flops for p in plan)
     value = total_flops / (ms_per_step * 1e-3) / 1e12
-
-    # Per-layer event times (eager mode only): mean over the K steps.
-    layer_ms = None
-    if graph is None:
-        layer_ms = [sum(ev[k][i][0].elapsed_time(ev[k][i][1]) for k in range(args.steps)) / args.steps
-                    for i in range(nl)]
-    else:
-        # graph replay: time each layer with events outside the graph
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(nl)]
-        layer_ms = [0.0] * nl
-        for _ in range(args.steps):
-            step(evs)
-            torch.cuda.synchronize()
-            for i in range(nl):
-                layer_ms[i] += evs[i][0].elapsed_time(evs[i][1]) / args.steps
 
     dtype = plan[0]["layer"].dtype
     by_algo = {}
@@ -244,15 +262,29 @@ def main():
         a[0] += ms
         a[1] += p["layer"].flops
         a[2] += 1
-    dom = max(by_algo, key=lambda a: by_algo[a][0])
-    dom_ms, dom_flops, dom_n = by_algo[dom]
-    achieved = dom_flops / (dom_ms * 1e-3) / 1e12
+
+    # Roofline of the dominant kernel: the main-kernel instantiation with the
+    # largest share of the step.  Measured on the prepacked step, counting the
+    # layers where that kernel is the call's only launch (no split-K reduce),
+    # so each HIP-event interval around a call times exactly one launch.
+    def main_kernel(desc):
+        ks = desc.split("kernels=")[1].split(" ")[0].split(";")
+        return [k for k in ks if not k.startswith("pack_filters") and not k.startswith("wino_filter")]
+    share = {}
+    for p, ms in zip(plan, lms_pk):
+        ks = main_kernel(p["describe"])
+        if len(ks) == 1:
+            share[ks[0]] = share.get(ks[0], 0.0) + ms
+    dom = max(share, key=share.get)
+    single = [(p, ms) for p, ms in zip(plan, lms_pk) if main_kernel(p["describe"]) == [dom]]
+    dom_ms = sum(ms for _, ms in single)
+    dom_flops = sum(p["layer"].flops for p, _ in single)
+    achieved = dom_flops / (dom_ms * 1e-3) / 1e12 if dom_ms > 0 else 0.0
     peak = PEAKS_TFLOPS[dtype]
-    kernel_names = {"implicit_gemm": "implicit_gemm_kernel", "direct": "direct_tile_kernel",
-                    "im2col_gemm": "im2col_kernel + gemm_nt_kernel", "winograd": "wino_* + gemm_nt_kernel"}
     roofline = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                "traffic": None, "kernel": kernel_names.get(dom, dom), "launches_per_step": dom_n,
-                "time_share": dom_ms / sum(layer_ms)}
+                "traffic": None, "kernel": dom, "launches_per_step": len(single),
+                "avg_launch_us": dom_ms * 1e3 / max(len(single), 1),
+                "time_share_prepacked_step": share[dom] / sum(lms_pk)}
 
     # The 3x3 layers of the workload (the headline target for ResNet-50).
     sel = [(p, ms) for p, ms in zip(plan, layer_ms) if p["layer"].r == 3]
@@ -264,6 +296,8 @@ def main():
                                "tflops": f3 / (t3 * 1e-3) / 1e12, "frac_peak": f3 / (t3 * 1e-3) / 1e12 / peak}
     extra["sum_layer_event_ms"] = sum(layer_ms)
     extra["algos"] = {a: v[2] for a, v in by_algo.items()}
+    other = "per_call_filter_packing" if args.prepacked else "prepacked_filters"
+    extra[other] = {"ms_per_step": ms_other, "tflops": total_flops / (ms_other * 1e-3) / 1e12}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -274,8 +308,9 @@ def main():
            "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
            "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": dtype, "data": "synthetic (seeded normal inputs, Kaiming-normal weights)",
-           "config": {"workload": "%s conv layers (%d convs), batch %d, %s data, fp32 accumulate, %s"
-                                  % (wl, len(layers), nbatch, dtype, "graph replay" if graph else "eager launches"),
+           "config": {"workload": "%s conv layers (%d convs), batch %d, %s data, fp32 accumulate, %s, %s"
+                                  % (wl, len(layers), nbatch, dtype, "graph replay" if args.graph else "eager launches",
+                                     "prepacked filters" if args.prepacked else "filters packed every call"),
                       "global_batch": nbatch, "layers": len(layers), "parallelism": "none (1 GPU)"},
            "roofline": roofline, "cpu_baseline": cpu, "detail": extra}
     print(json.dumps(out), flush=True)

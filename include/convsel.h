@@ -122,6 +122,35 @@ conv_algo_t conv2d_default_algo(const conv2d_desc_t* desc);
 conv_status_t conv2d(const void* x, const void* w, const void* b, void* y, const conv2d_desc_t* desc,
                      conv_algo_t algo, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Filter packages.  Implicit GEMM and Winograd first rearrange the filters
+ * (implicit GEMM: into its tile layout, zero-padded; Winograd: the filter
+ * transform U below); conv2d() redoes that in its workspace on every call.
+ * An inference caller whose filters do not change can build the package
+ * once and call conv2d_prepacked() instead, which then runs only the work
+ * that depends on the input.  For direct and IM2COL + GEMM the package is a
+ * copy of the filters.
+ *  - conv2d_packed_filter_bytes: size of the package.
+ *  - conv2d_pack_filters: writes it (`packed` 256-byte aligned, not
+ *    overlapping w; enqueued on `stream`).  Same errors as conv2d_check,
+ *    INVALID_ARG for NULL / misaligned / overlapping pointers.
+ *  - conv2d_prepacked_workspace_bytes: workspace of conv2d_prepacked()
+ *    (conv2d's workspace minus the package).
+ *  - conv2d_prepacked: as conv2d() with the package (256-byte aligned) in
+ *    place of w; same algorithm and descriptor as when the package was
+ *    built. */
+conv_status_t conv2d_packed_filter_bytes(const conv2d_desc_t* desc, conv_algo_t algo, size_t* bytes);
+conv_status_t conv2d_pack_filters(const void* w, void* packed, const conv2d_desc_t* desc, conv_algo_t algo,
+                                  void* stream);
+conv_status_t conv2d_prepacked_workspace_bytes(const conv2d_desc_t* desc, conv_algo_t algo, size_t* bytes);
+conv_status_t conv2d_prepacked(const void* x, const void* packed, const void* b, void* y,
+                               const conv2d_desc_t* desc, conv_algo_t algo, void* workspace, size_t workspace_bytes,
+                               void* stream);
+
+/* One line describing how conv2d() runs this layer with `algo` (the kernels
+ * it launches, tile and grid, workspace sizes), written NUL-terminated into
+ * buf (truncated to len - 1 characters).  Host only. */
+conv_status_t conv2d_describe(const conv2d_desc_t* desc, conv_algo_t algo, char* buf, size_t len);
+
 /* The column matrix of the IM2COL + GEMM algorithm for all N images: col is
  * N x G x (P*Q) x (Cg*R*S), element [n][g][p*Q+q][(c*R + r)*S + s] =
  * x[n, g*Cg + c, p*stride_h - pad_h + r*dil_h, q*stride_w - pad_w + s*dil_w]

@@ -8,8 +8,9 @@ The compute runs in hand-written HIP kernels behind a C ABI
 streams.
 """
 from ._lib import Conv2dError, ALGOS
-from .conv import conv2d, im2col, winograd_filter_transform, winograd_input_transform
+from .conv import (conv2d, conv2d_prepacked, pack_filters, describe, im2col, winograd_filter_transform,
+                   winograd_input_transform)
 from .selection import AlgoTable, Conv2dSwap, swap_conv2d, select_fastest, tune, time_conv, supported_algos
 
-__all__ = ["Conv2dError", "ALGOS", "conv2d", "im2col", "winograd_filter_transform", "winograd_input_transform",
+__all__ = ["Conv2dError", "ALGOS", "conv2d", "conv2d_prepacked", "pack_filters", "describe", "im2col", "winograd_filter_transform", "winograd_input_transform",
            "AlgoTable", "Conv2dSwap", "swap_conv2d", "select_fastest", "tune", "time_conv", "supported_algos"]

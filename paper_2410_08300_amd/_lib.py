@@ -21,7 +21,8 @@ ALGO_NAMES = {v: k for k, v in ALGOS.items()}
 DTYPES = {"f32": 0, "bf16": 1}
 
 EXPORTED = ("conv2d_output_shape", "conv2d_check", "conv2d_workspace_bytes", "conv2d_default_algo",
-            "conv2d", "conv2d_im2col", "conv2d_winograd_filter_transform",
+            "conv2d", "conv2d_packed_filter_bytes", "conv2d_pack_filters", "conv2d_prepacked_workspace_bytes",
+            "conv2d_prepacked", "conv2d_describe", "conv2d_im2col", "conv2d_winograd_filter_transform",
             "conv2d_winograd_input_transform", "conv2d_status_string", "conv2d_algo_name",
             "conv2d_algo_from_name")
 
@@ -70,6 +71,16 @@ def lib():
         L.conv2d_default_algo.restype = i32
         L.conv2d.argtypes = [vp, vp, vp, vp, dp, i32, vp, ctypes.c_size_t, vp]
         L.conv2d.restype = i32
+        L.conv2d_packed_filter_bytes.argtypes = [dp, i32, ctypes.POINTER(ctypes.c_size_t)]
+        L.conv2d_packed_filter_bytes.restype = i32
+        L.conv2d_pack_filters.argtypes = [vp, vp, dp, i32, vp]
+        L.conv2d_pack_filters.restype = i32
+        L.conv2d_prepacked_workspace_bytes.argtypes = [dp, i32, ctypes.POINTER(ctypes.c_size_t)]
+        L.conv2d_prepacked_workspace_bytes.restype = i32
+        L.conv2d_prepacked.argtypes = [vp, vp, vp, vp, dp, i32, vp, ctypes.c_size_t, vp]
+        L.conv2d_prepacked.restype = i32
+        L.conv2d_describe.argtypes = [dp, i32, ctypes.c_char_p, ctypes.c_size_t]
+        L.conv2d_describe.restype = i32
         L.conv2d_im2col.argtypes = [vp, vp, dp, vp]
         L.conv2d_im2col.restype = i32
         L.conv2d_winograd_filter_transform.argtypes = [vp, vp, dp, vp]
@@ -141,6 +152,34 @@ def workspace_bytes(desc, algo):
     return out.value
 
 
+def packed_filter_bytes(desc, algo):
+    out = ctypes.c_size_t()
+    st = lib().conv2d_packed_filter_bytes(ctypes.byref(desc), algo_id(algo) if isinstance(algo, str) else int(algo),
+                                          ctypes.byref(out))
+    if st != CONV_OK:
+        raise Conv2dError(st, "conv2d_packed_filter_bytes")
+    return out.value
+
+
+def prepacked_workspace_bytes(desc, algo):
+    out = ctypes.c_size_t()
+    st = lib().conv2d_prepacked_workspace_bytes(ctypes.byref(desc),
+                                                algo_id(algo) if isinstance(algo, str) else int(algo),
+                                                ctypes.byref(out))
+    if st != CONV_OK:
+        raise Conv2dError(st, "conv2d_prepacked_workspace_bytes")
+    return out.value
+
+
+def describe(desc, algo):
+    buf = ctypes.create_string_buffer(1024)
+    st = lib().conv2d_describe(ctypes.byref(desc), algo_id(algo) if isinstance(algo, str) else int(algo), buf,
+                               len(buf))
+    if st != CONV_OK:
+        raise Conv2dError(st, "conv2d_describe")
+    return buf.value.decode()
+
+
 def default_algo(desc):
     return ALGO_NAMES[lib().conv2d_default_algo(ctypes.byref(desc))]
 
@@ -164,11 +203,12 @@ def wino_input_raw(x_ptr, v_ptr, desc, stream):
 
 
 class PreparedCall:
-    """A conv2d() call with every argument converted once, for repeated
-    launches with no per-call Python work beyond the foreign call itself."""
+    """A conv2d() (or, with prepacked=True, conv2d_prepacked()) call with
+    every argument converted once, for repeated launches with no per-call
+    Python work beyond the foreign call itself."""
 
-    def __init__(self, x_ptr, w_ptr, b_ptr, y_ptr, desc, algo, ws_ptr, ws_bytes, stream):
-        self._fn = lib().conv2d
+    def __init__(self, x_ptr, w_ptr, b_ptr, y_ptr, desc, algo, ws_ptr, ws_bytes, stream, prepacked=False):
+        self._fn = lib().conv2d_prepacked if prepacked else lib().conv2d
         self._desc = desc  # keep alive: passed by reference
         self._args = (ctypes.c_void_p(x_ptr), ctypes.c_void_p(w_ptr), ctypes.c_void_p(b_ptr or 0),
                       ctypes.c_void_p(y_ptr), ctypes.byref(desc),

@@ -3,7 +3,9 @@
 // and dispatch to the kernel launchers.  All checks run on the host before
 // the first HIP call.
 #include <mutex>
+#include <stdio.h>
 #include <string.h>
+#include <string>
 
 #include "../../include/convsel.h"
 #include "kernels.hpp"
@@ -92,37 +94,48 @@ int64_t im2col_batch(const Shape& s, size_t* bytes) {
   return nb;
 }
 
+size_t wino_u_bytes(const Shape& s) { return (size_t)16 * s.K * s.C * s.esize(); }
+
+// Winograd workspace: [U (unless prepacked)] [V for nb images] [M for nb images].
 struct WinoLayout {
   int64_t nb, TPQ;
   size_t v_off, m_off, total;
 };
 
-WinoLayout wino_layout(const Shape& s) {
+WinoLayout wino_layout(const Shape& s, bool with_u) {
   WinoLayout L;
   L.TPQ = ((s.P + 1) / 2) * ((s.Q + 1) / 2);
-  const size_t u_bytes = (size_t)16 * s.K * s.C * s.esize();
   const size_t v_img = (size_t)16 * L.TPQ * s.C * s.esize();
   const size_t m_img = (size_t)16 * s.K * L.TPQ * 4;
   int64_t nb = (int64_t)(kWorkspaceCap / (v_img + m_img));
   if (nb < 1) nb = 1;
   if (nb > s.N) nb = s.N;
   L.nb = nb;
-  L.v_off = align256(u_bytes);
+  L.v_off = with_u ? align256(wino_u_bytes(s)) : 0;
   L.m_off = align256(L.v_off + nb * v_img);
   L.total = L.m_off + nb * m_img;
   return L;
 }
 
-size_t workspace_for(const Shape& s, conv_algo_t algo) {
+// Workspace of conv2d() (prepacked = false) or conv2d_prepacked().
+size_t workspace_for(const Shape& s, conv_algo_t algo, bool prepacked = false) {
   if (s.N == 0) return 0;
   if (algo == CONV_ALGO_IM2COL_GEMM) {
     size_t b = 0;
     im2col_batch(s, &b);
     return b;
   }
-  if (algo == CONV_ALGO_WINOGRAD) return wino_layout(s).total;
-  if (algo == CONV_ALGO_IMPLICIT_GEMM) return convsel::implicit_gemm_workspace(s);
+  if (algo == CONV_ALGO_WINOGRAD) return wino_layout(s, !prepacked).total;
+  if (algo == CONV_ALGO_IMPLICIT_GEMM)
+    return prepacked ? convsel::implicit_gemm_split_bytes(s) : convsel::implicit_gemm_workspace(s);
   return 0;
+}
+
+// Size of the filter package of conv2d_pack_filters().
+size_t packed_filter_bytes(const Shape& s, conv_algo_t algo) {
+  if (algo == CONV_ALGO_IMPLICIT_GEMM) return convsel::implicit_gemm_packed_bytes(s);
+  if (algo == CONV_ALGO_WINOGRAD) return wino_u_bytes(s);
+  return (size_t)s.K * s.Cg * s.R * s.S * s.esize();  // the filters themselves
 }
 
 bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
@@ -159,13 +172,19 @@ conv_status_t from_hip(hipError_t e) {
   return CONV_ERR_DEVICE;
 }
 
-conv_status_t run(const Shape& s, conv_algo_t algo, const void* x, const void* w, const void* b, void* y,
-                  void* ws, hipStream_t st) {
+// Runs the algorithm.  `wpk` is the filter package of conv2d_pack_filters()
+// (prepacked calls) or NULL, in which case the package is built in the
+// workspace first (implicit GEMM, Winograd) or the filters are used as they
+// are (direct, IM2COL + GEMM).
+conv_status_t run(const Shape& s, conv_algo_t algo, const void* x, const void* w, const void* wpk, const void* b,
+                  void* y, void* ws, hipStream_t st) {
   using namespace convsel;
+  const void* filt = wpk ? wpk : w;
   switch (algo) {
     case CONV_ALGO_DIRECT:
-      return from_hip(launch_direct(s, x, w, b, y, st));
+      return from_hip(launch_direct(s, x, filt, b, y, st));
     case CONV_ALGO_IMPLICIT_GEMM:
+      if (wpk) return from_hip(launch_implicit_main(s, x, wpk, b, y, ws, st));
       return from_hip(launch_implicit_gemm(s, x, w, b, y, ws, st));
     case CONV_ALGO_IM2COL_GEMM: {
       const int64_t nb = im2col_batch(s, nullptr);
@@ -175,7 +194,7 @@ conv_status_t run(const Shape& s, conv_algo_t algo, const void* x, const void* w
         hipError_t e = launch_im2col(s, x, ws, n0, cnt, st);
         if (e != hipSuccess) return from_hip(e);
         GemmArgs g;
-        g.A = w;
+        g.A = filt;
         g.B = ws;
         g.C = (char*)y + (size_t)n0 * s.K * PQ * s.esize();
         g.bias = b;
@@ -194,17 +213,20 @@ conv_status_t run(const Shape& s, conv_algo_t algo, const void* x, const void* w
       return CONV_OK;
     }
     case CONV_ALGO_WINOGRAD: {
-      const WinoLayout L = wino_layout(s);
+      const WinoLayout L = wino_layout(s, wpk == nullptr);
       char* base = (char*)ws;
-      void* U = base;
+      const void* U = wpk;
+      if (!wpk) {
+        const hipError_t e = launch_wino_filter(s, w, base, st);
+        if (e != hipSuccess) return from_hip(e);
+        U = base;
+      }
       void* V = base + L.v_off;
       float* M = (float*)(base + L.m_off);
-      hipError_t e = launch_wino_filter(s, w, U, st);
-      if (e != hipSuccess) return from_hip(e);
       for (int64_t n0 = 0; n0 < s.N; n0 += L.nb) {
         const int64_t cnt = s.N - n0 < L.nb ? s.N - n0 : L.nb;
         const int64_t Tc = cnt * L.TPQ;
-        e = launch_wino_input(s, x, V, n0, cnt, st);
+        hipError_t e = launch_wino_input(s, x, V, n0, cnt, st);
         if (e != hipSuccess) return from_hip(e);
         GemmArgs g;
         g.A = U; g.B = V; g.C = M; g.bias = nullptr;
@@ -227,6 +249,54 @@ conv_status_t run(const Shape& s, conv_algo_t algo, const void* x, const void* w
     default:
       return CONV_ERR_INVALID_ARG;
   }
+}
+
+// Shared checks of conv2d() and conv2d_prepacked() up to the device call.
+conv_status_t prepare_call(const conv2d_desc_t* desc, conv_algo_t* algo, Shape* s, const void* x, const void* w,
+                           const void* b, void* y, void* workspace, size_t workspace_bytes, bool prepacked) {
+  conv_status_t st = validate(desc, s);
+  if (st != CONV_OK) return st;
+  if (*algo == CONV_ALGO_DEFAULT) *algo = default_rule(*s);
+  st = support(*s, *algo);
+  if (st != CONV_OK) return st;
+  if (s->N == 0) return CONV_OK;
+  if (!x || !w || !y || (s->bias != (b != nullptr))) return CONV_ERR_INVALID_ARG;
+  const size_t need = workspace_for(*s, *algo, prepacked);
+  if (workspace_bytes < need || (need > 0 && !workspace)) return CONV_ERR_WORKSPACE;
+  if (need > 0 && reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return CONV_ERR_INVALID_ARG;
+  const size_t es = (size_t)s->esize();
+  const size_t ybytes = (size_t)s->N * s->K * s->P * s->Q * es;
+  const size_t wbytes = prepacked ? packed_filter_bytes(*s, *algo) : (size_t)s->K * s->Cg * s->R * s->S * es;
+  if (prepacked && reinterpret_cast<uintptr_t>(w) % 256 != 0) return CONV_ERR_INVALID_ARG;
+  if (overlaps(y, ybytes, x, (size_t)s->N * s->C * s->H * s->W * es) || overlaps(y, ybytes, w, wbytes) ||
+      overlaps(y, ybytes, b, s->bias ? (size_t)s->K * es : 0) || overlaps(y, ybytes, workspace, need))
+    return CONV_ERR_INVALID_ARG;
+  return ensure_device();
+}
+
+// Copies the filters into a package (algorithms that use them as they are):
+// 16-byte units, then the remaining bytes one per thread.
+__global__ void copy16_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst, int64_t n16) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i < n16) dst[i] = src[i];
+}
+__global__ void copy1_kernel(const unsigned char* __restrict__ src, unsigned char* __restrict__ dst, int64_t from,
+                             int64_t to) {
+  const int64_t i = from + static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i < to) dst[i] = src[i];
+}
+
+hipError_t copy_filters(const void* w, void* dst, size_t bytes, hipStream_t st) {
+  const bool aligned = reinterpret_cast<uintptr_t>(w) % 16 == 0;
+  const int64_t n16 = aligned ? (int64_t)(bytes / 16) : 0;
+  if (n16 > 0)
+    hipLaunchKernelGGL(copy16_kernel, dim3((unsigned)((n16 + 255) / 256)), dim3(256), 0, st, (const uint4*)w,
+                       (uint4*)dst, n16);
+  const int64_t from = n16 * 16, rest = (int64_t)bytes - from;
+  if (rest > 0)
+    hipLaunchKernelGGL(copy1_kernel, dim3((unsigned)((rest + 255) / 256)), dim3(256), 0, st,
+                       (const unsigned char*)w, (unsigned char*)dst, from, (int64_t)bytes);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -272,26 +342,100 @@ conv_algo_t conv2d_default_algo(const conv2d_desc_t* desc) {
 conv_status_t conv2d(const void* x, const void* w, const void* b, void* y, const conv2d_desc_t* desc,
                      conv_algo_t algo, void* workspace, size_t workspace_bytes, void* stream) {
   Shape s;
+  const conv_status_t st = prepare_call(desc, &algo, &s, x, w, b, y, workspace, workspace_bytes, false);
+  if (st != CONV_OK || s.N == 0) return st;
+  return run(s, algo, x, w, nullptr, b, y, workspace, (hipStream_t)stream);
+}
+
+conv_status_t conv2d_packed_filter_bytes(const conv2d_desc_t* desc, conv_algo_t algo, size_t* bytes) {
+  Shape s;
+  conv_status_t st = validate(desc, &s);
+  if (st != CONV_OK) return st;
+  if (!bytes) return CONV_ERR_INVALID_ARG;
+  if (algo == CONV_ALGO_DEFAULT) algo = default_rule(s);
+  st = support(s, algo);
+  if (st != CONV_OK) return st;
+  *bytes = packed_filter_bytes(s, algo);
+  return CONV_OK;
+}
+
+conv_status_t conv2d_prepacked_workspace_bytes(const conv2d_desc_t* desc, conv_algo_t algo, size_t* bytes) {
+  Shape s;
+  conv_status_t st = validate(desc, &s);
+  if (st != CONV_OK) return st;
+  if (!bytes) return CONV_ERR_INVALID_ARG;
+  if (algo == CONV_ALGO_DEFAULT) algo = default_rule(s);
+  st = support(s, algo);
+  if (st != CONV_OK) return st;
+  *bytes = workspace_for(s, algo, true);
+  return CONV_OK;
+}
+
+conv_status_t conv2d_pack_filters(const void* w, void* packed, const conv2d_desc_t* desc, conv_algo_t algo,
+                                  void* stream) {
+  Shape s;
   conv_status_t st = validate(desc, &s);
   if (st != CONV_OK) return st;
   if (algo == CONV_ALGO_DEFAULT) algo = default_rule(s);
   st = support(s, algo);
   if (st != CONV_OK) return st;
-  if (s.N == 0) return CONV_OK;
-  if (!x || !w || !y || (s.bias != (b != nullptr))) return CONV_ERR_INVALID_ARG;
-  const size_t need = workspace_for(s, algo);
-  if (workspace_bytes < need || (need > 0 && !workspace)) return CONV_ERR_WORKSPACE;
-  if (need > 0 && reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return CONV_ERR_INVALID_ARG;
-  const size_t es = (size_t)s.esize();
-  const size_t ybytes = (size_t)s.N * s.K * s.P * s.Q * es;
-  if (overlaps(y, ybytes, x, (size_t)s.N * s.C * s.H * s.W * es) ||
-      overlaps(y, ybytes, w, (size_t)s.K * s.Cg * s.R * s.S * es) ||
-      overlaps(y, ybytes, b, s.bias ? (size_t)s.K * es : 0) ||
-      overlaps(y, ybytes, workspace, need))
-    return CONV_ERR_INVALID_ARG;
+  if (!w || !packed) return CONV_ERR_INVALID_ARG;
+  if (reinterpret_cast<uintptr_t>(packed) % 256 != 0) return CONV_ERR_INVALID_ARG;
+  const size_t pbytes = packed_filter_bytes(s, algo);
+  const size_t wbytes = (size_t)s.K * s.Cg * s.R * s.S * s.esize();
+  if (overlaps(packed, pbytes, w, wbytes)) return CONV_ERR_INVALID_ARG;
   st = ensure_device();
   if (st != CONV_OK) return st;
-  return run(s, algo, x, w, b, y, workspace, (hipStream_t)stream);
+  const hipStream_t hs = (hipStream_t)stream;
+  if (algo == CONV_ALGO_IMPLICIT_GEMM) return from_hip(convsel::launch_implicit_pack(s, w, packed, hs));
+  if (algo == CONV_ALGO_WINOGRAD) return from_hip(convsel::launch_wino_filter(s, w, packed, hs));
+  return from_hip(copy_filters(w, packed, wbytes, hs));
+}
+
+conv_status_t conv2d_prepacked(const void* x, const void* packed, const void* b, void* y,
+                               const conv2d_desc_t* desc, conv_algo_t algo, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  Shape s;
+  const conv_status_t st = prepare_call(desc, &algo, &s, x, packed, b, y, workspace, workspace_bytes, true);
+  if (st != CONV_OK || s.N == 0) return st;
+  return run(s, algo, x, nullptr, packed, b, y, workspace, (hipStream_t)stream);
+}
+
+conv_status_t conv2d_describe(const conv2d_desc_t* desc, conv_algo_t algo, char* buf, size_t len) {
+  Shape s;
+  conv_status_t st = validate(desc, &s);
+  if (st != CONV_OK) return st;
+  if (!buf || len == 0) return CONV_ERR_INVALID_ARG;
+  if (algo == CONV_ALGO_DEFAULT) algo = default_rule(s);
+  st = support(s, algo);
+  if (st != CONV_OK) return st;
+  std::string d;
+  switch (algo) {
+    case CONV_ALGO_DIRECT:
+      d = s.Cg == 1 ? "direct kernels=direct_depthwise_kernel" : "direct kernels=direct_tile_kernel";
+      break;
+    case CONV_ALGO_IMPLICIT_GEMM:
+      d = convsel::implicit_gemm_describe(s);
+      break;
+    case CONV_ALGO_IM2COL_GEMM: {
+      const int64_t nb = im2col_batch(s, nullptr);
+      d = "im2col_gemm kernels=im2col_kernel;gemm_nt_kernel images_per_batch=" + std::to_string(nb);
+      break;
+    }
+    case CONV_ALGO_WINOGRAD: {
+      const WinoLayout L = wino_layout(s, true);
+      d = "winograd kernels=wino_filter_kernel;wino_input_kernel;gemm_nt_kernel;wino_output_kernel "
+          "images_per_batch=" + std::to_string(L.nb);
+      break;
+    }
+    default:
+      return CONV_ERR_INVALID_ARG;
+  }
+  d += " workspace=" + std::to_string(workspace_for(s, algo)) +
+       " prepacked_workspace=" + std::to_string(workspace_for(s, algo, true)) +
+       " packed_filters=" + std::to_string(packed_filter_bytes(s, algo));
+  snprintf(buf, len, "%s", d.c_str());
+  return CONV_OK;
 }
 
 conv_status_t conv2d_im2col(const void* x, void* col, const conv2d_desc_t* desc, void* stream) {

@@ -38,6 +38,8 @@
 // are arranged so that consecutive lanes write consecutive or odd-strided
 // units.
 #include <atomic>
+#include <stdio.h>
+#include <string>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -654,27 +656,30 @@ hipError_t launch_rst(const IgPlan& pl, const IgArgs& a, hipStream_t stream) {
 }
 
 template <typename T>
-hipError_t launch_typed(const Shape& s, const void* x, const void* w, const void* b, void* y, void* ws,
-                        hipStream_t stream) {
+hipError_t pack_typed(const Shape& s, const void* w, void* wp, hipStream_t stream) {
   IgPlan pl;
-  if (!make_plan<T>(s, pl) || !ws) return hipErrorInvalidValue;
-  T* wp = reinterpret_cast<T*>(ws);
-  float* part = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + align256(pl.wp_bytes));
-  {
-    const unsigned rows = (unsigned)(s.G * pl.a.nch * pl.a.Kpad);
-    hipLaunchKernelGGL(pack_filters_kernel<T>, dim3(rows), dim3(256), 0, stream, reinterpret_cast<const T*>(w), wp,
-                       (int)s.Kg, (int)s.Cg, (int)(s.R * s.S), pl.NG, pl.a.nch, pl.a.Kpad);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
+  if (!make_plan<T>(s, pl)) return hipErrorInvalidValue;
+  const unsigned rows = (unsigned)(s.G * pl.a.nch * pl.a.Kpad);
+  hipLaunchKernelGGL(pack_filters_kernel<T>, dim3(rows), dim3(256), 0, stream, reinterpret_cast<const T*>(w),
+                     reinterpret_cast<T*>(wp), (int)s.Kg, (int)s.Cg, (int)(s.R * s.S), pl.NG, pl.a.nch, pl.a.Kpad);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t main_typed(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* part_ws,
+                      hipStream_t stream) {
+  IgPlan pl;
+  if (!make_plan<T>(s, pl)) return hipErrorInvalidValue;
+  float* part = reinterpret_cast<float*>(part_ws);
   const int64_t img_elems = s.C * s.H * s.W, out_elems = s.K * s.P * s.Q;
   for (int64_t n0 = 0; n0 < s.N; n0 += pl.images_per_launch) {
     const int64_t cnt = s.N - n0 < pl.images_per_launch ? s.N - n0 : pl.images_per_launch;
     IgPlan cur = pl;
     // The last, smaller batch of images has its own tiles, halo span and
-    // split count (never more partial sums than the full batch).
+    // split count.
     if (cnt != pl.images_per_launch && !make_plan<T>(s, cur, cnt)) return hipErrorInvalidValue;
     if (cur.NG != pl.NG || cur.BM != pl.BM) return hipErrorInvalidValue;
+    if (cur.a.splits > 1 && !part) return hipErrorInvalidValue;
     IgArgs a = cur.a;
     a.x = reinterpret_cast<const T*>(x) + n0 * img_elems;
     a.y = reinterpret_cast<T*>(y) + n0 * out_elems;
@@ -694,16 +699,8 @@ hipError_t launch_typed(const Shape& s, const void* x, const void* w, const void
   return hipSuccess;
 }
 
-}  // namespace
-
-bool implicit_gemm_fits(const Shape& s) {
-  IgPlan pl;
-  if (s.dtype == DT_F32) return make_plan<float>(s, pl);
-  return make_plan<bf16_t>(s, pl);
-}
-
 template <typename T>
-size_t workspace_typed(const Shape& s) {
+size_t split_bytes_typed(const Shape& s) {
   IgPlan pl;
   if (!make_plan<T>(s, pl)) return 0;
   size_t part = pl.part_bytes;
@@ -712,17 +709,67 @@ size_t workspace_typed(const Shape& s) {
     IgPlan last;
     if (make_plan<T>(s, last, rem) && last.part_bytes > part) part = last.part_bytes;
   }
-  return align256(pl.wp_bytes) + part;
+  return part;
+}
+
+template <typename T>
+std::string describe_typed(const Shape& s) {
+  IgPlan pl;
+  if (!make_plan<T>(s, pl)) return "implicit_gemm: does not fit";
+  char buf[512];
+  const char* tn = sizeof(T) == 2 ? "bf16" : "f32";
+  snprintf(buf, sizeof(buf),
+           "implicit_gemm kernels=pack_filters_kernel<%s>;implicit_gemm_kernel<%s,%d,%d,%d>%s tile=%dx%d "
+           "grid=%dx%dx%d chunk=%d halo_rows=%d lds=%zu images_per_launch=%lld",
+           tn, tn, pl.BM, pl.NG, pl.RST, pl.a.splits > 1 ? ";splitk_reduce_kernel" : "", pl.BM, BN,
+           (pl.a.NPQ + BN - 1) / BN, pl.a.ktiles * s.G, pl.a.splits, pl.NG * elem<T>::per16, pl.a.VR, pl.lds,
+           (long long)pl.images_per_launch);
+  return buf;
+}
+
+}  // namespace
+
+bool implicit_gemm_fits(const Shape& s) {
+  IgPlan pl;
+  if (s.dtype == DT_F32) return make_plan<float>(s, pl);
+  return make_plan<bf16_t>(s, pl);
+}
+
+size_t implicit_gemm_packed_bytes(const Shape& s) {
+  IgPlan pl;
+  const bool ok = s.dtype == DT_F32 ? make_plan<float>(s, pl) : make_plan<bf16_t>(s, pl);
+  return ok ? pl.wp_bytes : 0;
+}
+
+size_t implicit_gemm_split_bytes(const Shape& s) {
+  return s.dtype == DT_F32 ? split_bytes_typed<float>(s) : split_bytes_typed<bf16_t>(s);
 }
 
 size_t implicit_gemm_workspace(const Shape& s) {
-  return s.dtype == DT_F32 ? workspace_typed<float>(s) : workspace_typed<bf16_t>(s);
+  return align256(implicit_gemm_packed_bytes(s)) + implicit_gemm_split_bytes(s);
+}
+
+hipError_t launch_implicit_pack(const Shape& s, const void* w, void* wp, hipStream_t stream) {
+  return s.dtype == DT_F32 ? pack_typed<float>(s, w, wp, stream) : pack_typed<bf16_t>(s, w, wp, stream);
+}
+
+hipError_t launch_implicit_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* part,
+                                hipStream_t stream) {
+  return s.dtype == DT_F32 ? main_typed<float>(s, x, wp, b, y, part, stream)
+                           : main_typed<bf16_t>(s, x, wp, b, y, part, stream);
 }
 
 hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, const void* b, void* y, void* ws,
                                 hipStream_t stream) {
-  if (s.dtype == DT_F32) return launch_typed<float>(s, x, w, b, y, ws, stream);
-  return launch_typed<bf16_t>(s, x, w, b, y, ws, stream);
+  if (!ws) return hipErrorInvalidValue;
+  hipError_t e = launch_implicit_pack(s, w, ws, stream);
+  if (e != hipSuccess) return e;
+  return launch_implicit_main(s, x, ws, b, y, reinterpret_cast<char*>(ws) + align256(implicit_gemm_packed_bytes(s)),
+                              stream);
+}
+
+std::string implicit_gemm_describe(const Shape& s) {
+  return s.dtype == DT_F32 ? describe_typed<float>(s) : describe_typed<bf16_t>(s);
 }
 
 }  // namespace convsel

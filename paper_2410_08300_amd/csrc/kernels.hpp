@@ -6,6 +6,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <string>
+
 namespace convsel {
 
 enum { DT_F32 = 0, DT_BF16 = 1 };
@@ -49,10 +51,18 @@ hipError_t launch_direct(const Shape& s, const void* x, const void* w, const voi
 // implicit GEMM (MFMA), all N images.  Layers whose output tiles alone
 // would leave CUs idle split the channel reduction over several workgroups;
 // they need implicit_gemm_workspace(s) bytes of fp32 partial sums in ws.
+// The filters are first repacked (launch_implicit_pack, packed_bytes of
+// space); the main kernel then reads only the packed copy.
 bool implicit_gemm_fits(const Shape& s);
-size_t implicit_gemm_workspace(const Shape& s);
+size_t implicit_gemm_packed_bytes(const Shape& s);
+size_t implicit_gemm_split_bytes(const Shape& s);
+size_t implicit_gemm_workspace(const Shape& s);  // packed filters (256-aligned) + split partials
+hipError_t launch_implicit_pack(const Shape& s, const void* w, void* wp, hipStream_t stream);
+hipError_t launch_implicit_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* part,
+                                hipStream_t stream);
 hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, const void* b, void* y, void* ws,
                                 hipStream_t stream);
+std::string implicit_gemm_describe(const Shape& s);
 
 // Column matrix [nb][G][P*Q][Cg*R*S] of images n0 .. n0+nb-1.
 hipError_t launch_im2col(const Shape& s, const void* x, void* col, int64_t n0, int64_t nb,

@@ -20,7 +20,7 @@ import torch
 from torch import nn
 
 from . import _lib
-from .conv import conv2d, prepare
+from .conv import conv2d, prepare, pack_filters, conv2d_prepacked, resolve_algo
 
 ALGO_CHOICES = ("default", "direct", "implicit_gemm", "im2col_gemm", "gemm", "winograd", "torch")
 CONCRETE_ALGOS = ("direct", "implicit_gemm", "im2col_gemm", "winograd")
@@ -99,6 +99,11 @@ class Conv2dSwap(nn.Module):
         # the module tree (its parameters are this module's parameters), so
         # it is neither listed again as a Conv2d nor moved twice.
         object.__setattr__(self, "_torch_conv", conv)
+        # Filter packages (see conv2d_prepacked) for inference calls, keyed by
+        # algorithm, input shape and the weight's identity and version; a
+        # weight update or a new shape builds a new one.
+        self._packages = {}
+        self.cache_filters = True
 
     @property
     def algo(self):
@@ -108,7 +113,20 @@ class Conv2dSwap(nn.Module):
         algo = self.algo
         if algo == "torch":
             return self._torch_conv(x)
-        return conv2d(x, self.weight, self.bias, self.stride, self.padding, self.dilation, self.groups, algo=algo)
+        w = self.weight
+        if not self.cache_filters or (torch.is_grad_enabled() and w.requires_grad) or not x.is_cuda:
+            return conv2d(x, w, self.bias, self.stride, self.padding, self.dilation, self.groups, algo=algo)
+        algo = resolve_algo(x, w, self.bias, self.stride, self.padding, self.dilation, self.groups, algo)
+        key = (algo, tuple(x.shape), x.dtype, w.data_ptr(), w._version)
+        pk = self._packages.get(key)
+        if pk is None:
+            if len(self._packages) >= 4:
+                self._packages.clear()
+            pk = pack_filters(w.detach(), tuple(x.shape), self.stride, self.padding, self.dilation, self.groups,
+                              algo, self.bias is not None)
+            self._packages[key] = pk
+        return conv2d_prepacked(x, pk, tuple(w.shape), self.bias, self.stride, self.padding, self.dilation,
+                                self.groups, algo=algo)
 
     def extra_repr(self):
         return "%d, %d, kernel_size=%s, stride=%s, padding=%s, groups=%d, algo=%s" % (
@@ -167,7 +185,7 @@ def supported_algos(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, rel
 
 
 def time_conv(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, algo="default", relu=False,
-              warmup=2, reps=5, launches=10, graph=True):
+              warmup=2, reps=5, launches=10, graph=True, prepacked=False):
     """Median milliseconds per call of the GPU work of one convolution.
 
     The call's arguments are marshalled once; ``launches`` calls are then
@@ -180,7 +198,7 @@ def time_conv(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, algo="def
     b = None if b is None else b.contiguous()
     stream = torch.cuda.Stream(x.device)
     with torch.cuda.stream(stream):
-        call, out = prepare(x, w, b, stride, padding, dilation, groups, algo=algo, relu=relu)
+        call, out = prepare(x, w, b, stride, padding, dilation, groups, algo=algo, relu=relu, prepacked=prepacked)
         for _ in range(warmup):
             call()
         stream.synchronize()
@@ -213,12 +231,13 @@ def time_conv(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, algo="def
 
 
 def select_fastest(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, relu=False, algos=None,
-                   warmup=2, reps=5):
+                   warmup=2, reps=5, prepacked=False):
     """(fastest algorithm, {algorithm: median ms}) over the supported ones."""
     cands = supported_algos(x, w, b, stride, padding, dilation, groups, relu)
     if algos is not None:
         cands = [a for a in cands if a in algos]
-    timings = {a: time_conv(x, w, b, stride, padding, dilation, groups, a, relu, warmup, reps) for a in cands}
+    timings = {a: time_conv(x, w, b, stride, padding, dilation, groups, a, relu, warmup, reps,
+                            prepacked=prepacked) for a in cands}
     best = min(timings, key=timings.get)
     return best, timings
 

@@ -184,3 +184,55 @@ def test_unsupported_and_invalid_calls_raise():
         cs.conv2d(x, torch.randn(4, 3, 3, 3, device=DEV))
     with pytest.raises(ValueError):
         cs.conv2d(x, torch.randn(4, 4, 3, 3, device=DEV, dtype=torch.bfloat16))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_prepacked_filters_give_identical_outputs(dtype):
+    """conv2d_prepacked with a package from conv2d_pack_filters runs the same
+    kernels on the same data as conv2d, so the outputs are bit-identical."""
+    g = torch.Generator().manual_seed(10)
+    for (N, C, H, Wd, K, R, st, pd, G) in [(4, 64, 14, 14, 96, 3, 1, 1, 1), (2, 48, 9, 11, 40, 1, 2, 0, 1),
+                                           (3, 24, 12, 12, 24, 3, 1, 1, 24), (1, 512, 7, 7, 512, 3, 1, 1, 1)]:
+        x = torch.randn(N, C, H, Wd, generator=g).to(TDT[dtype]).to(DEV)
+        w = (torch.randn(K, C // G, R, R, generator=g) * 0.1).to(TDT[dtype]).to(DEV)
+        b = (torch.randn(K, generator=g) * 0.1).to(TDT[dtype]).to(DEV)
+        for algo in ALGOS:
+            if not supports(algo, R, R, st, 1, G):
+                continue
+            say("case prepacked", dtype, (N, C, H, Wd, K, R, st, pd, G), algo)
+            y0 = cs.conv2d(x, w, b, st, pd, 1, G, algo=algo)
+            pk = cs.pack_filters(w, tuple(x.shape), st, pd, 1, G, algo, bias=True)
+            y1 = cs.conv2d_prepacked(x, pk, tuple(w.shape), b, st, pd, 1, G, algo=algo)
+            torch.cuda.synchronize()
+            assert torch.equal(y0, y1)
+
+
+def test_swapped_model_matches_oracle_chain_and_caches_packages():
+    """The paper's Listing 1 network, swapped per layer, on the GPU; each
+    layer checked against the oracle (fp32), and filter packages reused."""
+    import torch.nn.functional as F
+    from torch import nn
+    torch.manual_seed(0)
+    model = nn.Sequential(nn.Conv2d(3, 16, 3, padding=1), nn.ReLU(), nn.MaxPool2d(2, 2),
+                          nn.Conv2d(16, 32, 3, padding=1), nn.ReLU())
+    x = torch.randn(2, 3, 32, 32)
+    ref = x.double().numpy()
+    for m in model:
+        if isinstance(m, nn.Conv2d):
+            ref = oracle.conv2d(ref, m.weight.detach().double().numpy(), m.bias.detach().double().numpy(), 1, 1)
+        elif isinstance(m, nn.ReLU):
+            ref = np.maximum(ref, 0)
+        else:
+            ref = F.max_pool2d(torch.from_numpy(ref), 2, 2).numpy()
+    model = model.to(DEV)
+    for sel in (["direct", "winograd"], ["implicit_gemm", "gemm"], lambda c: "default"):
+        table = cs.swap_conv2d(model, sel)
+        say("case swapped model", list(table.values()))
+        with torch.no_grad():
+            out = model(x.to(DEV))
+            out2 = model(x.to(DEV))
+        torch.cuda.synchronize()
+        assert rel_err(f64(out), ref) <= 1e-3
+        assert torch.equal(out, out2)
+    convs = [m for m in model.modules() if isinstance(m, cs.Conv2dSwap)]
+    assert all(len(m._packages) >= 1 for m in convs)
