@@ -5,15 +5,22 @@ A step is one forward pass over every convolution layer of a workload (by
 default the 53 convolutions of ResNet-50 at batch 32, bf16 data, fp32
 accumulation), each layer running the algorithm chosen for it by measured
 per-layer selection (every supported algorithm timed on that layer before
-the timed region; the fastest goes into the algorithm table).  Inputs,
-weights and outputs are resident in HBM before timing starts.
+the timed region; the fastest goes into the algorithm table) or taken from a
+saved table.  Inputs, weights and outputs are resident in HBM before timing
+starts; each call is the full conv2d() of the C ABI (filters repacked every
+call) unless --prepacked.
 
-Prints one JSON line: throughput (TFLOP/s, 2*N*K*(C/G)*R*S*P*Q per layer),
-the roofline of the dominant kernel measured with HIP events inside the
-timed region, and the CPU oracle timed on a bounded sample on the host.
+The headline replays the step as one captured HIP graph (--eager: plain
+launches); all four step variants are reported.  Per-layer call durations
+come from HIP events around graph replays of back-to-back calls of that
+layer; the roofline of the dominant kernel is computed from them.  The CPU
+oracle is timed on a bounded sample on the host.
+
+Prints one JSON line (TFLOP/s, 2*N*K*(C/G)*R*S*P*Q per layer).
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload resnet50]
-                    [--select measured|default|<algo>] [--graph] [--sweep FILE]
+                    [--select measured|default|<algo>] [--eager] [--prepacked]
+                    [--table FILE] [--save-table FILE] [--sweep FILE]
 """
 import argparse
 import json
@@ -32,8 +39,9 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def build_plan(layers, wl_index, device, select, algos_allowed=None):
-    """Resident tensors, descriptors and the chosen algorithm of every layer."""
+def build_plan(layers, wl_index, device, select, algos_allowed=None, table=None):
+    """Resident tensors, descriptors and the chosen algorithm of every layer
+    (from ``table``, a {layer name: algorithm} map, when given)."""
     import torch
     import paper_2410_08300_amd as cs
     from paper_2410_08300_amd import _lib, workloads as W
@@ -46,7 +54,9 @@ def build_plan(layers, wl_index, device, select, algos_allowed=None):
         desc = _lib.make_desc(L.n, L.c, L.h, L.w, L.k, L.r, L.s, L.stride, L.pad, L.dilation, L.groups,
                               L.dtype, b is not None, L.relu)
         key = L.shape_key()
-        if key not in cache:
+        if table is not None:
+            cache[key] = (table[L.name], {})
+        elif key not in cache:
             if select == "measured":
                 best, timings = cs.select_fastest(x, w, b, L.stride, L.pad, L.dilation, L.groups, L.relu,
                                                   algos=algos_allowed)
@@ -86,16 +96,79 @@ def make_step(plan, ws, stream_ptr, prepacked=False):
                       ctypes.c_size_t(p["pk_ws_bytes"] if prepacked else p["ws_bytes"]),
                       ctypes.c_void_p(stream_ptr)))
 
-    def step(events=None):
-        for i, args in enumerate(calls):
-            if events is not None:
-                events[i][0].record()
+    def one(i, args):
+        def call():
             st = fn(*args)
-            if events is not None:
-                events[i][1].record()
             if st:
                 raise _lib.Conv2dError(st, "layer %d" % i)
+        return call
+
+    def step():
+        for i, args in enumerate(calls):
+            st = fn(*args)
+            if st:
+                raise _lib.Conv2dError(st, "layer %d" % i)
+    step.calls = [one(i, a) for i, a in enumerate(calls)]
     return step
+
+
+# Source files of each main kernel (the HBM traffic recorded for a kernel
+# under profiles/ is used only while these files are unchanged).
+KERNEL_SOURCES = {
+    "implicit_gemm_kernel": ("implicit_gemm.hip",),
+    "gemm_nt_kernel": ("gemm.hip",),
+    "direct_": ("direct.hip",),
+    "wino_": ("winograd.hip", "gemm.hip"),
+    "im2col_kernel": ("im2col.hip",),
+}
+
+
+def source_digest(kernel):
+    import hashlib
+    files = None
+    for prefix, fs in KERNEL_SOURCES.items():
+        if kernel.startswith(prefix):
+            files = fs + ("common.hpp", "kernels.hpp")
+    if files is None:
+        return None
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2410_08300_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` on `workload` from the table in
+    profiles/traffic.md (FETCH_SIZE + WRITE_SIZE counters, calibrated against
+    a copy kernel), or None when absent or recorded for other sources."""
+    path = os.path.join(ROOT, "profiles", "traffic.md")
+    if not os.path.exists(path):
+        return None
+    digest = source_digest(kernel)
+    with open(path) as f:
+        for line in f:
+            cells = [c.strip() for c in line.strip().strip("|").split("|")]
+            if len(cells) >= 6 and cells[0] == "`%s`" % kernel and cells[1] == workload and cells[5] == digest:
+                try:
+                    return {"fetch_bytes": float(cells[2]), "write_bytes": float(cells[3]),
+                            "bytes": float(cells[2]) + float(cells[3]), "source_digest": digest}
+                except ValueError:
+                    return None
+    return None
+
+
+def calibration_copy(mib, device):
+    """One plain copy of `mib` MiB through the library (the filter package of
+    the direct algorithm is a byte copy), for scaling the HBM byte counters."""
+    import torch
+    import paper_2410_08300_amd as cs
+    kc = mib * (1 << 20) // (2 * 1024)
+    w = torch.zeros((kc, 1024, 1, 1), dtype=torch.bfloat16, device=device)
+    torch.cuda.synchronize()
+    cs.pack_filters(w, (1, 1024, 1, 1), algo="direct")
+    torch.cuda.synchronize()
+    log("calibration copy: %d bytes read, %d bytes written" % (w.numel() * 2, w.numel() * 2))
 
 
 def cpu_baseline(workload, budget_s=20.0):
@@ -111,7 +184,7 @@ def cpu_baseline(workload, budget_s=20.0):
     t_total = 0.0
     images = 0
     rng = np.random.default_rng(0)
-    while images == 0 or (t_total < budget_s and images < 64):
+    while images == 0 or (t_total < budget_s and images < 256):
         for L in layers:
             x = rng.standard_normal((L.n, L.c, L.h, L.w))
             w = rng.standard_normal((L.k, L.c // L.groups, L.r, L.s))
@@ -160,13 +233,19 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="resnet50")
     ap.add_argument("--select", default="measured")
-    ap.add_argument("--graph", action="store_true", help="replay the step as a captured HIP graph")
+    ap.add_argument("--eager", action="store_true",
+                    help="headline from eager launches (default: the step captured once as a HIP graph and replayed)")
     ap.add_argument("--prepacked", action="store_true",
                     help="time the step with filter packages built before timing (conv2d_prepacked); by default "
                          "every call rebuilds them from the filters")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--sweep", default=None, help="write per-layer, per-algorithm timings to this JSONL file")
+    ap.add_argument("--table", default=None,
+                    help="JSON {layer name: algorithm} to use instead of measuring (e.g. a saved --save-table)")
+    ap.add_argument("--save-table", default=None, help="write the per-layer algorithm table to this JSON file")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="after timing, run one plain copy of MIB MiB (reference for HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -188,69 +267,87 @@ def main():
     wl = args.workload
     layers = W.layers(wl)
     log("bench: workload %s, %d layers, select=%s" % (wl, len(layers), args.select))
-    plan, ws = build_plan(layers, W.WORKLOADS.index(wl), dev, args.select)
+    table = None
+    if args.table:
+        with open(args.table) as f:
+            table = json.load(f)["algorithms"]
+    plan, ws = build_plan(layers, W.WORKLOADS.index(wl), dev, args.select, table=table)
+    if args.save_table:
+        with open(args.save_table, "w") as f:
+            json.dump({"workload": wl, "batch": layers[0].n, "dtype": layers[0].dtype,
+                       "selection": "table" if table else args.select,
+                       "algorithms": {p["layer"].name: p["algo"] for p in plan},
+                       "timings_ms": {p["layer"].name: p["timings"] for p in plan}}, f, indent=1)
     torch.cuda.synchronize()  # filter packages were built on the default stream
     for p in plan:
         L = p["layer"]
         log("  %-24s %-14s %s" % (L.name, p["algo"],
                                   " ".join("%s=%.4f" % kv for kv in sorted(p["timings"].items()))))
         log("      %s" % p["describe"])
-    # Graph capture needs a stream other than the default one; eager runs use
-    # the same stream so both modes launch identically.
-    stream = torch.cuda.Stream(dev) if args.graph else torch.cuda.current_stream(dev)
+    # All launches go to one side stream (graph capture needs a stream other
+    # than the default one), eager or replayed.
+    stream = torch.cuda.Stream(dev)
     torch.cuda.set_stream(stream)
     step = make_step(plan, ws, stream.cuda_stream)
+    step_pk = make_step(plan, ws, stream.cuda_stream, prepacked=True)
 
-    def timed(step_fn):
-        """Warm-up, optional graph capture, then K timed steps bracketed by
-        device synchronisation; per-layer HIP events on the launch stream."""
-        for _ in range(args.warmup):
+    def timed_steps(step_fn, graph):
+        """W warm-up steps, then exactly K timed steps bracketed by device
+        synchronisation; with graph=True one step is captured as a HIP graph
+        and the K steps are K replays."""
+        g = None
+        if graph:
             step_fn()
-        torch.cuda.synchronize()
-        graph = None
-        if args.graph:
-            graph = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(graph, stream=stream):
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
                 step_fn()
             torch.cuda.synchronize()
-            for _ in range(args.warmup):
-                graph.replay()
-            torch.cuda.synchronize()
-        nl = len(plan)
-        ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(nl)]
-              for _ in range(args.steps)]
+        for _ in range(args.warmup):
+            g.replay() if g is not None else step_fn()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        if graph is not None:
-            for _ in range(args.steps):
-                graph.replay()
-        else:
-            for k in range(args.steps):
-                step_fn(ev[k])
+        for _ in range(args.steps):
+            g.replay() if g is not None else step_fn()
         torch.cuda.synchronize()
-        t1 = time.perf_counter()
-        ms = (t1 - t0) * 1e3 / args.steps
-        if graph is None:
-            lms = [sum(ev[k][i][0].elapsed_time(ev[k][i][1]) for k in range(args.steps)) / args.steps
-                   for i in range(nl)]
-        else:
-            # graph replay: per-layer times from eager steps with events
-            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(nl)]
-            lms = [0.0] * nl
-            for _ in range(args.steps):
-                step_fn(evs)
-                torch.cuda.synchronize()
-                for i in range(nl):
-                    lms[i] += evs[i][0].elapsed_time(evs[i][1]) / args.steps
-        return ms, lms
+        return (time.perf_counter() - t0) * 1e3 / args.steps
 
-    step_pk = make_step(plan, ws, stream.cuda_stream, prepacked=True)
-    ms_unpk, lms_unpk = timed(step)
-    ms_pk, lms_pk = timed(step_pk)
-    if args.prepacked:
-        ms_per_step, layer_ms, ms_other = ms_pk, lms_pk, ms_unpk
-    else:
-        ms_per_step, layer_ms, ms_other = ms_unpk, lms_unpk, ms_pk
+    def layer_times(prepacked, launches=40, reps=3):
+        """Per-layer duration of one call: `launches` back-to-back calls of
+        the layer captured as a HIP graph, replayed between two HIP events on
+        the launch stream (median of `reps`, divided by `launches`), so host
+        launch overhead and event latency stay out of the figure."""
+        calls = make_step(plan, ws, stream.cuda_stream, prepacked=prepacked).calls
+        out = []
+        for call in calls:
+            g = torch.cuda.CUDAGraph()
+            call()
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g, stream=stream):
+                for _ in range(launches):
+                    call()
+            g.replay()
+            torch.cuda.synchronize()
+            ts = []
+            for _ in range(reps):
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                g.replay()
+                e1.record(stream)
+                e1.synchronize()
+                ts.append(e0.elapsed_time(e1) / launches)
+            out.append(sorted(ts)[len(ts) // 2])
+            del g
+        return out
+
+    modes = {"graph": timed_steps(step, True), "graph_prepacked": timed_steps(step_pk, True),
+             "eager": timed_steps(step, False), "eager_prepacked": timed_steps(step_pk, False)}
+    head = ("eager" if args.eager else "graph") + ("_prepacked" if args.prepacked else "")
+    ms_per_step = modes[head]
+    lms_unpk = layer_times(False)
+    lms_pk = layer_times(True)
+    layer_ms = lms_pk if args.prepacked else lms_unpk
 
     total_flops = sum(p["layer"].flops for p in plan)
     value = total_flops / (ms_per_step * 1e-3) / 1e12
@@ -264,9 +361,9 @@ def main():
         a[2] += 1
 
     # Roofline of the dominant kernel: the main-kernel instantiation with the
-    # largest share of the step.  Measured on the prepacked step, counting the
-    # layers where that kernel is the call's only launch (no split-K reduce),
-    # so each HIP-event interval around a call times exactly one launch.
+    # largest share of the prepacked per-layer times, counting the layers
+    # where that kernel is the call's only launch (no split-K reduce), so each
+    # timed call is exactly one launch of it.
     def main_kernel(desc):
         ks = desc.split("kernels=")[1].split(" ")[0].split(";")
         return [k for k in ks if not k.startswith("pack_filters") and not k.startswith("wino_filter")]
@@ -281,10 +378,13 @@ def main():
     dom_flops = sum(p["layer"].flops for p, _ in single)
     achieved = dom_flops / (dom_ms * 1e-3) / 1e12 if dom_ms > 0 else 0.0
     peak = PEAKS_TFLOPS[dtype]
+    wl_name = "%s-n%d-%s" % (wl, layers[0].n, layers[0].dtype)
+    traffic = recorded_traffic(dom, wl_name)
     roofline = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                "traffic": None, "kernel": dom, "launches_per_step": len(single),
+                "traffic": traffic["bytes"] if traffic else None, "traffic_detail": traffic,
+                "kernel": dom, "launches_per_step": len(single),
                 "avg_launch_us": dom_ms * 1e3 / max(len(single), 1),
-                "time_share_prepacked_step": share[dom] / sum(lms_pk)}
+                "time_share_prepacked": share[dom] / sum(lms_pk)}
 
     # The 3x3 layers of the workload (the headline target for ResNet-50).
     sel = [(p, ms) for p, ms in zip(plan, layer_ms) if p["layer"].r == 3]
@@ -294,10 +394,12 @@ def main():
         t3 = sum(ms for _, ms in sel)
         extra["layers_3x3"] = {"count": len(sel), "gflop": f3 / 1e9, "ms": t3,
                                "tflops": f3 / (t3 * 1e-3) / 1e12, "frac_peak": f3 / (t3 * 1e-3) / 1e12 / peak}
-    extra["sum_layer_event_ms"] = sum(layer_ms)
+    extra["sum_layer_ms"] = sum(layer_ms)
     extra["algos"] = {a: v[2] for a, v in by_algo.items()}
-    other = "per_call_filter_packing" if args.prepacked else "prepacked_filters"
-    extra[other] = {"ms_per_step": ms_other, "tflops": total_flops / (ms_other * 1e-3) / 1e12}
+    extra["steps"] = {m: {"ms_per_step": t, "tflops": total_flops / (t * 1e-3) / 1e12} for m, t in modes.items()}
+
+    if args.calibrate_copy > 0:
+        calibration_copy(args.calibrate_copy, dev)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -309,7 +411,8 @@ def main():
            "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": dtype, "data": "synthetic (seeded normal inputs, Kaiming-normal weights)",
            "config": {"workload": "%s conv layers (%d convs), batch %d, %s data, fp32 accumulate, %s, %s"
-                                  % (wl, len(layers), nbatch, dtype, "graph replay" if args.graph else "eager launches",
+                                  % (wl, len(layers), nbatch, dtype,
+                                     "eager launches" if args.eager else "one HIP graph per step",
                                      "prepacked filters" if args.prepacked else "filters packed every call"),
                       "global_batch": nbatch, "layers": len(layers), "parallelism": "none (1 GPU)"},
            "roofline": roofline, "cpu_baseline": cpu, "detail": extra}

@@ -274,8 +274,14 @@ conv_status_t prepare_call(const conv2d_desc_t* desc, conv_algo_t* algo, Shape* 
   return ensure_device();
 }
 
-// Copies the filters into a package (algorithms that use them as they are):
-// 16-byte units, then the remaining bytes one per thread.
+}  // namespace
+
+namespace convsel {
+
+// Byte copy (filter packages of the algorithms that use the filters as they
+// are): 16-byte units when the source is 16-byte aligned, then the remaining
+// bytes one per thread.
+namespace {
 __global__ void copy16_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst, int64_t n16) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (i < n16) dst[i] = src[i];
@@ -286,7 +292,9 @@ __global__ void copy1_kernel(const unsigned char* __restrict__ src, unsigned cha
   if (i < to) dst[i] = src[i];
 }
 
-hipError_t copy_filters(const void* w, void* dst, size_t bytes, hipStream_t st) {
+}  // namespace
+
+hipError_t launch_copy(const void* w, void* dst, size_t bytes, hipStream_t st) {
   const bool aligned = reinterpret_cast<uintptr_t>(w) % 16 == 0;
   const int64_t n16 = aligned ? (int64_t)(bytes / 16) : 0;
   if (n16 > 0)
@@ -299,7 +307,7 @@ hipError_t copy_filters(const void* w, void* dst, size_t bytes, hipStream_t st) 
   return hipGetLastError();
 }
 
-}  // namespace
+}  // namespace convsel
 
 extern "C" {
 
@@ -389,7 +397,7 @@ conv_status_t conv2d_pack_filters(const void* w, void* packed, const conv2d_desc
   const hipStream_t hs = (hipStream_t)stream;
   if (algo == CONV_ALGO_IMPLICIT_GEMM) return from_hip(convsel::launch_implicit_pack(s, w, packed, hs));
   if (algo == CONV_ALGO_WINOGRAD) return from_hip(convsel::launch_wino_filter(s, w, packed, hs));
-  return from_hip(copy_filters(w, packed, wbytes, hs));
+  return from_hip(convsel::launch_copy(w, packed, wbytes, hs));
 }
 
 conv_status_t conv2d_prepacked(const void* x, const void* packed, const void* b, void* y,

@@ -185,6 +185,17 @@ __device__ __forceinline__ void mfma_32x32<float>(f32x16_t& acc, const vec16& a,
 // Row of the 32x32 block held by accumulator register v of lane `lane`.
 __device__ __forceinline__ int mfma_row(int v, int lane) { return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3); }
 
+// Workgroup barrier that orders LDS accesses only.  __syncthreads() also
+// waits for every outstanding global load and store of the wave
+// (s_waitcnt vmcnt(0)), which would drain the prefetches and LDS-DMA loads
+// the kernels keep in flight across their barriers; those are waited for
+// explicitly where their data is used.
+__device__ __forceinline__ void lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __device__ __forceinline__ f32x16_t zero16() {
   f32x16_t z;
 #pragma unroll

@@ -109,7 +109,7 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_kernel(GemmArgs g, int batch
   const int nk = (g.Kred + BK - 1) / BK;
   fetch(0);
   stash();
-  __syncthreads();
+  lds_sync();
   const int half = lane >> 5, l32 = lane & 31;
   for (int kt = 0; kt < nk; ++kt) {
     if (kt + 1 < nk) fetch(kt + 1);
@@ -126,10 +126,10 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_kernel(GemmArgs g, int batch
 #pragma unroll
         for (int nj = 0; nj < NJ; ++nj) mfma_32x32<T>(acc[mi][nj], af[mi], bfr[nj]);
     }
-    __syncthreads();
+    lds_sync();
     if (kt + 1 < nk) {
       stash();
-      __syncthreads();
+      lds_sync();
     }
   }
 

@@ -38,6 +38,7 @@
 // are arranged so that consecutive lanes write consecutive or odd-strided
 // units.
 #include <atomic>
+#include <type_traits>
 #include <stdio.h>
 #include <string>
 
@@ -54,16 +55,25 @@ constexpr uint32_t kRsrcWord3 = 0x00020000u;  // raw buffer, 32-bit data format 
 
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 
+// Output side of a tile, shared by the implicit GEMM kernels.
+struct EpiArgs {
+  const void* b;
+  void* y;             // first image of this launch
+  float* partial;      // splits > 1: fp32 partial sums, [split][N][K][P][Q]
+  int K, Kg, NPQ, PQ, relu;
+  int splits;          // workgroups sharing one output tile along the channels
+  int slab;            // floats per split of `partial` (N*K*P*Q rounded up to 4)
+  int vec;             // store piece in elements (8, 4, 2 or 1; see store_tile)
+};
+
 struct IgArgs {
   const void* x;       // first image of this launch
   const void* wp;      // packed filters
-  const void* b;
-  void* y;             // first image of this launch
   uint32_t x_bytes;    // extent of the input buffer of this launch
   uint32_t wp_bytes;
   int N, C, H, W, K, R, S, P, Q;
   int sh, sw, ph, pw, dh, dw;
-  int Cg, Kg, G, relu;
+  int Cg, Kg, G;
   int Hv, Wv, VR;      // virtual rows per image, halo width, halo rows
   int NPQ;
   int units;           // R*S*NG: 16-byte units per filter row and chunk
@@ -74,11 +84,8 @@ struct IgArgs {
   int Kpad;            // ktiles * BM
   int nch;             // channel chunks per group
   int xs_units;        // VR * Wv * PS
-  int splits;          // workgroups sharing one output tile along the channels
   int chunks_per_split;
-  float* partial;      // splits > 1: fp32 partial sums, [split][N][K][P][Q]
-  int slab;            // floats per split of `partial` (N*K*P*Q rounded up to 4)
-  int vec_out;         // P*Q % 8 == 0 and y 16-byte aligned: staged 16-byte stores
+  EpiArgs e;
 };
 
 // Virtual row of the first filter row for pixel j.
@@ -108,6 +115,16 @@ __device__ __forceinline__ vec16 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t v
   return o;
 }
 
+// Calls f(std::integral_constant<int, i>{}) for i = 0 .. N-1 (compile-time
+// indices, so register arrays indexed by i stay in registers).
+template <int N, typename F, int I = 0>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, F, I + 1>(static_cast<F&&>(f));
+  }
+}
+
 // Halo items per thread kept in registers (offsets computed once, data
 // prefetched one chunk ahead); items beyond kImax * 256 (very wide images)
 // are loaded when stashed.
@@ -117,6 +134,111 @@ template <int RST, int BM, int NG>
 struct WUnits {
   static constexpr int value = RST > 0 ? (BM * RST * NG + kThreads - 1) / kThreads : 1;
 };
+
+// Bias, ReLU and the NCHW store of one BM x BN tile (rows k0.. of group g,
+// pixels j0..), or its raw fp32 partial sums when the channels are split.
+// The accumulators go through LDS (each wave stages its 32 x 64 block; the
+// caller provides 32 KiB) so that a lane then holds a run of 8 consecutive
+// pixels of one output channel: lane l takes pixels (l % 8) * 8 .. +7 of the
+// wave's 64 and rows l / 8 + 8 * it, it = 0..3, of each 32-row block.  Its
+// image, offset and the start of the next image are computed once per tile.
+// A run is stored in pieces of e.vec elements (8, 4, 2 or 1: the largest
+// that divides P*Q and keeps the stores aligned), so no piece crosses an
+// image boundary; a piece past the boundary moves to the next image.
+template <typename T, int BM>
+__device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / 64][BN / 64], vec16* smem, const EpiArgs& e,
+                                           int j0, int k0, int g, int split) {
+  constexpr int MI = BM / 64, NJ = BN / 64;
+  constexpr int EW = BN / 2;  // pixels per wave row
+  static_assert(EW == 64, "staging layout assumes 64 pixels per wave row");
+  const int tid = threadIdx.x, lane = tid & 63, wave = (tid >> 6) & 3;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l32 = lane & 31;
+  const int PQ = e.PQ;
+  const bool split_out = e.splits > 1;
+  float* part = split_out ? e.partial + static_cast<int64_t>(split) * e.slab : nullptr;
+  const T* bias = reinterpret_cast<const T*>(e.b);
+  T* y = reinterpret_cast<T*>(e.y);
+
+  // Each wave stages 32 rows x 64 pixels of fp32 (8 KiB).  Rows are
+  // unpadded; float4 f of row r sits at f ^ g(r), g(r) = (r & 1) | 8 *
+  // ((r >> 2) & 1): the two half-waves of a store (rows r and r+4) and the
+  // quarter-waves of a load (rows 2q, 2q+1) then touch distinct banks.
+  float* stage = reinterpret_cast<float*>(smem) + wave * 32 * EW;
+  auto spos = [](int r, int px) { return r * EW + ((((px >> 2) ^ (r & 1) ^ (((r >> 2) & 1) << 3))) << 2) + (px & 3); };
+
+  const int cb = (lane & 7) * 8;
+  const int j = j0 + wn * EW + cb;
+  const int nvalid = min(8, e.NPQ - j);  // pixels of the run inside the output (<= 0: none)
+  const int n = j / PQ, pq = j - n * PQ;
+  const int wrap = PQ - pq;              // run pixels before the next image starts
+  const int64_t next_img = static_cast<int64_t>(e.K - 1) * PQ;
+  const int i0 = k0 + wm * (BM / 2) + (lane >> 3);
+  const int64_t obase = (static_cast<int64_t>(n) * e.K + g * e.Kg + i0) * PQ + pq;
+
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi) {
+#pragma unroll
+    for (int nj = 0; nj < NJ; ++nj)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) stage[spos(mfma_row(v, lane), nj * 32 + l32)] = acc[mi][nj][v];
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int row = (lane >> 3) + 8 * it;
+      const int i = i0 + mi * 32 + 8 * it;
+      const float4 lo = *reinterpret_cast<const float4*>(stage + spos(row, cb));
+      const float4 hi = *reinterpret_cast<const float4*>(stage + spos(row, cb + 4));
+      if (i >= e.Kg || nvalid <= 0) continue;
+      const int64_t o = obase + static_cast<int64_t>(mi * 32 + 8 * it) * PQ;
+      float vals[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      if (split_out) {
+        if (e.vec == 8 && nvalid == 8) {
+          *reinterpret_cast<float4*>(part + o) = lo;
+          *reinterpret_cast<float4*>(part + o + 4) = hi;
+        } else {
+          for (int t = 0; t < nvalid; ++t) part[o + t + (t >= wrap ? next_img : 0)] = vals[t];
+        }
+        continue;
+      }
+      const float bv = bias ? elem<T>::load(bias + g * e.Kg + i) : 0.f;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        vals[t] += bv;
+        if (e.relu) vals[t] = fmaxf(vals[t], 0.f);
+      }
+      if constexpr (sizeof(T) == 2) {
+        uint32_t w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) w[q] = f32x2_to_bf16x2(vals[2 * q], vals[2 * q + 1]);
+        if (e.vec == 8 && nvalid == 8) {
+          *reinterpret_cast<uint4*>(y + o) = make_uint4(w[0], w[1], w[2], w[3]);
+        } else if (e.vec == 4) {
+          for (int t = 0; t < nvalid; t += 4)
+            *reinterpret_cast<uint2*>(y + o + t + (t >= wrap ? next_img : 0)) = make_uint2(w[t / 2], w[t / 2 + 1]);
+        } else if (e.vec == 2) {
+          for (int t = 0; t < nvalid; t += 2) *reinterpret_cast<uint32_t*>(y + o + t + (t >= wrap ? next_img : 0)) = w[t / 2];
+        } else {
+          for (int t = 0; t < nvalid; ++t) elem<T>::store(y + o + t + (t >= wrap ? next_img : 0), vals[t]);
+        }
+      } else {
+        float* yf = reinterpret_cast<float*>(y);
+        if (e.vec == 8 && nvalid == 8) {
+          *reinterpret_cast<float4*>(yf + o) = make_float4(vals[0], vals[1], vals[2], vals[3]);
+          *reinterpret_cast<float4*>(yf + o + 4) = make_float4(vals[4], vals[5], vals[6], vals[7]);
+        } else if (e.vec == 4) {
+          for (int t = 0; t < nvalid; t += 4)
+            *reinterpret_cast<float4*>(yf + o + t + (t >= wrap ? next_img : 0)) =
+                make_float4(vals[t], vals[t + 1], vals[t + 2], vals[t + 3]);
+        } else {
+          for (int t = 0; t < nvalid; ++t) yf[o + t + (t >= wrap ? next_img : 0)] = vals[t];
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();  // the next block reuses this wave's stage
+  }
+}
 
 template <typename T, int BM, int NG, int RST>
 __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
@@ -161,19 +283,15 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
 
   // Per-lane pixel offsets into the halo and output base offsets.
   int pofs[NJ];
-  int64_t ybase[NJ];
-  bool jvalid[NJ];
   {
     const int PQ = a.P * a.Q;
 #pragma unroll
     for (int nj = 0; nj < NJ; ++nj) {
       const int j = j0 + wn * (BN / 2) + nj * 32 + l32;
-      jvalid[nj] = j < a.NPQ;
-      const int jj = jvalid[nj] ? j : jl;
-      const int n = jj / PQ, pq = jj - n * PQ;
+      const int jj = j < a.NPQ ? j : jl;
+      const int pq = jj - (jj / PQ) * PQ;
       const int q = pq - (pq / a.Q) * a.Q;
       pofs[nj] = ((vrow_of(jj, a) - vr_lo) * a.Wv + q * a.sw) * a.PS;
-      ybase[nj] = static_cast<int64_t>(n) * a.K * PQ + pq;
     }
   }
   // Tap offsets in the halo (compile-time tap count only).
@@ -315,7 +433,7 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
 
   fetch(ch_begin);
   stash(ch_begin);
-  __syncthreads();
+  lds_sync();
   for (int ch = ch_begin; ch < ch_end; ++ch) {
     const bool more = ch + 1 < ch_end;
     fetch(more ? ch + 1 : ch);  // the last chunk's refetch is never stashed
@@ -341,99 +459,524 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
         mfma_step(u, utab[u]);
       }
     }
-    __syncthreads();
+    lds_sync();
     if (more) {
       stash(ch + 1);
-      __syncthreads();
+      lds_sync();
     }
   }
 
-  // ---- epilogue: bias, ReLU, NCHW store ----
-  // With P*Q a multiple of 8, every aligned run of 8 tile pixels lies in one
-  // image and starts 16-byte aligned in y, so the accumulators go through
-  // LDS (the chunk buffers are free now) and leave as 16-byte stores of 8
-  // consecutive pixels of one channel.  Otherwise each lane stores its own
-  // values (lanes hold consecutive pixels, so stores still coalesce).
-  // Split workgroups write raw fp32 partial sums instead (summed, biased and
-  // rounded by the reduce kernel).
-  const int64_t PQ = static_cast<int64_t>(a.P) * a.Q;
-  const bool split_out = a.splits > 1;
-  float* part = split_out ? a.partial + static_cast<int64_t>(split) * a.slab : nullptr;
-  const T* bias = reinterpret_cast<const T*>(a.b);
-  T* y = reinterpret_cast<T*>(a.y);
-  if (a.vec_out) {
-    constexpr int EW = BN / 2;        // pixels per wave row
-    constexpr int ES_ROW = EW + 4;    // staged row stride (floats)
-    float* stage = reinterpret_cast<float*>(smem) + wave * 32 * ES_ROW;
+  store_tile<T, BM>(acc, smem, a.e, j0, k0, g, blockIdx.z);
+}
+
+// ---------------------------------------------------------------------------
+// 1x1 layers (R = S = 1, one group).  The product is then a plain GEMM per
+// image, Y[k][pixel] = sum_c W[k][c] * X[c][pixel]: the filters need no
+// repacking (a K x C row is already reduction-contiguous) and there is no
+// halo.  The input, however, is pixel-contiguous (NCHW), while an MFMA lane
+// needs 8 bf16 (4 fp32) consecutive channels of one pixel; so each thread
+// loads UE channels x 4 consecutive pixels with wide loads (8 bytes bf16,
+// 16 bytes fp32 per channel), transposes them in registers into 4 pixel
+// units of UE channels, and stores those to LDS.
+//
+// A chunk is 8 units (64 bf16 / 32 fp32 channels) of every pixel and filter
+// row.  LDS rows of 8 units are XOR-swizzled, unit u of row r at
+// r*8 + (u ^ ((r >> 1) & 7)): the MFMA reads of 16 consecutive rows and the
+// stores of 16 consecutive lanes then hit distinct 16-byte bank groups.
+//
+// Strided or padded 1x1 layers, and plane sizes that are not a multiple of
+// 4, use the same kernel with one element load per pixel (GATHER).
+// ---------------------------------------------------------------------------
+struct PwArgs {
+  const void* x;        // first image of this launch
+  const void* w;        // K x C filters (a 1x1 layer's KCRS layout)
+  uint32_t x_bytes, w_bytes;
+  int C, H, W, HW, P, Q, sh, sw, ph, pw;
+  int NPQ, ktiles, ptiles, nch, chunks_per_split;
+  EpiArgs e;
+};
+
+constexpr int kPwUnits = 8;  // 16-byte channel units per row and chunk
+
+__device__ __forceinline__ int pw_swz(int row, int u) { return row * kPwUnits + (u ^ ((row >> 1) & 7)); }
+
+__device__ __forceinline__ u32x4_t buf_load_px4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, float*) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+}
+__device__ __forceinline__ u32x4_t buf_load_px4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, bf16_t*) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
+  u32x4_t o;
+  o[0] = v[0];
+  o[1] = v[1];
+  o[2] = 0u;
+  o[3] = 0u;
+  return o;
+}
+
+// Work is handed out in units (pixel tile, filter tile, channel split), with
+// the k-tiles and splits of one pixel tile adjacent.  The grid is persistent:
+// workgroup w serves XCD w % 8 (workgroups are dealt to the 8 XCDs
+// round-robin by id), each XCD takes one contiguous range of units -- so the
+// units that read the same input or the same filters share an L2 -- and the
+// workgroups of an XCD take its units in turn.  A workgroup runs through the
+// (unit, chunk) items of its units with the loads of the next NS items in
+// flight (NS register stages), across unit boundaries: a tile's epilogue
+// overlaps the loads of the next tile.
+template <typename T, int BM, bool GATHER, int NS>
+__global__ __launch_bounds__(kThreads) void pointwise_gemm_kernel(PwArgs a) {
+  constexpr int UE = elem<T>::per16;
+  constexpr int ES = elem<T>::bytes;
+  constexpr int MI = BM / 64, NJ = BN / 64;
+  constexpr int CC = kPwUnits * UE;               // channels per chunk
+  constexpr int AU = BM * kPwUnits / kThreads;    // filter units per thread
+  constexpr int BW = sizeof(T) == 2 ? 2 : 4;      // words per pixel-quad load
+  extern __shared__ __align__(16) vec16 smem[];
+  vec16* As = smem;                               // [BM][8], swizzled
+  vec16* Bs = smem + BM * kPwUnits;               // [BN][8], swizzled
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int half = lane >> 5, l32 = lane & 31;
+  const int cg = tid & 7, pg = tid >> 3;  // input: channel unit cg of pixels 4*pg .. +3
+
+  // This workgroup's units: u_first, u_first + stride, ... below u_end.
+  const int units = a.ptiles * a.ktiles * a.e.splits;
+  const int per_xcd = (units + 7) >> 3;
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3, slots = gridDim.x >> 3;
+  const int u_end = min(units, (xcd + 1) * per_xcd);
+  const int u_first = xcd * per_xcd + slot;
+
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
+  const uint32_t plane = static_cast<uint32_t>(a.H * a.W * ES);  // bytes per input channel plane
+
+  // Register stages.
+  u32x4_t braw[NS][GATHER ? 1 : UE];     // contiguous: 4 pixels of channel e (BW words used)
+  uint32_t graw[NS][GATHER ? UE : 1][4]; // gather: channel e of pixel i
+  vec16 areg[NS][AU];
+
+  // Chunk range of unit u.
+  auto chunk_begin = [&](int u) { return (u % a.e.splits) * a.chunks_per_split; };
+  auto chunk_end = [&](int u) { return min(a.nch, (u % a.e.splits + 1) * a.chunks_per_split); };
+
+  // Loads of item (u, ch) into stage S.  u and ch are workgroup-uniform;
+  // readfirstlane keeps everything derived from them in scalar registers.
+  auto fetch = [&](auto stage, int u_in, int ch_in) {
+    constexpr int S = decltype(stage)::value;
+    const int u = __builtin_amdgcn_readfirstlane(u_in);
+    const int ch = __builtin_amdgcn_readfirstlane(ch_in);
+    const int tile = u / a.e.splits;
+    const int pt = tile / a.ktiles, kt = tile - pt * a.ktiles;
+    const int j0 = pt * BN, k0 = kt * BM;
+    const int c0 = ch * CC;
+    const bool tail = c0 + CC > a.C;  // uniform
+    const bool cvalid = !tail || c0 + cg * UE < a.C;
+    // The channel offset (c0 + e) * plane is the scalar offset; a lane's
+    // vector offset is its pixel's, or x_bytes (reads zero) past the data.
+    if constexpr (!GATHER) {
+      // Plane size a multiple of 4: the 4 pixels are consecutive in one image.
+      const int j = j0 + 4 * pg;
+      const int n = j / a.HW, pix = j - n * a.HW;
+      const uint32_t vo = (cvalid && j < a.NPQ) ? static_cast<uint32_t>(((n * a.C + cg * UE) * a.HW + pix) * ES)
+                                                : a.x_bytes;
 #pragma unroll
-    for (int mi = 0; mi < MI; ++mi) {
+      for (int e = 0; e < UE; ++e)
+        braw[S][e] = buf_load_px4(xr, vo, static_cast<uint32_t>(c0 + e) * plane, (T*)nullptr);
+    } else {
+      const int PQ = a.P * a.Q;
+      uint32_t vo[4];
 #pragma unroll
-      for (int nj = 0; nj < NJ; ++nj)
+      for (int i = 0; i < 4; ++i) {
+        const int j = j0 + 4 * pg + i;
+        const int n = j / PQ, pq = j - n * PQ;
+        const int p = pq / a.Q, q = pq - p * a.Q;
+        const int ih = p * a.sh - a.ph, iw = q * a.sw - a.pw;
+        const bool ok = cvalid && j < a.NPQ && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
+        vo[i] = ok ? static_cast<uint32_t>(((n * a.C + cg * UE) * a.H * a.W + ih * a.W + iw) * ES) : a.x_bytes;
+      }
 #pragma unroll
-        for (int v = 0; v < 16; ++v) stage[mfma_row(v, lane) * ES_ROW + nj * 32 + l32] = acc[mi][nj][v];
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
-      __builtin_amdgcn_wave_barrier();
-      // 32 rows x EW pixels = 4*EW/8 runs of 8; lane takes runs lane, lane+64, ...
+      for (int e = 0; e < UE; ++e)
 #pragma unroll
-      for (int it = 0; it < 32 * EW / 8 / 64; ++it) {
-        const int run = lane + 64 * it;
-        const int row = run / (EW / 8), cb = (run % (EW / 8)) * 8;
-        const int i = k0 + wm * (BM / 2) + mi * 32 + row;
-        const int j = j0 + wn * (BN / 2) + cb;
-        if (i >= a.Kg || j >= a.NPQ) continue;
-        const int k = g * a.Kg + i;
-        const int n = j / static_cast<int>(PQ), pq = j - n * static_cast<int>(PQ);
-        const int64_t o = (static_cast<int64_t>(n) * a.K + k) * PQ + pq;
-        const float4 lo = *reinterpret_cast<const float4*>(stage + row * ES_ROW + cb);
-        const float4 hi = *reinterpret_cast<const float4*>(stage + row * ES_ROW + cb + 4);
-        float vals[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-        if (split_out) {
-          *reinterpret_cast<float4*>(part + o) = lo;
-          *reinterpret_cast<float4*>(part + o + 4) = hi;
-          continue;
-        }
-        const float bv = bias ? elem<T>::load(bias + k) : 0.f;
+        for (int i = 0; i < 4; ++i)
+          graw[S][e][i] = buf_load_elem(xr, vo[i], static_cast<uint32_t>(c0 + e) * plane, (T*)nullptr);
+    }
+    // Filters: unit f = tid + t*256 is row f / 8, unit f % 8 of the tile;
+    // rows past K fall past the buffer.
+    const uint32_t wso = static_cast<uint32_t>(c0 * ES);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          vals[e] += bv;
-          if (a.relu) vals[e] = fmaxf(vals[e], 0.f);
-        }
-        if constexpr (sizeof(T) == 2) {
-          uint4 u;
-          u.x = f32x2_to_bf16x2(vals[0], vals[1]);
-          u.y = f32x2_to_bf16x2(vals[2], vals[3]);
-          u.z = f32x2_to_bf16x2(vals[4], vals[5]);
-          u.w = f32x2_to_bf16x2(vals[6], vals[7]);
-          *reinterpret_cast<uint4*>(y + o) = u;
+    for (int t = 0; t < AU; ++t) {
+      const int f = tid + t * kThreads;
+      const int row = f >> 3, cu = f & 7;
+      const uint32_t vo = (!tail || c0 + cu * UE < a.C) ? static_cast<uint32_t>(((k0 + row) * a.C + cu * UE) * ES)
+                                                        : a.w_bytes;
+      areg[S][t] = buf_load16(wr, vo, wso);
+    }
+  };
+
+  // Stage S into LDS.
+  auto stash = [&](auto stage) {
+    constexpr int S = decltype(stage)::value;
+    // Pixel units: unit i holds channels cg*UE .. +UE-1 of pixel 4*pg + i.
+    vec16 u[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        if constexpr (GATHER) {
+          if constexpr (sizeof(T) == 2)
+            u[i].d[d] = (graw[S][2 * d][i] & 0xffffu) | (graw[S][2 * d + 1][i] << 16);
+          else
+            u[i].d[d] = graw[S][d][i];
         } else {
-          *reinterpret_cast<float4*>(reinterpret_cast<float*>(y) + o) = make_float4(vals[0], vals[1], vals[2], vals[3]);
-          *reinterpret_cast<float4*>(reinterpret_cast<float*>(y) + o + 4) =
-              make_float4(vals[4], vals[5], vals[6], vals[7]);
+          if constexpr (sizeof(T) == 2) {
+            // channel 2d / 2d+1 of pixel i: half i&1 of word i>>1
+            const uint32_t lo = braw[S][2 * d][i >> 1], hi = braw[S][2 * d + 1][i >> 1];
+            u[i].d[d] = (i & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+          } else {
+            u[i].d[d] = braw[S][d][i];
+          }
         }
       }
-      __builtin_amdgcn_wave_barrier();  // the next block reuses this wave's stage
+    }
+    // Odd pixel groups store their units in the order 1,0,3,2 so that the
+    // 16 lanes of two neighbouring groups write both pixel parities at once.
+    const uint32_t odd = static_cast<uint32_t>(pg & 1);
+    const uint32_t m = 0u - odd;  // all ones for odd groups (bit select, no register indexing)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      vec16 v;
+#pragma unroll
+      for (int d = 0; d < 4; ++d) v.d[d] = (u[i ^ 1].d[d] & m) | (u[i].d[d] & ~m);
+      Bs[pw_swz(4 * pg + (i ^ static_cast<int>(odd)), cg)] = v;
+    }
+#pragma unroll
+    for (int t = 0; t < AU; ++t) {
+      const int f = tid + t * kThreads;
+      As[pw_swz(f >> 3, f & 7)] = areg[S][t];
+    }
+  };
+
+  f32x16_t acc[MI][NJ];
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+    for (int nj = 0; nj < NJ; ++nj) acc[mi][nj] = zero16();
+
+  const int arow0 = wm * (BM / 2) + l32;
+  const int brow0 = wn * (BN / 2) + l32;
+  auto mfma_chunk = [&]() {
+#pragma unroll
+    for (int st = 0; st < kPwUnits / 2; ++st) {
+      const int u = 2 * st + half;
+      vec16 af[MI], bfr[NJ];
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi) af[mi] = As[pw_swz(arow0 + mi * 32, u)];
+#pragma unroll
+      for (int nj = 0; nj < NJ; ++nj) bfr[nj] = Bs[pw_swz(brow0 + nj * 32, u)];
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int nj = 0; nj < NJ; ++nj) mfma_32x32<T>(acc[mi][nj], af[mi], bfr[nj]);
+    }
+  };
+
+  // Items in order: (u, ch) for ch in the chunk range of u, then the next
+  // unit u + slots.  The fetch cursor (fu, fch) runs NS items ahead of the
+  // compute cursor (cu, cch).
+  int fu = u_first, fch = 0;
+  if (fu < u_end) fch = chunk_begin(fu);
+  static_for<NS>([&](auto s) {
+    if (fu < u_end) {
+      fetch(s, fu, fch);
+      if (++fch >= chunk_end(fu)) {
+        fu += slots;
+        fch = fu < u_end ? chunk_begin(fu) : 0;
+      }
+    }
+  });
+  int cu = u_first;
+  if (cu >= u_end) return;  // uniform: no work for this workgroup
+  int cch = chunk_begin(cu);
+  stash(std::integral_constant<int, 0>{});
+  lds_sync();
+  bool done = false;
+  while (!done) {
+    static_for<NS>([&](auto s) {
+      if (done) return;
+      constexpr int S = decltype(s)::value;
+      // LDS holds item (cu, cch), which came from stage S; refill S.
+      if (fu < u_end) {
+        fetch(s, fu, fch);
+        if (++fch >= chunk_end(fu)) {
+          fu += slots;
+          fch = fu < u_end ? chunk_begin(fu) : 0;
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_chunk();
+      lds_sync();
+      if (++cch >= chunk_end(cu)) {
+        const int tile = cu / a.e.splits;
+        const int pt = tile / a.ktiles, kt = tile - pt * a.ktiles;
+        store_tile<T, BM>(acc, smem, a.e, pt * BN, kt * BM, 0, cu % a.e.splits);
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+          for (int nj = 0; nj < NJ; ++nj) acc[mi][nj] = zero16();
+        lds_sync();
+        cu += slots;
+        if (cu >= u_end) {
+          done = true;
+          return;
+        }
+        cch = chunk_begin(cu);
+      }
+      stash(std::integral_constant<int, (S + 1) % NS>{});
+      lds_sync();
+    });
+  }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 1x1 layers, stride 1, no padding, plane size a multiple of 2 pixels:
+// the chunk of input (64 channels x 128 pixels) is copied by the buffer-to-LDS
+// DMA exactly as it lies in memory, pixel-contiguous, and the MFMA B
+// fragments are read with the gfx950 transposing LDS read ds_read_b64_tr_b16.
+// No operand passes through registers on its way in, so a workgroup keeps NS
+// chunks in LDS and the loads of NS-1 of them in flight while it multiplies
+// the oldest one (and, between tiles, while it stores the finished tile).
+//
+// ds_read_b64_tr_b16 works on 16-lane groups: lane r of a group addresses
+// 4 consecutive 16-bit elements (8 bytes); lane j receives element j % 4 of
+// the rows addressed by lanes j/4, j/4 + 4, j/4 + 8, j/4 + 12.  With lane r
+// addressing channel row c0 + r/4, pixels n0 + 4*(r%4) .. +3, lane j gets
+// channels c0 .. c0+3 of pixel n0 + j: four consecutive reduction elements of
+// one B column, half of an MFMA 32x32x16 B operand.
+//
+// LDS stage (32 KiB): A = 128 filter rows x 64 channels, 16-byte unit u of
+// row r at r*8 + (u ^ ((r >> 1) & 7)); B = 64 channel rows x 128 pixels,
+// 16-byte unit u of row c at c*16 + (u ^ 4*(c & 3)).  The DMA writes 64
+// consecutive units per instruction; the swizzles are realised by choosing
+// which global unit each lane fetches.  A reads of 16 consecutive rows, the
+// transposing reads of 4 rows x 64 bytes per half-wave and the epilogue
+// staging are free of bank conflicts.
+// ---------------------------------------------------------------------------
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+typedef short v8s_t __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+constexpr int kDmaStageBytes = 32 * 1024;
+constexpr int kDmaStages = 4;  // LDS stages of the 1x1 DMA kernel (plus 32 KiB of epilogue staging)
+
+// s_waitcnt with vmcnt = n and the other counters at their maximum (gfx9 encoding).
+#define CONVSEL_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (15 << 8))
+
+template <int UB, int NS>
+__global__ __launch_bounds__(2 * kThreads) void pointwise_dma_kernel(PwArgs a) {
+  constexpr int BM = 128, MI = 2, NJ = 2;
+  constexpr int CC = 64;                                // channels per chunk
+  constexpr int A_INS = 4;                              // A DMA instructions per loader wave per chunk
+  constexpr int B_INS = (CC * BN * 2) / (64 * UB) / 4;  // B DMA instructions per loader wave per chunk
+  constexpr int INS = A_INS + B_INS;
+  static_assert(UB == 16 || UB == 4, "DMA unit");
+  static_assert((NS - 1) * INS <= 63, "vmcnt range");
+  extern __shared__ __align__(16) vec16 smem[];
+  char* lds = reinterpret_cast<char*>(smem);
+  vec16* staging = reinterpret_cast<vec16*>(lds + NS * kDmaStageBytes);  // 8 KiB per compute wave
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const bool loader = wave >= 4;                        // waves 4..7 issue the DMA, 0..3 multiply
+  const int lw = wave & 3;
+  const int wm = lw >> 1, wn = lw & 1;
+  const int half = lane >> 5, l32 = lane & 31;
+
+  const int units = a.ptiles * a.ktiles * a.e.splits;
+  const int per_xcd = (units + 7) >> 3;
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3, slots = gridDim.x >> 3;
+  const int u_end = min(units, (xcd + 1) * per_xcd);
+  const int u_first = xcd * per_xcd + slot;
+  if (u_first >= u_end) return;  // uniform: no work for this workgroup
+
+  auto chunk_begin = [&](int u) { return (u % a.e.splits) * a.chunks_per_split; };
+  auto chunk_end = [&](int u) { return min(a.nch, (u % a.e.splits + 1) * a.chunks_per_split); };
+
+  if (loader) {
+    // ---- loader waves: DMA of item (u, ch) into stage st ----
+    const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
+    const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
+    const uint32_t plane = static_cast<uint32_t>(a.HW * 2);
+    // A instruction i fills units (lw*4 + i)*64 + lane: row (lw*4+i)*8 +
+    // lane/8, stored unit lane%8, global unit (lane%8) ^ ((row >> 1) & 7).
+    int a_row[A_INS], a_unit[A_INS];
+#pragma unroll
+    for (int i = 0; i < A_INS; ++i) {
+      const int row = (lw * A_INS + i) * 8 + (lane >> 3);
+      a_row[i] = row;
+      a_unit[i] = (lane & 7) ^ ((row >> 1) & 7);
+    }
+    // B instruction i: UB = 16 fills 4 channel rows (lw*4+i)*4 + lane/16,
+    // stored unit lane%16; UB = 4 fills channel row lw*16 + i, 4-byte slot
+    // lane (stored unit lane/4, pixel pair lane%4 within it).
+    auto b_chan = [&](int i) { return UB == 16 ? (lw * B_INS + i) * 4 + (lane >> 4) : lw * B_INS + i; };
+    auto b_pix = [&](int i) {  // first pixel (within the tile) of the lane's unit
+      const int c = b_chan(i);
+      if constexpr (UB == 16) return ((lane & 15) ^ (4 * (c & 3))) * 8;
+      else return (((lane >> 2) ^ (4 * (c & 3))) * 8) + 2 * (lane & 3);
+    };
+    // Pixel offsets per unit: UB = 16 has one pixel unit per lane for all
+    // instructions; UB = 4 one per value of c & 3 = i & 3.
+    constexpr int NPX = UB == 16 ? 1 : 4;
+    uint32_t pixoff[NPX];
+    int pix_unit = -1;
+    auto issue = [&](int u_in, int ch_in, int st) {
+      const int u = __builtin_amdgcn_readfirstlane(u_in);
+      const int ch = __builtin_amdgcn_readfirstlane(ch_in);
+      const int tile = u / a.e.splits;
+      const int pt = tile / a.ktiles, kt = tile - pt * a.ktiles;
+      const int j0 = pt * BN, k0 = kt * BM, c0 = ch * CC;
+      if (u != pix_unit) {
+        pix_unit = u;
+#pragma unroll
+        for (int q = 0; q < NPX; ++q) {
+          const int j = j0 + b_pix(q);
+          const int n = j / a.HW, pix = j - n * a.HW;
+          pixoff[q] = j < a.NPQ ? static_cast<uint32_t>((n * a.C * a.HW + pix) * 2) : a.x_bytes;
+        }
+      }
+      char __attribute__((address_space(3)))* base =
+          (char __attribute__((address_space(3)))*)(lds + st * kDmaStageBytes);
+      const uint32_t wso = static_cast<uint32_t>(c0 * 2);
+#pragma unroll
+      for (int i = 0; i < A_INS; ++i) {
+        const bool ok = c0 + a_unit[i] * 8 < a.C;  // rows past K fall past the buffer
+        const uint32_t vo = ok ? static_cast<uint32_t>(((k0 + a_row[i]) * a.C + a_unit[i] * 8) * 2) : a.w_bytes;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void_t*)(base + (lw * A_INS + i) * 1024), 16, vo, wso, 0,
+                                                 0);
+      }
+      const uint32_t xso = static_cast<uint32_t>(c0) * plane;
+#pragma unroll
+      for (int i = 0; i < B_INS; ++i) {
+        const int c = b_chan(i);
+        const uint32_t po = pixoff[UB == 16 ? 0 : (i & 3)];
+        const uint32_t vo = (c0 + c < a.C && po != a.x_bytes) ? po + static_cast<uint32_t>(c) * plane : a.x_bytes;
+        lds_void_t* dst = (lds_void_t*)(base + 16384 + (lw * B_INS + i) * 64 * UB);
+        if constexpr (UB == 16)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, dst, 16, vo, xso, 0, 0);
+        else
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, dst, 4, vo, xso, 0, 0);
+      }
+    };
+    // Fetch cursor (fu, fch).  All NS stages are filled up front; after that
+    // the stage freed at barrier B of item k-1 is refilled right after
+    // barrier A of item k, while the compute waves multiply item k, so the
+    // issue never delays the barrier.  `later` counts the items issued after
+    // the one being waited for (this wave issues nothing else, so that is
+    // the vmcnt to wait for).
+    int fu = u_first, fch = chunk_begin(u_first), fstage = 0;
+    auto fetch_next = [&]() -> bool {
+      if (fu >= u_end) return false;
+      issue(fu, fch, fstage);
+      fstage = fstage + 1 == NS ? 0 : fstage + 1;
+      if (++fch >= chunk_end(fu)) {
+        fu += slots;
+        if (fu < u_end) fch = chunk_begin(fu);
+      }
+      return true;
+    };
+    int later = -1;
+    for (int s = 0; s < NS; ++s)
+      if (fetch_next()) ++later;
+    int cu = u_first, cch = chunk_begin(u_first);
+    bool first = true;
+    for (;;) {
+      static_for<NS>([&](auto m) {
+        if (later == decltype(m)::value) CONVSEL_WAIT_VMCNT(decltype(m)::value * INS);
+      });
+      // Plain barriers: the wait above already covers the item's DMA, and an
+      // LDS fence here would also wait for the later items still in flight.
+      __builtin_amdgcn_s_barrier();  // A: item visible to the compute waves
+      if (!first && fetch_next()) ++later;  // refill the stage freed at the previous B
+      first = false;
+      __builtin_amdgcn_s_barrier();  // B: compute waves are done with this item's stage
+      --later;                       // the next item to wait for is one further on
+      if (++cch >= chunk_end(cu)) {
+        cu += slots;
+        if (cu >= u_end) break;
+        cch = chunk_begin(cu);
+      }
     }
     return;
   }
+
+  // ---- compute waves ----
+  // B fragment addresses (transposing reads): group g = lane/16 covers
+  // pixels n0 = 16*(g&1) of the 32-column block and channels kk0 = 8*(g>>1)
+  // of the 16-channel step; lane r = lane%16 reads channel row kk0 + r/4 (+4
+  // for the second read), pixels n0 + 4*(r%4).
+  int b_off[NJ];
+  {
+    const int g = lane >> 4, r = lane & 15;
+    const int c_rel = 8 * (g >> 1) + (r >> 2);
+#pragma unroll
+    for (int nj = 0; nj < NJ; ++nj) {
+      const int px = wn * 64 + nj * 32 + 16 * (g & 1) + 4 * (r & 3);
+      b_off[nj] = c_rel * 256 + ((((px >> 3) ^ (4 * (c_rel & 3)))) << 4) + ((px >> 2) & 1) * 8;
+    }
+  }
+  int a_off[MI], a_swz[MI];
 #pragma unroll
   for (int mi = 0; mi < MI; ++mi) {
+    const int row = wm * 64 + mi * 32 + l32;
+    a_off[mi] = row * 8;
+    a_swz[mi] = (row >> 1) & 7;
+  }
+
+  f32x16_t acc[MI][NJ];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int i = k0 + wm * (BM / 2) + mi * 32 + mfma_row(v, lane);
-      if (i >= a.Kg) continue;
-      const int k = g * a.Kg + i;
-      const float bv = (bias && !split_out) ? elem<T>::load(bias + k) : 0.f;
+  for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+    for (int nj = 0; nj < NJ; ++nj) acc[mi][nj] = zero16();
+
+  int cu = u_first, cch = chunk_begin(u_first), cstage = 0;
+  for (;;) {
+    lds_sync();  // A
+    const char* As = lds + cstage * kDmaStageBytes;
+    const char* Bs = As + 16384;
+#pragma unroll
+    for (int kst = 0; kst < CC / 16; ++kst) {
+      const int u = 2 * kst + half;
+      bf16x8_t af[MI], bfr[NJ];
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+        af[mi] = *reinterpret_cast<const bf16x8_t*>(As + (a_off[mi] + (u ^ a_swz[mi])) * 16);
 #pragma unroll
       for (int nj = 0; nj < NJ; ++nj) {
-        if (!jvalid[nj]) continue;
-        if (split_out) {
-          part[ybase[nj] + k * PQ] = acc[mi][nj][v];
-          continue;
-        }
-        float val = acc[mi][nj][v] + bv;
-        if (a.relu) val = fmaxf(val, 0.f);
-        elem<T>::store(y + ybase[nj] + k * PQ, val);
+        const char* p = Bs + kst * 16 * 256 + b_off[nj];
+        const v4s_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)(p));
+        const v4s_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)(p + 4 * 256));
+        bfr[nj] = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       }
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int nj = 0; nj < NJ; ++nj)
+          acc[mi][nj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mi], bfr[nj], acc[mi][nj], 0, 0, 0);
+    }
+    lds_sync();  // B: the stage may be refilled
+    cstage = cstage + 1 == NS ? 0 : cstage + 1;
+    if (++cch >= chunk_end(cu)) {
+      // Tile done: each compute wave stages its part in its own region.
+      const int tile = cu / a.e.splits;
+      const int pt = tile / a.ktiles, kt = tile - pt * a.ktiles;
+      store_tile<bf16_t, BM>(acc, staging, a.e, pt * BN, kt * BM, 0, cu % a.e.splits);
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int nj = 0; nj < NJ; ++nj) acc[mi][nj] = zero16();
+      cu += slots;
+      if (cu >= u_end) break;
+      cch = chunk_begin(cu);
     }
   }
 }
@@ -548,13 +1091,11 @@ struct IgPlan {
 // split) that minimises the number of full waves of 256 CUs per unit of work,
 // ceil(tiles*S / 256) / S, plus a small charge per extra split for the
 // partial-sum traffic.
-void choose_splits(const Shape& s, IgPlan& pl) {
-  IgArgs& a = pl.a;
-  const int64_t tiles = (int64_t)((a.NPQ + BN - 1) / BN) * a.ktiles * s.G;
+void split_chunks(int64_t tiles, int nch, int* splits, int* chunks_per_split) {
   int best = 1;
   double best_cost = 1e30;
   if (tiles < kCUs) {
-    for (int S = 1; S <= 8 && S <= (a.nch + 1) / 2; ++S) {
+    for (int S = 1; S <= 8 && S <= (nch + 1) / 2; ++S) {
       const double waves = (double)((tiles * S + kCUs - 1) / kCUs) / S;
       const double cost = waves + 0.05 * (S - 1);
       if (cost < best_cost - 1e-9) {
@@ -563,8 +1104,14 @@ void choose_splits(const Shape& s, IgPlan& pl) {
       }
     }
   }
-  a.chunks_per_split = (a.nch + best - 1) / best;
-  a.splits = (a.nch + a.chunks_per_split - 1) / a.chunks_per_split;
+  *chunks_per_split = (nch + best - 1) / best;
+  *splits = (nch + *chunks_per_split - 1) / *chunks_per_split;
+}
+
+void choose_splits(const Shape& s, IgPlan& pl) {
+  IgArgs& a = pl.a;
+  const int64_t tiles = (int64_t)((a.NPQ + BN - 1) / BN) * a.ktiles * s.G;
+  split_chunks(tiles, a.nch, &a.e.splits, &a.chunks_per_split);
 }
 
 // Plan for `N1` images per launch (all of them unless the input exceeds the
@@ -584,7 +1131,8 @@ bool make_plan(const Shape& s, IgPlan& pl, int64_t N1 = -1) {
   a.N = (int)N1; a.C = (int)s.C; a.H = (int)s.H; a.W = (int)s.W; a.K = (int)s.K;
   a.R = (int)s.R; a.S = (int)s.S; a.P = (int)s.P; a.Q = (int)s.Q;
   a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw; a.dh = s.dh; a.dw = s.dw;
-  a.Cg = (int)s.Cg; a.Kg = (int)s.Kg; a.G = s.G; a.relu = s.relu ? 1 : 0;
+  a.Cg = (int)s.Cg; a.Kg = (int)s.Kg; a.G = s.G;
+  a.e.K = (int)s.K; a.e.Kg = (int)s.Kg; a.e.relu = s.relu ? 1 : 0; a.e.PQ = (int)(s.P * s.Q);
   a.Hv = (int)((s.P - 1) * s.sh + (s.R - 1) * s.dh + 1);
   a.Wv = (int)((s.Q - 1) * s.sw + (s.S - 1) * s.dw + 1);
   a.VR = halo_rows(s, N1, a.Hv);
@@ -604,7 +1152,7 @@ bool make_plan(const Shape& s, IgPlan& pl, int64_t N1 = -1) {
       a.PS = ng | 1;
       a.xs_units = a.VR * a.Wv * a.PS;
       size_t lds = ((size_t)pl.BM * a.UR + (size_t)a.xs_units) * 16 + (size_t)2 * a.steps * 4;
-      const size_t stage = (size_t)4 * 32 * (BN / 2 + 4) * sizeof(float);  // epilogue staging
+      const size_t stage = (size_t)4 * 32 * (BN / 2) * sizeof(float);  // epilogue staging
       if (lds < stage) lds = stage;
       if (lds > limit) continue;
       pl.NG = ng;
@@ -613,8 +1161,8 @@ bool make_plan(const Shape& s, IgPlan& pl, int64_t N1 = -1) {
       pl.wp_bytes = (size_t)s.G * a.nch * a.Kpad * a.units * 16;
       if (pl.wp_bytes > (size_t)kMaxLaunchBytes) return false;
       choose_splits(s, pl);
-      a.slab = (int)((N1 * s.K * s.P * s.Q + 3) & ~(int64_t)3);
-      pl.part_bytes = a.splits > 1 ? (size_t)a.splits * a.slab * sizeof(float) : 0;
+      a.e.slab = (int)((N1 * s.K * s.P * s.Q + 3) & ~(int64_t)3);
+      pl.part_bytes = a.e.splits > 1 ? (size_t)a.e.splits * a.e.slab * sizeof(float) : 0;
       return true;
     }
   }
@@ -622,6 +1170,19 @@ bool make_plan(const Shape& s, IgPlan& pl, int64_t N1 = -1) {
 }
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+// Store piece of the epilogue (store_tile): the largest of 8, 4, 2, 1
+// elements that divides P*Q and whose stores stay aligned in y.
+int store_piece(const Shape& s, const void* y) {
+  const int64_t PQ = s.P * s.Q;
+  for (int r = 8; r > 1; r >>= 1) {
+    const int64_t align = r * s.esize() < 16 ? r * s.esize() : 16;
+    if (PQ % r == 0 && reinterpret_cast<uintptr_t>(y) % align == 0) return r;
+  }
+  return 1;
+}
+
+
 
 template <typename T, int BM, int NG, int RST>
 hipError_t launch_one(const IgPlan& pl, const IgArgs& a, hipStream_t stream) {
@@ -635,14 +1196,14 @@ hipError_t launch_one(const IgPlan& pl, const IgArgs& a, hipStream_t stream) {
     if (e != hipSuccess) return e;
     lds_limit.store((int)kLdsLimit);
   }
-  const dim3 grid((a.NPQ + BN - 1) / BN, a.ktiles * a.G, a.splits);
+  const dim3 grid((a.NPQ + BN - 1) / BN, a.ktiles * a.G, a.e.splits);
   hipLaunchKernelGGL(kern, grid, dim3(kThreads), pl.lds, stream, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.splits == 1) return e;
+  if (e != hipSuccess || a.e.splits == 1) return e;
   const int total = a.N * a.K * a.P * a.Q;
   hipLaunchKernelGGL(splitk_reduce_kernel<T>, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, stream,
-                     a.partial, reinterpret_cast<const T*>(a.b), reinterpret_cast<T*>(a.y), total, a.slab, a.P * a.Q,
-                     a.K, a.splits, a.relu);
+                     a.e.partial, reinterpret_cast<const T*>(a.e.b), reinterpret_cast<T*>(a.e.y), total, a.e.slab,
+                     a.P * a.Q, a.K, a.e.splits, a.e.relu);
   return hipGetLastError();
 }
 
@@ -679,16 +1240,17 @@ hipError_t main_typed(const Shape& s, const void* x, const void* wp, const void*
     // split count.
     if (cnt != pl.images_per_launch && !make_plan<T>(s, cur, cnt)) return hipErrorInvalidValue;
     if (cur.NG != pl.NG || cur.BM != pl.BM) return hipErrorInvalidValue;
-    if (cur.a.splits > 1 && !part) return hipErrorInvalidValue;
+    if (cur.a.e.splits > 1 && !part) return hipErrorInvalidValue;
     IgArgs a = cur.a;
     a.x = reinterpret_cast<const T*>(x) + n0 * img_elems;
-    a.y = reinterpret_cast<T*>(y) + n0 * out_elems;
+    a.e.y = reinterpret_cast<T*>(y) + n0 * out_elems;
     a.x_bytes = (uint32_t)(cnt * img_elems * s.esize());
     a.wp = wp;
     a.wp_bytes = (uint32_t)pl.wp_bytes;
-    a.b = b;
-    a.partial = part;
-    a.vec_out = (s.P * s.Q) % 8 == 0 && reinterpret_cast<uintptr_t>(a.y) % 16 == 0;
+    a.e.b = b;
+    a.e.partial = part;
+    a.e.NPQ = a.NPQ;
+    a.e.vec = store_piece(s, a.e.y);
     hipError_t e;
     if (pl.BM == 64)
       e = pl.NG == 2 ? launch_rst<T, 64, 2>(cur, a, stream) : launch_rst<T, 64, 1>(cur, a, stream);
@@ -697,6 +1259,191 @@ hipError_t main_typed(const Shape& s, const void* x, const void* wp, const void*
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+// ---- 1x1 layers ----
+
+struct PwPlan {
+  int BM;
+  bool gather;
+  int dma;               // bf16 LDS-DMA kernel: bytes per DMA unit (16 or 4), 0 = not used
+  int64_t images_per_launch;
+  size_t part_bytes;
+  size_t lds;
+  PwArgs a;
+};
+
+template <typename T>
+bool make_pw_plan(const Shape& s, PwPlan& pl, int64_t N1 = -1) {
+  constexpr int UE = elem<T>::per16;
+  const int64_t img_bytes = s.C * s.H * s.W * s.esize();
+  if (s.R != 1 || s.S != 1 || s.G != 1 || s.C % UE != 0) return false;
+  if (img_bytes > kMaxLaunchBytes || s.K * s.C * s.esize() > kMaxLaunchBytes) return false;
+  if (N1 < 0) {
+    N1 = kMaxLaunchBytes / img_bytes;
+    if (N1 > s.N) N1 = s.N;
+    if (N1 < 1) N1 = 1;
+  }
+  pl.images_per_launch = N1;
+  PwArgs& a = pl.a;
+  a.C = (int)s.C; a.H = (int)s.H; a.W = (int)s.W; a.HW = (int)(s.H * s.W);
+  a.P = (int)s.P; a.Q = (int)s.Q; a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw;
+  a.NPQ = (int)(N1 * s.P * s.Q);
+  pl.BM = s.K <= 64 ? 64 : 128;
+  a.ktiles = (int)((s.K + pl.BM - 1) / pl.BM);
+  a.ptiles = (a.NPQ + BN - 1) / BN;
+  a.nch = (int)((s.C + kPwUnits * UE - 1) / (kPwUnits * UE));
+  pl.gather = !(s.sh == 1 && s.sw == 1 && s.ph == 0 && s.pw == 0 && (s.H * s.W) % 4 == 0);
+  pl.dma = 0;
+  if (sizeof(T) == 2 && s.sh == 1 && s.sw == 1 && s.ph == 0 && s.pw == 0) {
+    if ((s.H * s.W) % 8 == 0) pl.dma = 16;
+    else if ((s.H * s.W) % 2 == 0) pl.dma = 4;
+  }
+  if (pl.dma) pl.BM = 128;
+  split_chunks((int64_t)a.ptiles * a.ktiles, a.nch, &a.e.splits, &a.chunks_per_split);
+  a.e.K = (int)s.K; a.e.Kg = (int)s.K; a.e.PQ = (int)(s.P * s.Q); a.e.relu = s.relu ? 1 : 0;
+  a.e.NPQ = a.NPQ;
+  a.e.slab = (int)((N1 * s.K * s.P * s.Q + 3) & ~(int64_t)3);
+  pl.part_bytes = a.e.splits > 1 ? (size_t)a.e.splits * a.e.slab * sizeof(float) : 0;
+  const size_t tiles = (size_t)(pl.BM + BN) * kPwUnits * 16;
+  const size_t stage = (size_t)4 * 32 * (BN / 2) * sizeof(float);  // epilogue staging
+  pl.lds = tiles > stage ? tiles : stage;
+  if (pl.dma) pl.lds = (size_t)(kDmaStages + 1) * kDmaStageBytes;
+  return true;
+}
+
+// Persistent grid of the 1x1 kernel: a multiple of 8 workgroups (one per
+// XCD slot), as many as fit on the CUs at once (the 128-row tile holds one
+// workgroup per CU, the 64-row tile two).
+constexpr int kPwStages = 2;
+
+// The DMA kernel keeps kDmaStages chunks of 32 KiB in LDS: workgroups per
+// CU = 160 KiB / (kDmaStages * 32 KiB).
+int pw_dma_grid(const PwArgs& a) {
+  const int units = a.ptiles * a.ktiles * a.e.splits;
+  const int g = (units + 7) / 8 * 8;
+  const int resident = kCUs * (int)(kLdsLimit / ((size_t)(kDmaStages + 1) * kDmaStageBytes));
+  return g < resident ? g : resident;
+}
+
+int pw_grid(const PwArgs& a, int BM) {
+  const int units = a.ptiles * a.ktiles * a.e.splits;
+  const int g = (units + 7) / 8 * 8;
+  const int resident = kCUs * (BM == 64 ? 2 : 1);
+  return g < resident ? g : resident;
+}
+
+template <int UB>
+hipError_t pw_dma_launch(const PwPlan& pl, const PwArgs& a, hipStream_t stream) {
+  const auto kern = pointwise_dma_kernel<UB, kDmaStages>;
+  static std::atomic<int> lds_raised{0};
+  if (!lds_raised.load()) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsLimit);
+    if (e != hipSuccess) return e;
+    lds_raised.store(1);
+  }
+  const dim3 grid((unsigned)pw_dma_grid(a));
+  hipLaunchKernelGGL(kern, grid, dim3(2 * kThreads), pl.lds, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.e.splits == 1) return e;
+  const int total = (int)((int64_t)a.NPQ * a.e.K);
+  hipLaunchKernelGGL(splitk_reduce_kernel<bf16_t>, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, stream,
+                     a.e.partial, reinterpret_cast<const bf16_t*>(a.e.b), reinterpret_cast<bf16_t*>(a.e.y), total,
+                     a.e.slab, a.e.PQ, a.e.K, a.e.splits, a.e.relu);
+  return hipGetLastError();
+}
+
+template <typename T, int BM, bool GATHER>
+hipError_t pw_launch(const PwPlan& pl, const PwArgs& a, hipStream_t stream) {
+  const dim3 grid((unsigned)pw_grid(a, BM));
+  hipLaunchKernelGGL((pointwise_gemm_kernel<T, BM, GATHER, kPwStages>), grid, dim3(kThreads), pl.lds, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.e.splits == 1) return e;
+  const int total = (int)((int64_t)a.NPQ * a.e.K);
+  hipLaunchKernelGGL(splitk_reduce_kernel<T>, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, stream,
+                     a.e.partial, reinterpret_cast<const T*>(a.e.b), reinterpret_cast<T*>(a.e.y), total, a.e.slab,
+                     a.e.PQ, a.e.K, a.e.splits, a.e.relu);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t pw_main_typed(const Shape& s, const void* x, const void* w, const void* b, void* y, void* part_ws,
+                         hipStream_t stream) {
+  PwPlan pl;
+  if (!make_pw_plan<T>(s, pl)) return hipErrorInvalidValue;
+  if (reinterpret_cast<uintptr_t>(w) % 16 != 0) return hipErrorInvalidValue;
+  float* part = reinterpret_cast<float*>(part_ws);
+  const int64_t img_elems = s.C * s.H * s.W, out_elems = s.K * s.P * s.Q;
+  for (int64_t n0 = 0; n0 < s.N; n0 += pl.images_per_launch) {
+    const int64_t cnt = s.N - n0 < pl.images_per_launch ? s.N - n0 : pl.images_per_launch;
+    PwPlan cur = pl;
+    if (cnt != pl.images_per_launch && !make_pw_plan<T>(s, cur, cnt)) return hipErrorInvalidValue;
+    if (cur.a.e.splits > 1 && !part) return hipErrorInvalidValue;
+    PwArgs a = cur.a;
+    a.x = reinterpret_cast<const T*>(x) + n0 * img_elems;
+    a.w = w;
+    a.x_bytes = (uint32_t)(cnt * img_elems * s.esize());
+    a.w_bytes = (uint32_t)(s.K * s.C * s.esize());
+    a.e.y = reinterpret_cast<T*>(y) + n0 * out_elems;
+    a.e.b = b;
+    a.e.partial = part;
+    a.e.vec = store_piece(s, a.e.y);
+    // Pixel-quad loads need the input aligned to 4 elements, DMA units to
+    // their size.
+    const bool gather = cur.gather || reinterpret_cast<uintptr_t>(a.x) % (4 * s.esize()) != 0;
+    hipError_t e;
+    if (cur.dma && reinterpret_cast<uintptr_t>(a.x) % cur.dma == 0)
+      e = cur.dma == 16 ? pw_dma_launch<16>(cur, a, stream) : pw_dma_launch<4>(cur, a, stream);
+    else if (cur.BM == 64)
+      e = gather ? pw_launch<T, 64, true>(cur, a, stream) : pw_launch<T, 64, false>(cur, a, stream);
+    else
+      e = gather ? pw_launch<T, 128, true>(cur, a, stream) : pw_launch<T, 128, false>(cur, a, stream);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+template <typename T>
+size_t pw_split_bytes(const Shape& s) {
+  PwPlan pl;
+  if (!make_pw_plan<T>(s, pl)) return 0;
+  size_t part = pl.part_bytes;
+  const int64_t rem = s.N % pl.images_per_launch;
+  if (rem) {
+    PwPlan last;
+    if (make_pw_plan<T>(s, last, rem) && last.part_bytes > part) part = last.part_bytes;
+  }
+  return part;
+}
+
+template <typename T>
+std::string pw_describe(const Shape& s) {
+  PwPlan pl;
+  make_pw_plan<T>(s, pl);
+  char buf[512];
+  const char* tn = sizeof(T) == 2 ? "bf16" : "f32";
+  if (pl.dma) {
+    snprintf(buf, sizeof(buf),
+             "implicit_gemm kernels=pointwise_dma_kernel<%d,%d>%s tile=128x%d units=%dx%dx%d grid=%d chunk=64 "
+             "lds=%zu images_per_launch=%lld (1x1: filters used as given; input staged by LDS DMA when 16-byte "
+             "aligned)",
+             pl.dma, kDmaStages, pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "", BN, pl.a.ptiles, pl.a.ktiles,
+             pl.a.e.splits, pw_dma_grid(pl.a), pl.lds, (long long)pl.images_per_launch);
+    return buf;
+  }
+  snprintf(buf, sizeof(buf),
+           "implicit_gemm kernels=pointwise_gemm_kernel<%s,%d,%d,%d>%s tile=%dx%d units=%dx%dx%d grid=%d "
+           "chunk=%d lds=%zu images_per_launch=%lld (1x1: filters used as given)",
+           tn, pl.BM, pl.gather ? 1 : 0, kPwStages, pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "", pl.BM, BN,
+           pl.a.ptiles, pl.a.ktiles, pl.a.e.splits, pw_grid(pl.a, pl.BM), kPwUnits * elem<T>::per16, pl.lds,
+           (long long)pl.images_per_launch);
+  return buf;
+}
+
+bool use_pointwise(const Shape& s) {
+  PwPlan pl;
+  return s.dtype == DT_F32 ? make_pw_plan<float>(s, pl) : make_pw_plan<bf16_t>(s, pl);
 }
 
 template <typename T>
@@ -721,8 +1468,8 @@ std::string describe_typed(const Shape& s) {
   snprintf(buf, sizeof(buf),
            "implicit_gemm kernels=pack_filters_kernel<%s>;implicit_gemm_kernel<%s,%d,%d,%d>%s tile=%dx%d "
            "grid=%dx%dx%d chunk=%d halo_rows=%d lds=%zu images_per_launch=%lld",
-           tn, tn, pl.BM, pl.NG, pl.RST, pl.a.splits > 1 ? ";splitk_reduce_kernel" : "", pl.BM, BN,
-           (pl.a.NPQ + BN - 1) / BN, pl.a.ktiles * s.G, pl.a.splits, pl.NG * elem<T>::per16, pl.a.VR, pl.lds,
+           tn, tn, pl.BM, pl.NG, pl.RST, pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "", pl.BM, BN,
+           (pl.a.NPQ + BN - 1) / BN, pl.a.ktiles * s.G, pl.a.e.splits, pl.NG * elem<T>::per16, pl.a.VR, pl.lds,
            (long long)pl.images_per_launch);
   return buf;
 }
@@ -730,18 +1477,21 @@ std::string describe_typed(const Shape& s) {
 }  // namespace
 
 bool implicit_gemm_fits(const Shape& s) {
+  if (use_pointwise(s)) return true;
   IgPlan pl;
   if (s.dtype == DT_F32) return make_plan<float>(s, pl);
   return make_plan<bf16_t>(s, pl);
 }
 
 size_t implicit_gemm_packed_bytes(const Shape& s) {
+  if (use_pointwise(s)) return (size_t)(s.K * s.C * s.esize());  // a plain copy of the filters
   IgPlan pl;
   const bool ok = s.dtype == DT_F32 ? make_plan<float>(s, pl) : make_plan<bf16_t>(s, pl);
   return ok ? pl.wp_bytes : 0;
 }
 
 size_t implicit_gemm_split_bytes(const Shape& s) {
+  if (use_pointwise(s)) return s.dtype == DT_F32 ? pw_split_bytes<float>(s) : pw_split_bytes<bf16_t>(s);
   return s.dtype == DT_F32 ? split_bytes_typed<float>(s) : split_bytes_typed<bf16_t>(s);
 }
 
@@ -750,25 +1500,34 @@ size_t implicit_gemm_workspace(const Shape& s) {
 }
 
 hipError_t launch_implicit_pack(const Shape& s, const void* w, void* wp, hipStream_t stream) {
+  if (use_pointwise(s)) return launch_copy(w, wp, implicit_gemm_packed_bytes(s), stream);
   return s.dtype == DT_F32 ? pack_typed<float>(s, w, wp, stream) : pack_typed<bf16_t>(s, w, wp, stream);
 }
 
 hipError_t launch_implicit_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* part,
                                 hipStream_t stream) {
+  if (use_pointwise(s))
+    return s.dtype == DT_F32 ? pw_main_typed<float>(s, x, wp, b, y, part, stream)
+                             : pw_main_typed<bf16_t>(s, x, wp, b, y, part, stream);
   return s.dtype == DT_F32 ? main_typed<float>(s, x, wp, b, y, part, stream)
                            : main_typed<bf16_t>(s, x, wp, b, y, part, stream);
 }
 
 hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, const void* b, void* y, void* ws,
                                 hipStream_t stream) {
+  char* part = ws ? reinterpret_cast<char*>(ws) + align256(implicit_gemm_packed_bytes(s)) : nullptr;
+  // A 1x1 layer reads its filters as given when they are 16-byte aligned;
+  // otherwise (and for every other layer) the package is built in the
+  // workspace first.
+  if (use_pointwise(s) && reinterpret_cast<uintptr_t>(w) % 16 == 0) return launch_implicit_main(s, x, w, b, y, part, stream);
   if (!ws) return hipErrorInvalidValue;
   hipError_t e = launch_implicit_pack(s, w, ws, stream);
   if (e != hipSuccess) return e;
-  return launch_implicit_main(s, x, ws, b, y, reinterpret_cast<char*>(ws) + align256(implicit_gemm_packed_bytes(s)),
-                              stream);
+  return launch_implicit_main(s, x, ws, b, y, part, stream);
 }
 
 std::string implicit_gemm_describe(const Shape& s) {
+  if (use_pointwise(s)) return s.dtype == DT_F32 ? pw_describe<float>(s) : pw_describe<bf16_t>(s);
   return s.dtype == DT_F32 ? describe_typed<float>(s) : describe_typed<bf16_t>(s);
 }
 

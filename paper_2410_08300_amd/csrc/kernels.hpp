@@ -44,6 +44,9 @@ struct GemmArgs {
 
 hipError_t launch_gemm_nt(int dtype, const GemmArgs& g, hipStream_t stream);
 
+// Byte copy of `bytes` from src to dst (dst 16-byte aligned).
+hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
+
 // direct convolution (VALU), all N images.
 hipError_t launch_direct(const Shape& s, const void* x, const void* w, const void* b, void* y,
                          hipStream_t stream);

@@ -125,6 +125,17 @@ def test_workspace_sizes():
     small = _lib.make_desc(32, 512, 7, 7, 512, 3, 3, 1, 1, 1, 1, "bf16")
     packed = 32 * 512 * 18 * 16
     assert _lib.workspace_bytes(small, "implicit_gemm") == packed + 4 * 32 * 512 * 49 * 4
+    # 1x1 layers: the package is a plain copy of the K x C filters.
+    # 256 -> 64 channels, 56x56, batch 32: 784 pixel tiles, no split.
+    pw = _lib.make_desc(32, 256, 56, 56, 64, 1, 1, 1, 0, 1, 1, "bf16")
+    assert _lib.workspace_bytes(pw, "implicit_gemm") == 64 * 256 * 2
+    assert _lib.packed_filter_bytes(pw, "implicit_gemm") == 64 * 256 * 2
+    # 2048 -> 512 channels, 7x7, batch 32: 13 x 4 tiles; 32 chunks of 64
+    # channels split four ways.
+    pws = _lib.make_desc(32, 2048, 7, 7, 512, 1, 1, 1, 0, 1, 1, "bf16")
+    assert _lib.workspace_bytes(pws, "implicit_gemm") == 512 * 2048 * 2 + 4 * 32 * 512 * 49 * 4
+    assert "pointwise_gemm_kernel<bf16,128,1,2>;splitk_reduce_kernel" in _lib.describe(pws, "implicit_gemm")
+    assert "pointwise_dma_kernel<16,4>" in _lib.describe(pw, "implicit_gemm")
 
 
 def test_default_rule():

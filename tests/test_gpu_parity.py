@@ -70,10 +70,14 @@ def sweep_cases(count, seed):
     return cases
 
 
-@pytest.mark.parametrize("case", sweep_cases(48, 2024), ids=lambda c: "x".join(map(str, c[:7])) + "_" + c[11])
-def test_random_shape_sweep(case):
+SWEEP = sweep_cases(48, 2024)
+
+
+@pytest.mark.parametrize("idx", range(len(SWEEP)), ids=lambda i: "%d_" % i + "x".join(map(str, SWEEP[i][:7])) + "_" + SWEEP[i][11])
+def test_random_shape_sweep(idx):
+    case = SWEEP[idx]
     N, C, H, Wd, K, R, S, st, pd, dl, G, dtype, bias, relu = case
-    g = torch.Generator().manual_seed(hash(case) & 0xffffffff)
+    g = torch.Generator().manual_seed(W.seed_for(7, idx))
     x = torch.randn(N, C, H, Wd, generator=g).to(TDT[dtype])
     w = (torch.randn(K, C // G, R, S, generator=g) * (2.0 / ((C // G) * R * S)) ** 0.5).to(TDT[dtype])
     b = (torch.randn(K, generator=g) * 0.1).to(TDT[dtype]) if bias else None
@@ -236,3 +240,57 @@ def test_swapped_model_matches_oracle_chain_and_caches_packages():
         assert torch.equal(out, out2)
     convs = [m for m in model.modules() if isinstance(m, cs.Conv2dSwap)]
     assert all(len(m._packages) >= 1 for m in convs)
+
+
+# 1x1 layers take their own kernel (filters used as given, pixel-quad loads
+# transposed in registers) when C is a multiple of the 16-byte unit; strided,
+# padded or odd-plane layers and unaligned inputs take its gather variant;
+# unaligned filters are copied first.  Each case names the path it covers.
+POINTWISE = [
+    # N, C, H, W, K, stride, pad, dtype, bias, relu, what
+    (3, 72, 10, 10, 200, 1, 0, "bf16", True, True, "contiguous, channel / filter / pixel tails"),
+    (3, 36, 10, 10, 200, 1, 0, "f32", True, False, "contiguous fp32, channel tail"),
+    (2, 64, 15, 15, 96, 2, 0, "bf16", False, False, "stride 2 (gather)"),
+    (2, 32, 15, 15, 96, 2, 0, "f32", True, True, "stride 2 fp32 (gather)"),
+    (5, 128, 7, 7, 256, 1, 0, "bf16", False, True, "7x7 plane, not a multiple of 4 (gather)"),
+    (2, 16, 6, 6, 32, 1, 1, "bf16", True, False, "padding 1 (gather, zero border)"),
+    (2, 1000, 7, 7, 300, 1, 0, "bf16", True, True, "channel split over workgroups, tail chunk"),
+    (2, 40, 9, 12, 40, 1, 0, "f32", False, False, "K <= 64 tile"),
+    (4, 24, 28, 28, 64, 1, 0, "bf16", False, False, "single partial chunk"),
+]
+
+
+@pytest.mark.parametrize("idx", range(len(POINTWISE)), ids=lambda i: POINTWISE[i][-1].replace(" ", "_"))
+def test_pointwise_paths(idx):
+    N, C, H, Wd, K, st, pd, dtype, bias, relu, what = POINTWISE[idx]
+    g = torch.Generator().manual_seed(W.seed_for(11, idx))
+    x = torch.randn(N, C, H, Wd, generator=g).to(TDT[dtype])
+    w = (torch.randn(K, C, 1, 1, generator=g) * (2.0 / C) ** 0.5).to(TDT[dtype])
+    b = (torch.randn(K, generator=g) * 0.1).to(TDT[dtype]) if bias else None
+    check_full(x, w, b, st, pd, 1, 1, relu, ("implicit_gemm", "im2col_gemm", "direct"), what)
+
+
+@pytest.mark.parametrize("which", ["x", "w"])
+def test_pointwise_unaligned_operands(which):
+    """1x1 layer with the input (gather variant) or the filters (copied into
+    the workspace first) one element past a 16-byte boundary."""
+    N, C, H, Wd, K = 2, 64, 12, 12, 80
+    g = torch.Generator().manual_seed(W.seed_for(12, 0 if which == "x" else 1))
+    x = torch.randn(N, C, H, Wd, generator=g).to(torch.bfloat16)
+    w = (torch.randn(K, C, 1, 1, generator=g) * (2.0 / C) ** 0.5).to(torch.bfloat16)
+    ref = oracle.conv2d(f64(x), f64(w), None, 1, 0, 1, 1, False)
+    xd, wd = x.to(DEV), w.to(DEV)
+    if which == "x":
+        buf = torch.empty(xd.numel() + 1, dtype=xd.dtype, device=DEV)
+        buf[1:].copy_(xd.reshape(-1))
+        xd = buf[1:].view(xd.shape)
+        assert xd.data_ptr() % 16 != 0
+    else:
+        buf = torch.empty(wd.numel() + 1, dtype=wd.dtype, device=DEV)
+        buf[1:].copy_(wd.reshape(-1))
+        wd = buf[1:].view(wd.shape)
+        assert wd.data_ptr() % 16 != 0
+    say("case unaligned", which)
+    y = cs.conv2d(xd, wd, None, algo="implicit_gemm")
+    torch.cuda.synchronize()
+    assert rel_err(f64(y), ref) <= tolerance("bf16", "implicit_gemm")
