@@ -61,6 +61,7 @@ struct EpiArgs {
   void* y;             // first image of this launch
   float* partial;      // splits > 1: fp32 partial sums, [split][N][K][P][Q]
   int K, Kg, NPQ, PQ, relu;
+  int span;            // pixels per image in the tile index space: P*Q, or a padded plane (a multiple of 8)
   int splits;          // workgroups sharing one output tile along the channels
   int slab;            // floats per split of `partial` (N*K*P*Q rounded up to 4)
   int vec;             // store piece in elements (8, 4, 2 or 1; see store_tile)
@@ -169,9 +170,14 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / 64][BN / 6
 
   const int cb = (lane & 7) * 8;
   const int j = j0 + wn * EW + cb;
-  const int nvalid = min(8, e.NPQ - j);  // pixels of the run inside the output (<= 0: none)
-  const int n = j / PQ, pq = j - n * PQ;
-  const int wrap = PQ - pq;              // run pixels before the next image starts
+  // Pixel j of the tile index space is pixel pq of image n.  With a padded
+  // plane (span > P*Q, a multiple of 8) a run never crosses an image and its
+  // pixels past P*Q are padding; otherwise a run may cross into the next
+  // image after `wrap` pixels.
+  const int span = e.span;
+  const int n = j / span, pq = j - n * span;
+  const int nvalid = j >= e.NPQ ? 0 : span == PQ ? min(8, e.NPQ - j) : min(8, PQ - pq);  // <= 0: none
+  const int wrap = span == PQ ? PQ - pq : 8;
   const int64_t next_img = static_cast<int64_t>(e.K - 1) * PQ;
   const int i0 = k0 + wm * (BM / 2) + (lane >> 3);
   const int64_t obase = (static_cast<int64_t>(n) * e.K + g * e.Kg + i0) * PQ + pq;
@@ -488,10 +494,10 @@ __global__ __launch_bounds__(kThreads) void implicit_gemm_kernel(IgArgs a) {
 // 4, use the same kernel with one element load per pixel (GATHER).
 // ---------------------------------------------------------------------------
 struct PwArgs {
-  const void* x;        // first image of this launch
+  const void* x;        // first image of this launch (the DMA kernel: possibly the repacked input)
   const void* w;        // K x C filters (a 1x1 layer's KCRS layout)
   uint32_t x_bytes, w_bytes;
-  int C, H, W, HW, P, Q, sh, sw, ph, pw;
+  int C, H, W, HW, P, Q, sh, sw, ph, pw;  // HW: input plane (the DMA kernel: its pixel span)
   int NPQ, ktiles, ptiles, nch, chunks_per_split;
   EpiArgs e;
 };
@@ -981,6 +987,36 @@ __global__ __launch_bounds__(2 * kThreads) void pointwise_dma_kernel(PwArgs a) {
   }
 }
 
+// Input of the 1x1 DMA kernel for layers whose plane is not a multiple of 8
+// pixels, or that are strided or padded: xr[n][c][pix] = the input pixel
+// that output pixel pix = p*Q + q reads (zero outside the image), and zero
+// for P*Q <= pix < span (span = P*Q rounded up to 8).  Each thread writes 8
+// consecutive pixels (one 16-byte store).
+__global__ __launch_bounds__(256) void repack_plane_kernel(const uint16_t* __restrict__ x, uint16_t* __restrict__ xr,
+                                                           int planes, int H, int W, int P, int Q, int sh, int sw,
+                                                           int ph, int pw, int span) {
+  const int per_plane = span / 8;
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= planes * per_plane) return;
+  const int plane = t / per_plane, pix0 = (t - plane * per_plane) * 8;
+  const uint16_t* src = x + static_cast<int64_t>(plane) * H * W;
+  uint32_t v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int pix = pix0 + e;
+    const int p = pix / Q, q = pix - p * Q;
+    const int ih = p * sh - ph, iw = q * sw - pw;
+    const bool ok = pix < P * Q && ih >= 0 && ih < H && iw >= 0 && iw < W;
+    v[e] = ok ? src[ih * W + iw] : 0u;
+  }
+  uint4 o;
+  o.x = v[0] | (v[1] << 16);
+  o.y = v[2] | (v[3] << 16);
+  o.z = v[4] | (v[5] << 16);
+  o.w = v[6] | (v[7] << 16);
+  *reinterpret_cast<uint4*>(xr + static_cast<int64_t>(plane) * span + pix0) = o;
+}
+
 // Wp[g][ch][kp][tap][cg][e] = w[g*Kg + kp][ch*Cc + cg*UE + e][tap], zero past
 // Kg rows or Cg channels.  One workgroup per packed row (g, ch, kp); its
 // threads write the row's RS*NG*UE elements consecutively.
@@ -1133,6 +1169,7 @@ bool make_plan(const Shape& s, IgPlan& pl, int64_t N1 = -1) {
   a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw; a.dh = s.dh; a.dw = s.dw;
   a.Cg = (int)s.Cg; a.Kg = (int)s.Kg; a.G = s.G;
   a.e.K = (int)s.K; a.e.Kg = (int)s.Kg; a.e.relu = s.relu ? 1 : 0; a.e.PQ = (int)(s.P * s.Q);
+  a.e.span = a.e.PQ;
   a.Hv = (int)((s.P - 1) * s.sh + (s.R - 1) * s.dh + 1);
   a.Wv = (int)((s.Q - 1) * s.sw + (s.S - 1) * s.dw + 1);
   a.VR = halo_rows(s, N1, a.Hv);
@@ -1266,7 +1303,10 @@ hipError_t main_typed(const Shape& s, const void* x, const void* wp, const void*
 struct PwPlan {
   int BM;
   bool gather;
-  int dma;               // bf16 LDS-DMA kernel: bytes per DMA unit (16 or 4), 0 = not used
+  bool dma;              // bf16: the LDS-DMA kernel
+  bool repack;           // ... on a repacked input (see repack_plane_kernel)
+  int span;              // pixels per image of the tile index space
+  size_t repack_bytes;   // repacked input of one launch
   int64_t images_per_launch;
   size_t part_bytes;
   size_t lds;
@@ -1274,10 +1314,17 @@ struct PwPlan {
 };
 
 template <typename T>
-bool make_pw_plan(const Shape& s, PwPlan& pl, int64_t N1 = -1) {
+bool make_pw_plan(const Shape& s, PwPlan& pl, int64_t N1 = -1, bool allow_dma = true) {
   constexpr int UE = elem<T>::per16;
-  const int64_t img_bytes = s.C * s.H * s.W * s.esize();
   if (s.R != 1 || s.S != 1 || s.G != 1 || s.C % UE != 0) return false;
+  // bf16: the DMA kernel, on the input as it is when its plane is a
+  // multiple of 8 pixels and the layer unstrided and unpadded, else on a
+  // repacked copy (plane = P*Q rounded up to 8).
+  pl.dma = sizeof(T) == 2 && allow_dma;
+  pl.repack = pl.dma && !(s.sh == 1 && s.sw == 1 && s.ph == 0 && s.pw == 0 && (s.H * s.W) % 8 == 0);
+  pl.span = pl.repack ? (int)((s.P * s.Q + 7) / 8 * 8) : pl.dma ? (int)(s.H * s.W) : (int)(s.P * s.Q);
+  int64_t img_bytes = s.C * s.H * s.W * s.esize();
+  if (pl.repack && s.C * pl.span * s.esize() > img_bytes) img_bytes = s.C * pl.span * s.esize();
   if (img_bytes > kMaxLaunchBytes || s.K * s.C * s.esize() > kMaxLaunchBytes) return false;
   if (N1 < 0) {
     N1 = kMaxLaunchBytes / img_bytes;
@@ -1286,23 +1333,20 @@ bool make_pw_plan(const Shape& s, PwPlan& pl, int64_t N1 = -1) {
   }
   pl.images_per_launch = N1;
   PwArgs& a = pl.a;
-  a.C = (int)s.C; a.H = (int)s.H; a.W = (int)s.W; a.HW = (int)(s.H * s.W);
+  a.C = (int)s.C; a.H = (int)s.H; a.W = (int)s.W;
+  a.HW = pl.dma ? pl.span : (int)(s.H * s.W);
   a.P = (int)s.P; a.Q = (int)s.Q; a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw;
-  a.NPQ = (int)(N1 * s.P * s.Q);
-  pl.BM = s.K <= 64 ? 64 : 128;
+  a.NPQ = (int)(N1 * (pl.dma ? pl.span : s.P * s.Q));
+  pl.BM = pl.dma || s.K > 64 ? 128 : 64;
   a.ktiles = (int)((s.K + pl.BM - 1) / pl.BM);
   a.ptiles = (a.NPQ + BN - 1) / BN;
   a.nch = (int)((s.C + kPwUnits * UE - 1) / (kPwUnits * UE));
   pl.gather = !(s.sh == 1 && s.sw == 1 && s.ph == 0 && s.pw == 0 && (s.H * s.W) % 4 == 0);
-  pl.dma = 0;
-  if (sizeof(T) == 2 && s.sh == 1 && s.sw == 1 && s.ph == 0 && s.pw == 0) {
-    if ((s.H * s.W) % 8 == 0) pl.dma = 16;
-    else if ((s.H * s.W) % 2 == 0) pl.dma = 4;
-  }
-  if (pl.dma) pl.BM = 128;
+  pl.repack_bytes = pl.repack ? (size_t)N1 * s.C * pl.span * s.esize() : 0;
   split_chunks((int64_t)a.ptiles * a.ktiles, a.nch, &a.e.splits, &a.chunks_per_split);
   a.e.K = (int)s.K; a.e.Kg = (int)s.K; a.e.PQ = (int)(s.P * s.Q); a.e.relu = s.relu ? 1 : 0;
   a.e.NPQ = a.NPQ;
+  a.e.span = pl.dma ? pl.span : (int)(s.P * s.Q);
   a.e.slab = (int)((N1 * s.K * s.P * s.Q + 3) & ~(int64_t)3);
   pl.part_bytes = a.e.splits > 1 ? (size_t)a.e.splits * a.e.slab * sizeof(float) : 0;
   const size_t tiles = (size_t)(pl.BM + BN) * kPwUnits * 16;
@@ -1347,7 +1391,8 @@ hipError_t pw_dma_launch(const PwPlan& pl, const PwArgs& a, hipStream_t stream) 
   hipLaunchKernelGGL(kern, grid, dim3(2 * kThreads), pl.lds, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.e.splits == 1) return e;
-  const int total = (int)((int64_t)a.NPQ * a.e.K);
+  // Outputs: images x K x P*Q (a.NPQ counts the padded pixel span).
+  const int total = (int)((int64_t)(a.NPQ / a.e.span) * a.e.PQ * a.e.K);
   hipLaunchKernelGGL(splitk_reduce_kernel<bf16_t>, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, stream,
                      a.e.partial, reinterpret_cast<const bf16_t*>(a.e.b), reinterpret_cast<bf16_t*>(a.e.y), total,
                      a.e.slab, a.e.PQ, a.e.K, a.e.splits, a.e.relu);
@@ -1373,13 +1418,17 @@ hipError_t pw_main_typed(const Shape& s, const void* x, const void* w, const voi
   PwPlan pl;
   if (!make_pw_plan<T>(s, pl)) return hipErrorInvalidValue;
   if (reinterpret_cast<uintptr_t>(w) % 16 != 0) return hipErrorInvalidValue;
-  float* part = reinterpret_cast<float*>(part_ws);
+  // An unaligned input that would be read in place cannot go through the
+  // DMA: those calls take the register-transposing kernel.
+  if (pl.dma && !pl.repack && reinterpret_cast<uintptr_t>(x) % 16 != 0 && !make_pw_plan<T>(s, pl, -1, false))
+    return hipErrorInvalidValue;
+  char* ws = reinterpret_cast<char*>(part_ws);
   const int64_t img_elems = s.C * s.H * s.W, out_elems = s.K * s.P * s.Q;
   for (int64_t n0 = 0; n0 < s.N; n0 += pl.images_per_launch) {
     const int64_t cnt = s.N - n0 < pl.images_per_launch ? s.N - n0 : pl.images_per_launch;
     PwPlan cur = pl;
-    if (cnt != pl.images_per_launch && !make_pw_plan<T>(s, cur, cnt)) return hipErrorInvalidValue;
-    if (cur.a.e.splits > 1 && !part) return hipErrorInvalidValue;
+    if (cnt != pl.images_per_launch && !make_pw_plan<T>(s, cur, cnt, pl.dma)) return hipErrorInvalidValue;
+    if ((cur.repack || cur.a.e.splits > 1) && !ws) return hipErrorInvalidValue;
     PwArgs a = cur.a;
     a.x = reinterpret_cast<const T*>(x) + n0 * img_elems;
     a.w = w;
@@ -1387,34 +1436,56 @@ hipError_t pw_main_typed(const Shape& s, const void* x, const void* w, const voi
     a.w_bytes = (uint32_t)(s.K * s.C * s.esize());
     a.e.y = reinterpret_cast<T*>(y) + n0 * out_elems;
     a.e.b = b;
-    a.e.partial = part;
+    a.e.partial = reinterpret_cast<float*>(ws + align256(cur.repack_bytes));
     a.e.vec = store_piece(s, a.e.y);
-    // Pixel-quad loads need the input aligned to 4 elements, DMA units to
-    // their size.
-    const bool gather = cur.gather || reinterpret_cast<uintptr_t>(a.x) % (4 * s.esize()) != 0;
     hipError_t e;
-    if (cur.dma && reinterpret_cast<uintptr_t>(a.x) % cur.dma == 0)
-      e = cur.dma == 16 ? pw_dma_launch<16>(cur, a, stream) : pw_dma_launch<4>(cur, a, stream);
-    else if (cur.BM == 64)
-      e = gather ? pw_launch<T, 64, true>(cur, a, stream) : pw_launch<T, 64, false>(cur, a, stream);
-    else
-      e = gather ? pw_launch<T, 128, true>(cur, a, stream) : pw_launch<T, 128, false>(cur, a, stream);
+    if (cur.dma) {
+      if (cur.repack) {
+        const int planes = (int)(cnt * s.C);
+        const int threads = planes * (cur.span / 8);
+        hipLaunchKernelGGL(repack_plane_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream,
+                           reinterpret_cast<const uint16_t*>(a.x), reinterpret_cast<uint16_t*>(ws), planes,
+                           (int)s.H, (int)s.W, (int)s.P, (int)s.Q, s.sh, s.sw, s.ph, s.pw, cur.span);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        a.x = ws;
+        a.x_bytes = (uint32_t)(cnt * s.C * cur.span * s.esize());
+      }
+      e = pw_dma_launch<16>(cur, a, stream);
+    } else {
+      // Pixel-quad loads need the input aligned to 4 elements.
+      const bool gather = cur.gather || reinterpret_cast<uintptr_t>(a.x) % (4 * s.esize()) != 0;
+      if (cur.BM == 64)
+        e = gather ? pw_launch<T, 64, true>(cur, a, stream) : pw_launch<T, 64, false>(cur, a, stream);
+      else
+        e = gather ? pw_launch<T, 128, true>(cur, a, stream) : pw_launch<T, 128, false>(cur, a, stream);
+    }
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
 
+// Input-dependent workspace of a 1x1 layer: the repacked input (DMA kernel,
+// 256-byte aligned) followed by the split partial sums, the largest over
+// the launches.
 template <typename T>
 size_t pw_split_bytes(const Shape& s) {
   PwPlan pl;
   if (!make_pw_plan<T>(s, pl)) return 0;
-  size_t part = pl.part_bytes;
+  size_t need = (pl.repack_bytes ? align256(pl.repack_bytes) : 0) + pl.part_bytes;
   const int64_t rem = s.N % pl.images_per_launch;
   if (rem) {
     PwPlan last;
-    if (make_pw_plan<T>(s, last, rem) && last.part_bytes > part) part = last.part_bytes;
+    if (make_pw_plan<T>(s, last, rem)) {
+      const size_t n2 = (last.repack_bytes ? align256(last.repack_bytes) : 0) + last.part_bytes;
+      if (n2 > need) need = n2;
+    }
   }
-  return part;
+  // Calls that fall back to the register-transposing kernel (unaligned
+  // input) use their own split count.
+  PwPlan alt;
+  if (make_pw_plan<T>(s, alt, -1, false) && alt.part_bytes > need) need = alt.part_bytes;
+  return need;
 }
 
 template <typename T>
@@ -1425,11 +1496,11 @@ std::string pw_describe(const Shape& s) {
   const char* tn = sizeof(T) == 2 ? "bf16" : "f32";
   if (pl.dma) {
     snprintf(buf, sizeof(buf),
-             "implicit_gemm kernels=pointwise_dma_kernel<%d,%d>%s tile=128x%d units=%dx%dx%d grid=%d chunk=64 "
-             "lds=%zu images_per_launch=%lld (1x1: filters used as given; input staged by LDS DMA when 16-byte "
-             "aligned)",
-             pl.dma, kDmaStages, pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "", BN, pl.a.ptiles, pl.a.ktiles,
-             pl.a.e.splits, pw_dma_grid(pl.a), pl.lds, (long long)pl.images_per_launch);
+             "implicit_gemm kernels=%spointwise_dma_kernel<16,%d>%s tile=128x%d units=%dx%dx%d grid=%d chunk=64 "
+             "span=%d lds=%zu images_per_launch=%lld (1x1: filters used as given)",
+             pl.repack ? "repack_plane_kernel;" : "", kDmaStages, pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "",
+             BN, pl.a.ptiles, pl.a.ktiles, pl.a.e.splits, pw_dma_grid(pl.a), pl.span, pl.lds,
+             (long long)pl.images_per_launch);
     return buf;
   }
   snprintf(buf, sizeof(buf),

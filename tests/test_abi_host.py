@@ -130,11 +130,17 @@ def test_workspace_sizes():
     pw = _lib.make_desc(32, 256, 56, 56, 64, 1, 1, 1, 0, 1, 1, "bf16")
     assert _lib.workspace_bytes(pw, "implicit_gemm") == 64 * 256 * 2
     assert _lib.packed_filter_bytes(pw, "implicit_gemm") == 64 * 256 * 2
-    # 2048 -> 512 channels, 7x7, batch 32: 13 x 4 tiles; 32 chunks of 64
-    # channels split four ways.
+    # 2048 -> 512 channels, 7x7, batch 32: the 49-pixel planes are repacked
+    # into 56-pixel ones (32 x 2048 x 56 bf16), giving 14 x 4 tiles; the 32
+    # chunks of 64 channels are split four ways.
     pws = _lib.make_desc(32, 2048, 7, 7, 512, 1, 1, 1, 0, 1, 1, "bf16")
-    assert _lib.workspace_bytes(pws, "implicit_gemm") == 512 * 2048 * 2 + 4 * 32 * 512 * 49 * 4
-    assert "pointwise_gemm_kernel<bf16,128,1,2>;splitk_reduce_kernel" in _lib.describe(pws, "implicit_gemm")
+    repack = 32 * 2048 * 56 * 2
+    assert _lib.workspace_bytes(pws, "implicit_gemm") == 512 * 2048 * 2 + repack + 4 * 32 * 512 * 49 * 4
+    assert _lib.prepacked_workspace_bytes(pws, "implicit_gemm") == repack + 4 * 32 * 512 * 49 * 4
+    assert "repack_plane_kernel;pointwise_dma_kernel<16,4>;splitk_reduce_kernel" in _lib.describe(pws, "implicit_gemm")
+    # fp32 1x1 layers keep the register-transposing kernel.
+    pwf = _lib.make_desc(32, 256, 56, 56, 64, 1, 1, 1, 0, 1, 1, "f32")
+    assert "pointwise_gemm_kernel<f32,64,0,2>" in _lib.describe(pwf, "implicit_gemm")
     assert "pointwise_dma_kernel<16,4>" in _lib.describe(pw, "implicit_gemm")
 
 

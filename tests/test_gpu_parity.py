@@ -294,3 +294,61 @@ def test_pointwise_unaligned_operands(which):
     y = cs.conv2d(xd, wd, None, algo="implicit_gemm")
     torch.cuda.synchronize()
     assert rel_err(f64(y), ref) <= tolerance("bf16", "implicit_gemm")
+
+
+# Every byte a call writes must lie in y or in its workspace: the operands
+# and the workspace sit in one buffer between guard bands of a fill pattern,
+# and after the call the guards and the inputs must be unchanged.
+GUARDED = [
+    # N, C, H, W, K, R, stride, pad, dtype, algos
+    (1, 1024, 14, 14, 512, 1, 1, 0, "bf16", ("implicit_gemm", "im2col_gemm")),
+    (2, 2048, 7, 7, 512, 1, 1, 0, "bf16", ("implicit_gemm",)),
+    (3, 64, 56, 56, 256, 1, 1, 0, "bf16", ("implicit_gemm",)),
+    (2, 256, 15, 15, 128, 1, 2, 0, "bf16", ("implicit_gemm", "im2col_gemm")),
+    (2, 512, 7, 7, 512, 3, 1, 1, "bf16", ("implicit_gemm", "winograd", "im2col_gemm")),
+    (1, 3, 33, 33, 64, 7, 2, 3, "bf16", ("implicit_gemm", "direct", "im2col_gemm")),
+    (2, 96, 9, 11, 40, 1, 1, 0, "f32", ("implicit_gemm", "direct")),
+    (2, 64, 10, 10, 64, 3, 1, 1, "f32", ("implicit_gemm", "winograd")),
+]
+
+
+@pytest.mark.parametrize("idx", range(len(GUARDED)), ids=lambda i: "x".join(map(str, GUARDED[i][:6])) + "_" + GUARDED[i][8])
+def test_writes_stay_in_output_and_workspace(idx):
+    from paper_2410_08300_amd import _lib
+    N, C, H, Wd, K, R, st, pd, dtype, algos = GUARDED[idx]
+    tdt = TDT[dtype]
+    es = 2 if dtype == "bf16" else 4
+    g = torch.Generator().manual_seed(W.seed_for(13, idx))
+    x = torch.randn(N, C, H, Wd, generator=g).to(tdt)
+    w = (torch.randn(K, C, R, R, generator=g) * (2.0 / (C * R * R)) ** 0.5).to(tdt)
+    b = (torch.randn(K, generator=g) * 0.1).to(tdt)
+    desc = _lib.make_desc(N, C, H, Wd, K, R, R, st, pd, 1, 1, dtype, True, False)
+    P, Q = _lib.output_shape(desc)
+    ref = oracle.conv2d(f64(x), f64(w), f64(b), st, pd, 1, 1, False)
+    guard = 4096
+    for algo in algos:
+        nws = _lib.workspace_bytes(desc, algo)
+        sizes = [x.numel() * es, w.numel() * es, b.numel() * es, nws, N * K * P * Q * es]
+        offs, pos = [], guard
+        for sz in sizes:
+            offs.append(pos)
+            pos += (sz + 255) // 256 * 256 + guard
+        buf = torch.full((pos,), 0xA5, dtype=torch.uint8, device=DEV)
+        for t, o in zip((x, w, b), offs):
+            buf[o:o + t.numel() * es].copy_(t.reshape(-1).view(torch.uint8).to(DEV))
+        before = buf.cpu()
+        base = buf.data_ptr()
+        say("case guarded", GUARDED[idx][:9], algo)
+        stv = _lib.conv2d_raw(base + offs[0], base + offs[1], base + offs[2], base + offs[4], desc, algo,
+                              base + offs[3] if nws else None, nws, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        assert stv == _lib.CONV_OK
+        after = buf.cpu()
+        ys, ye = offs[4], offs[4] + sizes[4]
+        wss, wse = offs[3], offs[3] + nws
+        changed = (after != before).nonzero().flatten()
+        outside = changed[~(((changed >= ys) & (changed < ye)) | ((changed >= wss) & (changed < wse)))]
+        assert outside.numel() == 0, "%s wrote %d bytes outside y and the workspace (first at offset %d)" % (
+            algo, outside.numel(), int(outside[0]) - ys)
+        y = after[ys:ye].view(tdt).reshape(N, K, P, Q)
+        assert rel_err(f64(y), ref) <= tolerance(dtype, algo)
