@@ -1,0 +1,295 @@
+// Pieces shared by the implicit GEMM kernels: tile constants, buffer-load
+// helpers, the tile epilogue, the split-K reduction and host-side planning
+// helpers.
+#pragma once
+
+#include <stdint.h>
+
+#include <type_traits>
+
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace convsel {
+namespace igemm {
+
+constexpr int kThreads = 256;
+constexpr int BN = 128;
+constexpr uint32_t kRsrcWord3 = 0x00020000u;  // raw buffer, 32-bit data format (gfx9 family)
+
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+
+// Output side of a tile, shared by the implicit GEMM kernels.
+struct EpiArgs {
+  const void* b;
+  void* y;             // first image of this launch
+  float* partial;      // splits > 1: fp32 partial sums, [split][N][K][P][Q]
+  int K, Kg, NPQ, PQ, relu;
+  int span;            // pixels per image in the tile index space: P*Q, or a padded plane (a multiple of 8)
+  int splits;          // workgroups sharing one output tile along the channels
+  int slab;            // floats per split of `partial` (N*K*P*Q rounded up to 4)
+  int vec;             // store piece in elements (8, 4, 2 or 1; see store_tile)
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, (int)kRsrcWord3);
+}
+
+__device__ __forceinline__ uint32_t buf_load_elem(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, float*) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+}
+__device__ __forceinline__ uint32_t buf_load_elem(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, bf16_t*) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
+}
+__device__ __forceinline__ vec16 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+  vec16 o;
+  o.d[0] = v[0];
+  o.d[1] = v[1];
+  o.d[2] = v[2];
+  o.d[3] = v[3];
+  return o;
+}
+
+// Calls f(std::integral_constant<int, i>{}) for i = 0 .. N-1 (compile-time
+// indices, so register arrays indexed by i stay in registers).
+template <int N, typename F, int I = 0>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, F, I + 1>(static_cast<F&&>(f));
+  }
+}
+
+// Bias, ReLU and the NCHW store of one BM x BN tile (rows k0.. of group g,
+// pixels j0..), or its raw fp32 partial sums when the channels are split.
+// The accumulators go through LDS (each wave stages its 32 x 64 block; the
+// caller provides 32 KiB) so that a lane then holds a run of 8 consecutive
+// pixels of one output channel: lane l takes pixels (l % 8) * 8 .. +7 of the
+// wave's 64 and rows l / 8 + 8 * it, it = 0..3, of each 32-row block.  Its
+// image, offset and the start of the next image are computed once per tile.
+// A run is stored in pieces of e.vec elements (8, 4, 2 or 1: the largest
+// that divides P*Q and keeps the stores aligned), so no piece crosses an
+// image boundary; a piece past the boundary moves to the next image.
+template <typename T, int BM>
+__device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / 64][BN / 64], vec16* smem, const EpiArgs& e,
+                                           int j0, int k0, int g, int split) {
+  constexpr int MI = BM / 64, NJ = BN / 64;
+  constexpr int EW = BN / 2;  // pixels per wave row
+  static_assert(EW == 64, "staging layout assumes 64 pixels per wave row");
+  const int tid = threadIdx.x, lane = tid & 63, wave = (tid >> 6) & 3;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l32 = lane & 31;
+  const int PQ = e.PQ;
+  const bool split_out = e.splits > 1;
+  float* part = split_out ? e.partial + static_cast<int64_t>(split) * e.slab : nullptr;
+  const T* bias = reinterpret_cast<const T*>(e.b);
+  T* y = reinterpret_cast<T*>(e.y);
+
+  // Each wave stages 32 rows x 64 pixels of fp32 (8 KiB).  Rows are
+  // unpadded; float4 f of row r sits at f ^ g(r), g(r) = (r & 1) | 8 *
+  // ((r >> 2) & 1): the two half-waves of a store (rows r and r+4) and the
+  // quarter-waves of a load (rows 2q, 2q+1) then touch distinct banks.
+  float* stage = reinterpret_cast<float*>(smem) + wave * 32 * EW;
+  auto spos = [](int r, int px) { return r * EW + ((((px >> 2) ^ (r & 1) ^ (((r >> 2) & 1) << 3))) << 2) + (px & 3); };
+
+  const int cb = (lane & 7) * 8;
+  const int j = j0 + wn * EW + cb;
+  // Pixel j of the tile index space is pixel pq of image n.  With a padded
+  // plane (span > P*Q, a multiple of 8) a run never crosses an image and its
+  // pixels past P*Q are padding; otherwise a run may cross into the next
+  // image after `wrap` pixels.
+  const int span = e.span;
+  const int n = j / span, pq = j - n * span;
+  const int nvalid = j >= e.NPQ ? 0 : span == PQ ? min(8, e.NPQ - j) : min(8, PQ - pq);  // <= 0: none
+  const int wrap = span == PQ ? PQ - pq : 8;
+  const int64_t next_img = static_cast<int64_t>(e.K - 1) * PQ;
+  const int i0 = k0 + wm * (BM / 2) + (lane >> 3);
+  const int64_t obase = (static_cast<int64_t>(n) * e.K + g * e.Kg + i0) * PQ + pq;
+
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi) {
+#pragma unroll
+    for (int nj = 0; nj < NJ; ++nj)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) stage[spos(mfma_row(v, lane), nj * 32 + l32)] = acc[mi][nj][v];
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int row = (lane >> 3) + 8 * it;
+      const int i = i0 + mi * 32 + 8 * it;
+      const float4 lo = *reinterpret_cast<const float4*>(stage + spos(row, cb));
+      const float4 hi = *reinterpret_cast<const float4*>(stage + spos(row, cb + 4));
+      if (i >= e.Kg || nvalid <= 0) continue;
+      const int64_t o = obase + static_cast<int64_t>(mi * 32 + 8 * it) * PQ;
+      float vals[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      if (split_out) {
+        if (e.vec == 8 && nvalid == 8) {
+          *reinterpret_cast<float4*>(part + o) = lo;
+          *reinterpret_cast<float4*>(part + o + 4) = hi;
+        } else {
+          for (int t = 0; t < nvalid; ++t) part[o + t + (t >= wrap ? next_img : 0)] = vals[t];
+        }
+        continue;
+      }
+      const float bv = bias ? elem<T>::load(bias + g * e.Kg + i) : 0.f;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        vals[t] += bv;
+        if (e.relu) vals[t] = fmaxf(vals[t], 0.f);
+      }
+      if constexpr (sizeof(T) == 2) {
+        uint32_t w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) w[q] = f32x2_to_bf16x2(vals[2 * q], vals[2 * q + 1]);
+        if (e.vec == 8 && nvalid == 8) {
+          *reinterpret_cast<uint4*>(y + o) = make_uint4(w[0], w[1], w[2], w[3]);
+        } else if (e.vec == 4) {
+          for (int t = 0; t < nvalid; t += 4)
+            *reinterpret_cast<uint2*>(y + o + t + (t >= wrap ? next_img : 0)) = make_uint2(w[t / 2], w[t / 2 + 1]);
+        } else if (e.vec == 2) {
+          for (int t = 0; t < nvalid; t += 2) *reinterpret_cast<uint32_t*>(y + o + t + (t >= wrap ? next_img : 0)) = w[t / 2];
+        } else {
+          for (int t = 0; t < nvalid; ++t) elem<T>::store(y + o + t + (t >= wrap ? next_img : 0), vals[t]);
+        }
+      } else {
+        float* yf = reinterpret_cast<float*>(y);
+        if (e.vec == 8 && nvalid == 8) {
+          *reinterpret_cast<float4*>(yf + o) = make_float4(vals[0], vals[1], vals[2], vals[3]);
+          *reinterpret_cast<float4*>(yf + o + 4) = make_float4(vals[4], vals[5], vals[6], vals[7]);
+        } else if (e.vec == 4) {
+          for (int t = 0; t < nvalid; t += 4)
+            *reinterpret_cast<float4*>(yf + o + t + (t >= wrap ? next_img : 0)) =
+                make_float4(vals[t], vals[t + 1], vals[t + 2], vals[t + 3]);
+        } else {
+          for (int t = 0; t < nvalid; ++t) yf[o + t + (t >= wrap ? next_img : 0)] = vals[t];
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();  // the next block reuses this wave's stage
+  }
+}
+
+// s_waitcnt with vmcnt = n and the other counters at their maximum (gfx9 encoding).
+#define CONVSEL_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (15 << 8))
+
+// The same for a count known only at run time (0 .. 63; uniform).
+__device__ __forceinline__ void wait_vmcnt(int n) {
+  static_for<64>([&](auto m) {
+    if (n == decltype(m)::value) CONVSEL_WAIT_VMCNT(decltype(m)::value);
+  });
+}
+
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+typedef short v8s_t __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// Sum of the split partials, plus bias, ReLU, rounding to the output type;
+// four consecutive outputs per thread (flat index: outputs stay below 2^31).
+template <typename T>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, const T* __restrict__ bias,
+                                                            T* __restrict__ y, int total, int slab, int PQ, int K,
+                                                            int splits, int relu) {
+  const int i0 = (blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i0 >= total) return;
+  const int n4 = total - i0 < 4 ? total - i0 : 4;
+  float sum[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < splits; ++s) {
+    const float* p = part + static_cast<int64_t>(s) * slab + i0;
+    if (n4 == 4) {
+      const float4 v = *reinterpret_cast<const float4*>(p);  // slabs and i0 are multiples of 4 floats
+      sum[0] += v.x; sum[1] += v.y; sum[2] += v.z; sum[3] += v.w;
+    } else {
+      for (int e = 0; e < n4; ++e) sum[e] += p[e];
+    }
+  }
+  for (int e = 0; e < n4; ++e) {
+    const int i = i0 + e;
+    float v = sum[e];
+    if (bias) v += elem<T>::load(bias + (i / PQ) % K);
+    if (relu) v = fmaxf(v, 0.f);
+    elem<T>::store(y + i, v);
+  }
+}
+
+// Largest halo span (in virtual rows) over all pixel tiles of N images.  The
+// span of a tile depends only on where it starts within an image, which
+// repeats every PQ / gcd(BN, PQ) tiles, so one period is scanned.
+inline int halo_rows(const Shape& s, int64_t N, int Hv) {
+  const int64_t PQ = s.P * s.Q, NPQ = N * PQ;
+  const int64_t tiles = (NPQ + BN - 1) / BN;
+  int64_t a = BN, b = PQ;
+  while (b) {
+    const int64_t t = a % b;
+    a = b;
+    b = t;
+  }
+  const int64_t period = PQ / a;
+  const int64_t scan = tiles < period + 1 ? tiles : period + 1;
+  auto vrow = [&](int64_t j) {
+    const int64_t n = j / PQ, pq = j % PQ;
+    return n * Hv + (pq / s.Q) * s.sh;
+  };
+  int64_t best = 0;
+  for (int64_t t = 0; t < scan; ++t) {
+    const int64_t j0 = t * BN;
+    const int64_t j1 = (j0 + BN < NPQ ? j0 + BN : NPQ) - 1;
+    const int64_t span = vrow(j1) - vrow(j0) + (s.R - 1) * s.dh + 1;
+    if (span > best) best = span;
+  }
+  // The last, possibly partial, tile.
+  {
+    const int64_t j0 = (tiles - 1) * BN;
+    const int64_t span = vrow(NPQ - 1) - vrow(j0) + (s.R - 1) * s.dh + 1;
+    if (span > best) best = span;
+  }
+  return (int)best;
+}
+
+// Two workgroups per CU fit in 80 KiB each; larger halos use up to the
+// 160 KiB a workgroup may hold.
+constexpr size_t kLdsPreferred = 80 * 1024;
+constexpr size_t kLdsLimit = 160 * 1024;
+// Each launch reads at most 1 GiB of input, so a buffer offset (at most the
+// buffer size, which marks out-of-range lanes) plus a channel offset stays
+// within 32 bits.
+constexpr int64_t kMaxLaunchBytes = (int64_t)1 << 30;
+constexpr int kCUs = 256;
+
+inline void split_chunks(int64_t tiles, int nch, int* splits, int* chunks_per_split) {
+  int best = 1;
+  double best_cost = 1e30;
+  if (tiles < kCUs) {
+    for (int S = 1; S <= 8 && S <= (nch + 1) / 2; ++S) {
+      const double waves = (double)((tiles * S + kCUs - 1) / kCUs) / S;
+      const double cost = waves + 0.05 * (S - 1);
+      if (cost < best_cost - 1e-9) {
+        best_cost = cost;
+        best = S;
+      }
+    }
+  }
+  *chunks_per_split = (nch + best - 1) / best;
+  *splits = (nch + *chunks_per_split - 1) / *chunks_per_split;
+}
+
+inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+// Store piece of the epilogue (store_tile): the largest of 8, 4, 2, 1
+// elements that divides P*Q and whose stores stay aligned in y.
+inline int store_piece(const Shape& s, const void* y) {
+  const int64_t PQ = s.P * s.Q;
+  for (int r = 8; r > 1; r >>= 1) {
+    const int64_t align = r * s.esize() < 16 ? r * s.esize() : 16;
+    if (PQ % r == 0 && reinterpret_cast<uintptr_t>(y) % align == 0) return r;
+  }
+  return 1;
+}
+
+
+
+
+}  // namespace igemm
+}  // namespace convsel

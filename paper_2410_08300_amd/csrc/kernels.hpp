@@ -67,6 +67,7 @@ hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, co
                                 hipStream_t stream);
 std::string implicit_gemm_describe(const Shape& s);
 
+
 // Column matrix [nb][G][P*Q][Cg*R*S] of images n0 .. n0+nb-1.
 hipError_t launch_im2col(const Shape& s, const void* x, void* col, int64_t n0, int64_t nb,
                          hipStream_t stream);
