@@ -376,11 +376,22 @@ def main():
     single = [(p, ms) for p, ms in zip(plan, lms_pk) if main_kernel(p["describe"]) == [dom]]
     dom_ms = sum(ms for _, ms in single)
     dom_flops = sum(p["layer"].flops for p, _ in single)
-    achieved = dom_flops / (dom_ms * 1e-3) / 1e12 if dom_ms > 0 else 0.0
+    dom_bytes = sum(p["layer"].compulsory_bytes() for p, _ in single)
     peak = PEAKS_TFLOPS[dtype]
+    # The kernel's roofline is the one its launches reach first: MFMA when the
+    # flops take longer at peak than the compulsory bytes at HBM peak, else HBM.
+    if dom_bytes / (HBM_GBS * 1e9) > dom_flops / (peak * 1e12):
+        bound, unit, peak_b = "hbm", "GB/s", HBM_GBS
+        achieved = dom_bytes / (dom_ms * 1e-3) / 1e9 if dom_ms > 0 else 0.0
+    else:
+        bound, unit, peak_b = "mfma", "TFLOP/s", peak
+        achieved = dom_flops / (dom_ms * 1e-3) / 1e12 if dom_ms > 0 else 0.0
     wl_name = "%s-n%d-%s" % (wl, layers[0].n, layers[0].dtype)
     traffic = recorded_traffic(dom, wl_name)
-    roofline = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+    roofline = {"bound": bound, "achieved": achieved, "peak": peak_b, "unit": unit, "frac": achieved / peak_b,
+                "algorithmic_bytes_per_launch": dom_bytes / max(len(single), 1),
+                "algorithmic_flops_per_launch": dom_flops / max(len(single), 1),
+                "tflops": dom_flops / (dom_ms * 1e-3) / 1e12 if dom_ms > 0 else 0.0,
                 "traffic": traffic["bytes"] if traffic else None, "traffic_detail": traffic,
                 "kernel": dom, "launches_per_step": len(single),
                 "avg_launch_us": dom_ms * 1e3 / max(len(single), 1),

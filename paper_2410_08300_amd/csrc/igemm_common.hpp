@@ -115,21 +115,36 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / 64][BN / 6
       for (int v = 0; v < 16; ++v) stage[spos(mfma_row(v, lane), nj * 32 + l32)] = acc[mi][nj][v];
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
     __builtin_amdgcn_wave_barrier();
+    // All four runs of this block are read from LDS before any is stored,
+    // so the reads overlap instead of each waiting on the previous store.
+    float4 lo[4], hi[4];
 #pragma unroll
     for (int it = 0; it < 4; ++it) {
       const int row = (lane >> 3) + 8 * it;
+      lo[it] = *reinterpret_cast<const float4*>(stage + spos(row, cb));
+      hi[it] = *reinterpret_cast<const float4*>(stage + spos(row, cb + 4));
+    }
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
       const int i = i0 + mi * 32 + 8 * it;
-      const float4 lo = *reinterpret_cast<const float4*>(stage + spos(row, cb));
-      const float4 hi = *reinterpret_cast<const float4*>(stage + spos(row, cb + 4));
       if (i >= e.Kg || nvalid <= 0) continue;
       const int64_t o = obase + static_cast<int64_t>(mi * 32 + 8 * it) * PQ;
-      float vals[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      float vals[8] = {lo[it].x, lo[it].y, lo[it].z, lo[it].w, hi[it].x, hi[it].y, hi[it].z, hi[it].w};
+      // Pieces past `wrap` belong to the next image.
+      auto at = [&](int t) { return o + t + (t >= wrap ? next_img : 0); };
       if (split_out) {
         if (e.vec == 8 && nvalid == 8) {
-          *reinterpret_cast<float4*>(part + o) = lo;
-          *reinterpret_cast<float4*>(part + o + 4) = hi;
+          *reinterpret_cast<float4*>(part + o) = lo[it];
+          *reinterpret_cast<float4*>(part + o + 4) = hi[it];
+        } else if (e.vec >= 4) {
+#pragma unroll
+          for (int t = 0; t < 8; t += 4)
+            if (t < nvalid)
+              *reinterpret_cast<float4*>(part + at(t)) = make_float4(vals[t], vals[t + 1], vals[t + 2], vals[t + 3]);
         } else {
-          for (int t = 0; t < nvalid; ++t) part[o + t + (t >= wrap ? next_img : 0)] = vals[t];
+#pragma unroll
+          for (int t = 0; t < 8; ++t)
+            if (t < nvalid) part[at(t)] = vals[t];
         }
         continue;
       }
@@ -145,25 +160,33 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / 64][BN / 6
         for (int q = 0; q < 4; ++q) w[q] = f32x2_to_bf16x2(vals[2 * q], vals[2 * q + 1]);
         if (e.vec == 8 && nvalid == 8) {
           *reinterpret_cast<uint4*>(y + o) = make_uint4(w[0], w[1], w[2], w[3]);
-        } else if (e.vec == 4) {
-          for (int t = 0; t < nvalid; t += 4)
-            *reinterpret_cast<uint2*>(y + o + t + (t >= wrap ? next_img : 0)) = make_uint2(w[t / 2], w[t / 2 + 1]);
+        } else if (e.vec >= 4) {
+#pragma unroll
+          for (int t = 0; t < 8; t += 4)
+            if (t < nvalid) *reinterpret_cast<uint2*>(y + at(t)) = make_uint2(w[t / 2], w[t / 2 + 1]);
         } else if (e.vec == 2) {
-          for (int t = 0; t < nvalid; t += 2) *reinterpret_cast<uint32_t*>(y + o + t + (t >= wrap ? next_img : 0)) = w[t / 2];
+#pragma unroll
+          for (int t = 0; t < 8; t += 2)
+            if (t < nvalid) *reinterpret_cast<uint32_t*>(y + at(t)) = w[t / 2];
         } else {
-          for (int t = 0; t < nvalid; ++t) elem<T>::store(y + o + t + (t >= wrap ? next_img : 0), vals[t]);
+#pragma unroll
+          for (int t = 0; t < 8; ++t)
+            if (t < nvalid) elem<T>::store(y + at(t), vals[t]);
         }
       } else {
         float* yf = reinterpret_cast<float*>(y);
         if (e.vec == 8 && nvalid == 8) {
           *reinterpret_cast<float4*>(yf + o) = make_float4(vals[0], vals[1], vals[2], vals[3]);
           *reinterpret_cast<float4*>(yf + o + 4) = make_float4(vals[4], vals[5], vals[6], vals[7]);
-        } else if (e.vec == 4) {
-          for (int t = 0; t < nvalid; t += 4)
-            *reinterpret_cast<float4*>(yf + o + t + (t >= wrap ? next_img : 0)) =
-                make_float4(vals[t], vals[t + 1], vals[t + 2], vals[t + 3]);
+        } else if (e.vec >= 4) {
+#pragma unroll
+          for (int t = 0; t < 8; t += 4)
+            if (t < nvalid)
+              *reinterpret_cast<float4*>(yf + at(t)) = make_float4(vals[t], vals[t + 1], vals[t + 2], vals[t + 3]);
         } else {
-          for (int t = 0; t < nvalid; ++t) yf[o + t + (t >= wrap ? next_img : 0)] = vals[t];
+#pragma unroll
+          for (int t = 0; t < 8; ++t)
+            if (t < nvalid) yf[at(t)] = vals[t];
         }
       }
     }

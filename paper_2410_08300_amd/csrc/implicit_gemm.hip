@@ -381,7 +381,6 @@ __global__ __launch_bounds__(kThreads) void pointwise_gemm_kernel(PwArgs a) {
   constexpr int MI = BM / 64, NJ = BN / 64;
   constexpr int CC = kPwUnits * UE;               // channels per chunk
   constexpr int AU = BM * kPwUnits / kThreads;    // filter units per thread
-  constexpr int BW = sizeof(T) == 2 ? 2 : 4;      // words per pixel-quad load
   extern __shared__ __align__(16) vec16 smem[];
   vec16* As = smem;                               // [BM][8], swizzled
   vec16* Bs = smem + BM * kPwUnits;               // [BN][8], swizzled
@@ -839,14 +838,25 @@ __global__ __launch_bounds__(256) void repack_plane_kernel(const uint16_t* __res
   if (t >= planes * per_plane) return;
   const int plane = t / per_plane, pix0 = (t - plane * per_plane) * 8;
   const uint16_t* src = x + static_cast<int64_t>(plane) * H * W;
+  const int PQ = P * Q;
   uint32_t v[8];
+  if (sh == 1 && sw == 1 && ph == 0 && pw == 0) {
+    // Unstrided, unpadded: output pixel pix is input pixel pix.
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int pix = pix0 + e;
-    const int p = pix / Q, q = pix - p * Q;
-    const int ih = p * sh - ph, iw = q * sw - pw;
-    const bool ok = pix < P * Q && ih >= 0 && ih < H && iw >= 0 && iw < W;
-    v[e] = ok ? src[ih * W + iw] : 0u;
+    for (int e = 0; e < 8; ++e) v[e] = pix0 + e < PQ ? src[pix0 + e] : 0u;
+  } else {
+    // Walk the 8 pixels along the output row (one division for the first).
+    int p = pix0 / Q, q = pix0 - p * Q;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int ih = p * sh - ph, iw = q * sw - pw;
+      const bool ok = pix0 + e < PQ && ih >= 0 && ih < H && iw >= 0 && iw < W;
+      v[e] = ok ? src[ih * W + iw] : 0u;
+      if (++q == Q) {
+        q = 0;
+        ++p;
+      }
+    }
   }
   uint4 o;
   o.x = v[0] | (v[1] << 16);
@@ -1283,7 +1293,7 @@ std::string describe_typed(const Shape& s) {
 }  // namespace
 
 bool implicit_gemm_fits(const Shape& s) {
-  if (use_pointwise(s)) return true;
+  if (use_pointwise(s) || rows_applies(s)) return true;
   IgPlan pl;
   if (s.dtype == DT_F32) return make_plan<float>(s, pl);
   return make_plan<bf16_t>(s, pl);
@@ -1291,12 +1301,14 @@ bool implicit_gemm_fits(const Shape& s) {
 
 size_t implicit_gemm_packed_bytes(const Shape& s) {
   if (use_pointwise(s)) return (size_t)(s.K * s.C * s.esize());  // a plain copy of the filters
+  if (rows_applies(s)) return (size_t)(s.K * s.C * s.R * s.S * s.esize());
   IgPlan pl;
   const bool ok = s.dtype == DT_F32 ? make_plan<float>(s, pl) : make_plan<bf16_t>(s, pl);
   return ok ? pl.wp_bytes : 0;
 }
 
 size_t implicit_gemm_split_bytes(const Shape& s) {
+  if (rows_applies(s)) return 0;
   if (use_pointwise(s)) return s.dtype == DT_F32 ? pw_split_bytes<float>(s) : pw_split_bytes<bf16_t>(s);
   return s.dtype == DT_F32 ? split_bytes_typed<float>(s) : split_bytes_typed<bf16_t>(s);
 }
@@ -1306,12 +1318,13 @@ size_t implicit_gemm_workspace(const Shape& s) {
 }
 
 hipError_t launch_implicit_pack(const Shape& s, const void* w, void* wp, hipStream_t stream) {
-  if (use_pointwise(s)) return launch_copy(w, wp, implicit_gemm_packed_bytes(s), stream);
+  if (use_pointwise(s) || rows_applies(s)) return launch_copy(w, wp, implicit_gemm_packed_bytes(s), stream);
   return s.dtype == DT_F32 ? pack_typed<float>(s, w, wp, stream) : pack_typed<bf16_t>(s, w, wp, stream);
 }
 
 hipError_t launch_implicit_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* part,
                                 hipStream_t stream) {
+  if (rows_applies(s)) return rows_main(s, x, wp, b, y, stream);
   if (use_pointwise(s))
     return s.dtype == DT_F32 ? pw_main_typed<float>(s, x, wp, b, y, part, stream)
                              : pw_main_typed<bf16_t>(s, x, wp, b, y, part, stream);
@@ -1324,7 +1337,8 @@ hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, co
   char* part = ws ? reinterpret_cast<char*>(ws) + align256(implicit_gemm_packed_bytes(s)) : nullptr;
   // A 1x1 layer reads its filters as given when they are 16-byte aligned;
   // otherwise (and for every other layer) the package is built in the
-  // workspace first.
+  // workspace first.  Filter-row layers read them as given.
+  if (rows_applies(s)) return rows_main(s, x, w, b, y, stream);
   if (use_pointwise(s) && reinterpret_cast<uintptr_t>(w) % 16 == 0) return launch_implicit_main(s, x, w, b, y, part, stream);
   if (!ws) return hipErrorInvalidValue;
   hipError_t e = launch_implicit_pack(s, w, ws, stream);
@@ -1333,6 +1347,7 @@ hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, co
 }
 
 std::string implicit_gemm_describe(const Shape& s) {
+  if (rows_applies(s)) return rows_describe(s);
   if (use_pointwise(s)) return s.dtype == DT_F32 ? pw_describe<float>(s) : pw_describe<bf16_t>(s);
   return s.dtype == DT_F32 ? describe_typed<float>(s) : describe_typed<bf16_t>(s);
 }

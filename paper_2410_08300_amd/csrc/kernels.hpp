@@ -47,6 +47,14 @@ hipError_t launch_gemm_nt(int dtype, const GemmArgs& g, hipStream_t stream);
 // Byte copy of `bytes` from src to dst (dst 16-byte aligned).
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
 
+// Implicit GEMM over filter rows (bf16, one group, 5 <= S <= 8, even column
+// stride, C*R <= 64: the wide-filter, few-channel layers such as a 7x7
+// stem).  Reads the filters as given (K x C x R x S, any alignment); no
+// workspace.
+bool rows_applies(const Shape& s);
+hipError_t rows_main(const Shape& s, const void* x, const void* w, const void* b, void* y, hipStream_t stream);
+std::string rows_describe(const Shape& s);
+
 // direct convolution (VALU), all N images.
 hipError_t launch_direct(const Shape& s, const void* x, const void* w, const void* b, void* y,
                          hipStream_t stream);

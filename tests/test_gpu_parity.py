@@ -296,6 +296,61 @@ def test_pointwise_unaligned_operands(which):
     assert rel_err(f64(y), ref) <= tolerance("bf16", "implicit_gemm")
 
 
+# Wide-filter, few-channel bf16 layers (5 <= S <= 8, even column stride,
+# C*R <= 64) take the filter-row kernel: the filter width padded to 8 and
+# each reduction slice one input row of the staged halo.  Each case names
+# the part of it that it covers.
+ROWS = [
+    # N, C, H, W, K, R, S, stride, pad, dilation, bias, relu, what
+    (2, 3, 40, 40, 64, 7, 7, 2, 3, 1, True, True, "stem-like 7x7 s2"),
+    (3, 3, 23, 29, 64, 7, 7, 2, 3, 1, False, False, "odd plane: tiles cross images"),
+    (2, 8, 20, 20, 40, 7, 7, 2, 3, 1, True, False, "C*R = 56 units, K tail"),
+    (2, 5, 19, 17, 130, 5, 5, 2, 2, 1, False, True, "5x5, three K tiles with tail, odd C*R"),
+    (2, 2, 17, 30, 64, 3, 8, 2, 1, 1, True, False, "1x8 taps wide, 3 rows"),
+    (2, 3, 26, 26, 32, 6, 6, (1, 2), (2, 3), (2, 1), False, False, "row stride 1, row dilation 2"),
+    (1, 1, 9, 70, 64, 5, 7, (3, 4), (0, 5), 1, True, True, "one channel, stride 3x4, wide pad"),
+]
+
+
+@pytest.mark.parametrize("idx", range(len(ROWS)), ids=lambda i: ROWS[i][-1].replace(" ", "_"))
+def test_filter_row_kernel(idx):
+    N, C, H, Wd, K, R, S, st, pd, dl, bias, relu, what = ROWS[idx]
+    g = torch.Generator().manual_seed(W.seed_for(14, idx))
+    x = torch.randn(N, C, H, Wd, generator=g).to(torch.bfloat16)
+    w = (torch.randn(K, C, R, S, generator=g) * (2.0 / (C * R * S)) ** 0.5).to(torch.bfloat16)
+    b = (torch.randn(K, generator=g) * 0.1).to(torch.bfloat16) if bias else None
+    check_full(x, w, b, st, pd, dl, 1, relu, ("implicit_gemm", "direct"), what)
+
+
+def test_filter_row_kernel_unaligned_filters_and_nonfinite_outside_taps():
+    """Stem-like layer with the filters one element past a 16-byte boundary,
+    and an input whose columns past every window's reach hold infinities:
+    the kernel's zero-weight taps (s >= S) must not pick them up."""
+    N, C, H, Wd, K = 2, 3, 21, 21, 64
+    g = torch.Generator().manual_seed(W.seed_for(15, 0))
+    x = torch.randn(N, C, H, Wd, generator=g).to(torch.bfloat16)
+    w = (torch.randn(K, C, 7, 7, generator=g) * (2.0 / 147) ** 0.5).to(torch.bfloat16)
+    # stride 2, pad 3: P = Q = 11 and the last window covers columns 17..23
+    # (21..23 padding), so column 20 is read; stride 2 without padding on
+    # the right: Q = 8, windows end at column 20, and tap s = 7 of the last
+    # output would read column 21 -- pass width 22 with inf there.
+    x2 = torch.cat([x, torch.full((N, C, H, 1), float("inf"), dtype=torch.bfloat16)], dim=3)
+    ref = oracle.conv2d(f64(x2), f64(w), None, 2, (3, 0), 1, 1, False)
+    assert np.isfinite(ref).all()
+    wd = torch.empty(w.numel() + 1, dtype=w.dtype, device=DEV)
+    wd[1:].copy_(w.reshape(-1).to(DEV))
+    wd = wd[1:].view(w.shape)
+    assert wd.data_ptr() % 16 != 0
+    from paper_2410_08300_amd import _lib
+    desc = _lib.make_desc(N, C, H, Wd + 1, K, 7, 7, 2, (3, 0), 1, 1, "bf16")
+    assert "implicit_rows_kernel" in _lib.describe(desc, "implicit_gemm")
+    say("case rows unaligned+inf")
+    y = cs.conv2d(x2.to(DEV), wd, None, 2, (3, 0), algo="implicit_gemm")
+    torch.cuda.synchronize()
+    assert torch.isfinite(y).all()
+    assert rel_err(f64(y), ref) <= tolerance("bf16", "implicit_gemm")
+
+
 # Every byte a call writes must lie in y or in its workspace: the operands
 # and the workspace sit in one buffer between guard bands of a fill pattern,
 # and after the call the guards and the inputs must be unchanged.
@@ -307,6 +362,7 @@ GUARDED = [
     (2, 256, 15, 15, 128, 1, 2, 0, "bf16", ("implicit_gemm", "im2col_gemm")),
     (2, 512, 7, 7, 512, 3, 1, 1, "bf16", ("implicit_gemm", "winograd", "im2col_gemm")),
     (1, 3, 33, 33, 64, 7, 2, 3, "bf16", ("implicit_gemm", "direct", "im2col_gemm")),
+    (3, 3, 29, 23, 64, 7, 2, 3, "bf16", ("implicit_gemm",)),
     (2, 96, 9, 11, 40, 1, 1, 0, "f32", ("implicit_gemm", "direct")),
     (2, 64, 10, 10, 64, 3, 1, 1, "f32", ("implicit_gemm", "winograd")),
 ]
