@@ -1301,7 +1301,7 @@ bool implicit_gemm_fits(const Shape& s) {
 
 size_t implicit_gemm_packed_bytes(const Shape& s) {
   if (use_pointwise(s)) return (size_t)(s.K * s.C * s.esize());  // a plain copy of the filters
-  if (rows_applies(s)) return (size_t)(s.K * s.C * s.R * s.S * s.esize());
+  if (rows_applies(s)) return rows_packed_bytes(s);
   IgPlan pl;
   const bool ok = s.dtype == DT_F32 ? make_plan<float>(s, pl) : make_plan<bf16_t>(s, pl);
   return ok ? pl.wp_bytes : 0;
@@ -1318,7 +1318,8 @@ size_t implicit_gemm_workspace(const Shape& s) {
 }
 
 hipError_t launch_implicit_pack(const Shape& s, const void* w, void* wp, hipStream_t stream) {
-  if (use_pointwise(s) || rows_applies(s)) return launch_copy(w, wp, implicit_gemm_packed_bytes(s), stream);
+  if (rows_applies(s)) return rows_pack(s, w, wp, stream);
+  if (use_pointwise(s)) return launch_copy(w, wp, implicit_gemm_packed_bytes(s), stream);
   return s.dtype == DT_F32 ? pack_typed<float>(s, w, wp, stream) : pack_typed<bf16_t>(s, w, wp, stream);
 }
 
@@ -1337,8 +1338,7 @@ hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, co
   char* part = ws ? reinterpret_cast<char*>(ws) + align256(implicit_gemm_packed_bytes(s)) : nullptr;
   // A 1x1 layer reads its filters as given when they are 16-byte aligned;
   // otherwise (and for every other layer) the package is built in the
-  // workspace first.  Filter-row layers read them as given.
-  if (rows_applies(s)) return rows_main(s, x, w, b, y, stream);
+  // workspace first.
   if (use_pointwise(s) && reinterpret_cast<uintptr_t>(w) % 16 == 0) return launch_implicit_main(s, x, w, b, y, part, stream);
   if (!ws) return hipErrorInvalidValue;
   hipError_t e = launch_implicit_pack(s, w, ws, stream);

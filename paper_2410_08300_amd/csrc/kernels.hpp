@@ -47,12 +47,14 @@ hipError_t launch_gemm_nt(int dtype, const GemmArgs& g, hipStream_t stream);
 // Byte copy of `bytes` from src to dst (dst 16-byte aligned).
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
 
-// Implicit GEMM over filter rows (bf16, one group, 5 <= S <= 8, even column
-// stride, C*R <= 64: the wide-filter, few-channel layers such as a 7x7
-// stem).  Reads the filters as given (K x C x R x S, any alignment); no
-// workspace.
+// Implicit GEMM over filter rows (bf16, one group, 5 <= S <= 8, S + (pw % 2)
+// <= 8, even column stride, C*R <= 64: the wide-filter, few-channel layers
+// such as a 7x7 stem).  The filter package (rows_packed_bytes) is the LDS
+// image of each 64-channel tile; no other workspace.
 bool rows_applies(const Shape& s);
-hipError_t rows_main(const Shape& s, const void* x, const void* w, const void* b, void* y, hipStream_t stream);
+size_t rows_packed_bytes(const Shape& s);
+hipError_t rows_pack(const Shape& s, const void* w, void* wp, hipStream_t stream);
+hipError_t rows_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, hipStream_t stream);
 std::string rows_describe(const Shape& s);
 
 // direct convolution (VALU), all N images.

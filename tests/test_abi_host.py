@@ -142,14 +142,16 @@ def test_workspace_sizes():
     pwf = _lib.make_desc(32, 256, 56, 56, 64, 1, 1, 1, 0, 1, 1, "f32")
     assert "pointwise_gemm_kernel<f32,64,0,2>" in _lib.describe(pwf, "implicit_gemm")
     assert "pointwise_dma_kernel<16,4>" in _lib.describe(pw, "implicit_gemm")
-    # The 7x7 stride-2 stem (bf16, 3 channels) takes the filter-row kernel,
-    # which reads the filters as given: its package is a plain copy and it
-    # needs no other workspace.  fp32 and 3x3 layers do not.
+    # The 7x7 stride-2 stem (bf16, 3 channels) takes the filter-row kernel:
+    # its package is the LDS image of each 64-filter tile, 64 x 23 units of
+    # 16 bytes (21 filter rows, rounded up to an odd count); no other
+    # workspace.  fp32 and 3x3 layers do not take it.
     stem = _lib.make_desc(32, 3, 224, 224, 64, 7, 7, 2, 3, 1, 1, "bf16")
-    assert _lib.packed_filter_bytes(stem, "implicit_gemm") == 64 * 3 * 7 * 7 * 2
-    assert _lib.workspace_bytes(stem, "implicit_gemm") == (64 * 3 * 7 * 7 * 2 + 255) // 256 * 256
+    assert _lib.packed_filter_bytes(stem, "implicit_gemm") == 64 * 23 * 16
+    assert _lib.workspace_bytes(stem, "implicit_gemm") == 64 * 23 * 16
     assert _lib.prepacked_workspace_bytes(stem, "implicit_gemm") == 0
-    assert "implicit_rows_kernel" in _lib.describe(stem, "implicit_gemm")
+    assert "rows_pack_kernel;implicit_rows_kernel" in _lib.describe(stem, "implicit_gemm")
+    assert "lead_taps=1" in _lib.describe(stem, "implicit_gemm")
     stem32 = _lib.make_desc(32, 3, 224, 224, 64, 7, 7, 2, 3, 1, 1, "f32")
     assert "implicit_rows_kernel" not in _lib.describe(stem32, "implicit_gemm")
     s3 = _lib.make_desc(32, 3, 224, 224, 64, 3, 3, 2, 1, 1, 1, "bf16")

@@ -302,11 +302,12 @@ def test_pointwise_unaligned_operands(which):
 # the part of it that it covers.
 ROWS = [
     # N, C, H, W, K, R, S, stride, pad, dilation, bias, relu, what
-    (2, 3, 40, 40, 64, 7, 7, 2, 3, 1, True, True, "stem-like 7x7 s2"),
+    (2, 3, 40, 40, 64, 7, 7, 2, 3, 1, True, True, "stem-like 7x7 s2 (16-byte halo loads)"),
     (3, 3, 23, 29, 64, 7, 7, 2, 3, 1, False, False, "odd plane: tiles cross images"),
-    (2, 8, 20, 20, 40, 7, 7, 2, 3, 1, True, False, "C*R = 56 units, K tail"),
-    (2, 5, 19, 17, 130, 5, 5, 2, 2, 1, False, True, "5x5, three K tiles with tail, odd C*R"),
-    (2, 2, 17, 30, 64, 3, 8, 2, 1, 1, True, False, "1x8 taps wide, 3 rows"),
+    (3, 3, 23, 32, 64, 7, 7, 2, 3, 1, True, False, "16-byte halo loads, tiles cross images"),
+    (2, 8, 20, 24, 40, 7, 7, 2, 3, 1, True, False, "C*R = 56 units, K tail"),
+    (2, 5, 19, 17, 130, 5, 5, 2, 2, 1, False, True, "5x5 even pad, three K tiles with tail, odd C*R"),
+    (2, 2, 17, 30, 64, 3, 8, 2, (1, 2), 1, True, False, "3x8 taps, no lead tap"),
     (2, 3, 26, 26, 32, 6, 6, (1, 2), (2, 3), (2, 1), False, False, "row stride 1, row dilation 2"),
     (1, 1, 9, 70, 64, 5, 7, (3, 4), (0, 5), 1, True, True, "one channel, stride 3x4, wide pad"),
 ]
