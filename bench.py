@@ -115,7 +115,11 @@ def make_step(plan, ws, stream_ptr, prepacked=False):
 # Source files of each main kernel (the HBM traffic recorded for a kernel
 # under profiles/ is used only while these files are unchanged).
 KERNEL_SOURCES = {
-    "implicit_gemm_kernel": ("implicit_gemm.hip",),
+    "implicit_gemm_kernel": ("implicit_gemm.hip", "igemm_common.hpp"),
+    "pointwise_": ("implicit_gemm.hip", "igemm_common.hpp"),
+    "repack_plane_kernel": ("implicit_gemm.hip", "igemm_common.hpp"),
+    "splitk_reduce_kernel": ("igemm_common.hpp",),
+    "implicit_rows_kernel": ("implicit_rows.hip", "igemm_common.hpp"),
     "gemm_nt_kernel": ("gemm.hip",),
     "direct_": ("direct.hip",),
     "wino_": ("winograd.hip", "gemm.hip"),
@@ -366,7 +370,7 @@ def main():
     # timed call is exactly one launch of it.
     def main_kernel(desc):
         ks = desc.split("kernels=")[1].split(" ")[0].split(";")
-        return [k for k in ks if not k.startswith("pack_filters") and not k.startswith("wino_filter")]
+        return [k for k in ks if not k.startswith(("pack_filters", "wino_filter", "rows_pack"))]
     share = {}
     for p, ms in zip(plan, lms_pk):
         ks = main_kernel(p["describe"])
