@@ -837,16 +837,46 @@ __global__ __launch_bounds__(256) void repack_plane_kernel(const uint16_t* __res
   const int t = blockIdx.x * 256 + threadIdx.x;
   if (t >= planes * per_plane) return;
   const int plane = t / per_plane, pix0 = (t - plane * per_plane) * 8;
-  const uint16_t* src = x + static_cast<int64_t>(plane) * H * W;
+  const int HW = H * W;
+  const uint16_t* src = x + static_cast<int64_t>(plane) * HW;
+  const int64_t left = static_cast<int64_t>(planes - plane) * HW;  // elements from src to the end of x
   const int PQ = P * Q;
   uint32_t v[8];
-  if (sh == 1 && sw == 1 && ph == 0 && pw == 0) {
+  // 16-byte loads need only 2-byte alignment on gfx950 (the compiler emits
+  // them for any 16-byte copy); a load must not run past the end of x.
+  auto load8 = [&](int64_t off, uint32_t (&e)[8]) {
+    uint4 u;
+    __builtin_memcpy(&u, src + off, 16);
+    e[0] = u.x & 0xFFFFu; e[1] = u.x >> 16; e[2] = u.y & 0xFFFFu; e[3] = u.y >> 16;
+    e[4] = u.z & 0xFFFFu; e[5] = u.z >> 16; e[6] = u.w & 0xFFFFu; e[7] = u.w >> 16;
+  };
+  const int p0 = pix0 / Q, q0 = pix0 - p0 * Q;
+  const int ih0 = p0 * sh - ph, iw0 = q0 * sw - pw;
+  if (sh == 1 && sw == 1 && ph == 0 && pw == 0 && pix0 + 8 <= left) {
     // Unstrided, unpadded: output pixel pix is input pixel pix.
+    load8(pix0, v);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = pix0 + e < PQ ? src[pix0 + e] : 0u;
+    for (int e = 0; e < 8; ++e) v[e] = pix0 + e < PQ ? v[e] : 0u;
+  } else if (sw <= 2 && pix0 + 8 <= PQ && q0 + 8 <= Q && ih0 >= 0 && ih0 < H && iw0 >= 0 &&
+             iw0 + 7 * sw < W && static_cast<int64_t>(ih0) * W + iw0 + 16 <= left) {
+    // Eight outputs of one row with every input inside the image: two
+    // 16-byte loads cover the (at most 15) input elements.
+    uint32_t a[8], b[8];
+    load8(static_cast<int64_t>(ih0) * W + iw0, a);
+    load8(static_cast<int64_t>(ih0) * W + iw0 + 8, b);
+    if (sw == 1) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = a[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[e] = a[2 * e];
+        v[e + 4] = b[2 * e];
+      }
+    }
   } else {
-    // Walk the 8 pixels along the output row (one division for the first).
-    int p = pix0 / Q, q = pix0 - p * Q;
+    // Element by element, walking the 8 pixels along the output row.
+    int p = p0, q = q0;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int ih = p * sh - ph, iw = q * sw - pw;
