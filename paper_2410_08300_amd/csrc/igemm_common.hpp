@@ -61,24 +61,22 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
-// Bias, ReLU and the NCHW store of one BM x BN tile (rows k0.. of group g,
-// pixels j0..), or its raw fp32 partial sums when the channels are split.
-// The accumulators go through LDS (each wave stages its 32 x 64 block; the
-// caller provides 32 KiB) so that a lane then holds a run of 8 consecutive
-// pixels of one output channel: lane l takes pixels (l % 8) * 8 .. +7 of the
-// wave's 64 and rows l / 8 + 8 * it, it = 0..3, of each 32-row block.  Its
-// image, offset and the start of the next image are computed once per tile.
-// A run is stored in pieces of e.vec elements (8, 4, 2 or 1: the largest
-// that divides P*Q and keeps the stores aligned), so no piece crosses an
-// image boundary; a piece past the boundary moves to the next image.
-template <typename T, int BM>
-__device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / 64][BN / 64], vec16* smem, const EpiArgs& e,
-                                           int j0, int k0, int g, int split) {
-  constexpr int MI = BM / 64, NJ = BN / 64;
-  constexpr int EW = BN / 2;  // pixels per wave row
-  static_assert(EW == 64, "staging layout assumes 64 pixels per wave row");
-  const int tid = threadIdx.x, lane = tid & 63, wave = (tid >> 6) & 3;
-  const int wm = wave >> 1, wn = wave & 1;
+// Bias, ReLU and the NCHW store of one wave's MI x NJ blocks of 32 x 32
+// accumulators (NJ even): rows row0 + 32 mi + .. of group g, pixels col0 +
+// 32 nj + .., or their raw fp32 partial sums when the channels are split.
+// The accumulators go through LDS (`stage`: this wave's 8 KiB), 32 rows x 64
+// pixels at a time, so that a lane then holds a run of 8 consecutive pixels
+// of one output channel: lane l takes pixels (l % 8) * 8 .. +7 of the 64 and
+// rows l / 8 + 8 * it, it = 0..3.  A run is stored in pieces of e.vec
+// elements (8, 4, 2 or 1: the largest that divides P*Q and keeps the stores
+// aligned), so no piece crosses an image boundary; a piece past the boundary
+// moves to the next image.
+template <typename T, int MI, int NJ>
+__device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float* stage, const EpiArgs& e, int row0,
+                                            int col0, int g, int split) {
+  static_assert(NJ % 2 == 0, "blocks of 64 pixels");
+  constexpr int EW = 64;  // pixels per staged row
+  const int lane = threadIdx.x & 63;
   const int l32 = lane & 31;
   const int PQ = e.PQ;
   const bool split_out = e.splits > 1;
@@ -86,112 +84,125 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / 64][BN / 6
   const T* bias = reinterpret_cast<const T*>(e.b);
   T* y = reinterpret_cast<T*>(e.y);
 
-  // Each wave stages 32 rows x 64 pixels of fp32 (8 KiB).  Rows are
-  // unpadded; float4 f of row r sits at f ^ g(r), g(r) = (r & 1) | 8 *
-  // ((r >> 2) & 1): the two half-waves of a store (rows r and r+4) and the
-  // quarter-waves of a load (rows 2q, 2q+1) then touch distinct banks.
-  float* stage = reinterpret_cast<float*>(smem) + wave * 32 * EW;
+  // Rows are unpadded; float4 f of row r sits at f ^ g(r), g(r) = (r & 1) |
+  // 8 * ((r >> 2) & 1): the two half-waves of a store (rows r and r+4) and
+  // the quarter-waves of a load (rows 2q, 2q+1) then touch distinct banks.
   auto spos = [](int r, int px) { return r * EW + ((((px >> 2) ^ (r & 1) ^ (((r >> 2) & 1) << 3))) << 2) + (px & 3); };
-
   const int cb = (lane & 7) * 8;
-  const int j = j0 + wn * EW + cb;
-  // Pixel j of the tile index space is pixel pq of image n.  With a padded
-  // plane (span > P*Q, a multiple of 8) a run never crosses an image and its
-  // pixels past P*Q are padding; otherwise a run may cross into the next
-  // image after `wrap` pixels.
   const int span = e.span;
-  const int n = j / span, pq = j - n * span;
-  const int nvalid = j >= e.NPQ ? 0 : span == PQ ? min(8, e.NPQ - j) : min(8, PQ - pq);  // <= 0: none
-  const int wrap = span == PQ ? PQ - pq : 8;
   const int64_t next_img = static_cast<int64_t>(e.K - 1) * PQ;
-  const int i0 = k0 + wm * (BM / 2) + (lane >> 3);
-  const int64_t obase = (static_cast<int64_t>(n) * e.K + g * e.Kg + i0) * PQ + pq;
+  const int i0 = row0 + (lane >> 3);
 
 #pragma unroll
-  for (int mi = 0; mi < MI; ++mi) {
+  for (int h = 0; h < NJ / 2; ++h) {
+    // Pixel j of the tile index space is pixel pq of image n.  With a padded
+    // plane (span > P*Q, a multiple of 8) a run never crosses an image and
+    // its pixels past P*Q are padding; otherwise a run may cross into the
+    // next image after `wrap` pixels.
+    const int j = col0 + h * EW + cb;
+    const int n = j / span, pq = j - n * span;
+    const int nvalid = j >= e.NPQ ? 0 : span == PQ ? min(8, e.NPQ - j) : min(8, PQ - pq);  // <= 0: none
+    const int wrap = span == PQ ? PQ - pq : 8;
+    const int64_t obase = (static_cast<int64_t>(n) * e.K + g * e.Kg + i0) * PQ + pq;
 #pragma unroll
-    for (int nj = 0; nj < NJ; ++nj)
+    for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) stage[spos(mfma_row(v, lane), nj * 32 + l32)] = acc[mi][nj][v];
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
-    __builtin_amdgcn_wave_barrier();
-    // All four runs of this block are read from LDS before any is stored,
-    // so the reads overlap instead of each waiting on the previous store.
-    float4 lo[4], hi[4];
+      for (int q = 0; q < 2; ++q)
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      const int row = (lane >> 3) + 8 * it;
-      lo[it] = *reinterpret_cast<const float4*>(stage + spos(row, cb));
-      hi[it] = *reinterpret_cast<const float4*>(stage + spos(row, cb + 4));
+        for (int v = 0; v < 16; ++v) stage[spos(mfma_row(v, lane), q * 32 + l32)] = acc[mi][2 * h + q][v];
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+      __builtin_amdgcn_wave_barrier();
+      // All four runs of this block are read from LDS before any is stored,
+      // so the reads overlap instead of each waiting on the previous store.
+      float4 lo[4], hi[4];
+#pragma unroll
+      for (int it = 0; it < 4; ++it) {
+        const int row = (lane >> 3) + 8 * it;
+        lo[it] = *reinterpret_cast<const float4*>(stage + spos(row, cb));
+        hi[it] = *reinterpret_cast<const float4*>(stage + spos(row, cb + 4));
+      }
+#pragma unroll
+      for (int it = 0; it < 4; ++it) {
+        const int i = i0 + mi * 32 + 8 * it;
+        if (i >= e.Kg || nvalid <= 0) continue;
+        const int64_t o = obase + static_cast<int64_t>(mi * 32 + 8 * it) * PQ;
+        float vals[8] = {lo[it].x, lo[it].y, lo[it].z, lo[it].w, hi[it].x, hi[it].y, hi[it].z, hi[it].w};
+        // Pieces past `wrap` belong to the next image.
+        auto at = [&](int t) { return o + t + (t >= wrap ? next_img : 0); };
+        if (split_out) {
+          if (e.vec == 8 && nvalid == 8) {
+            *reinterpret_cast<float4*>(part + o) = lo[it];
+            *reinterpret_cast<float4*>(part + o + 4) = hi[it];
+          } else if (e.vec >= 4) {
+#pragma unroll
+            for (int t = 0; t < 8; t += 4)
+              if (t < nvalid)
+                *reinterpret_cast<float4*>(part + at(t)) = make_float4(vals[t], vals[t + 1], vals[t + 2], vals[t + 3]);
+          } else {
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+              if (t < nvalid) part[at(t)] = vals[t];
+          }
+          continue;
+        }
+        const float bv = bias ? elem<T>::load(bias + g * e.Kg + i) : 0.f;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          vals[t] += bv;
+          if (e.relu) vals[t] = fmaxf(vals[t], 0.f);
+        }
+        if constexpr (sizeof(T) == 2) {
+          uint32_t w[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) w[q] = f32x2_to_bf16x2(vals[2 * q], vals[2 * q + 1]);
+          if (e.vec == 8 && nvalid == 8) {
+            *reinterpret_cast<uint4*>(y + o) = make_uint4(w[0], w[1], w[2], w[3]);
+          } else if (e.vec >= 4) {
+#pragma unroll
+            for (int t = 0; t < 8; t += 4)
+              if (t < nvalid) *reinterpret_cast<uint2*>(y + at(t)) = make_uint2(w[t / 2], w[t / 2 + 1]);
+          } else if (e.vec == 2) {
+#pragma unroll
+            for (int t = 0; t < 8; t += 2)
+              if (t < nvalid) *reinterpret_cast<uint32_t*>(y + at(t)) = w[t / 2];
+          } else {
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+              if (t < nvalid) elem<T>::store(y + at(t), vals[t]);
+          }
+        } else {
+          float* yf = reinterpret_cast<float*>(y);
+          if (e.vec == 8 && nvalid == 8) {
+            *reinterpret_cast<float4*>(yf + o) = make_float4(vals[0], vals[1], vals[2], vals[3]);
+            *reinterpret_cast<float4*>(yf + o + 4) = make_float4(vals[4], vals[5], vals[6], vals[7]);
+          } else if (e.vec >= 4) {
+#pragma unroll
+            for (int t = 0; t < 8; t += 4)
+              if (t < nvalid)
+                *reinterpret_cast<float4*>(yf + at(t)) = make_float4(vals[t], vals[t + 1], vals[t + 2], vals[t + 3]);
+          } else {
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+              if (t < nvalid) yf[at(t)] = vals[t];
+          }
+        }
+      }
+      __builtin_amdgcn_wave_barrier();  // the next block reuses this wave's stage
     }
-#pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      const int i = i0 + mi * 32 + 8 * it;
-      if (i >= e.Kg || nvalid <= 0) continue;
-      const int64_t o = obase + static_cast<int64_t>(mi * 32 + 8 * it) * PQ;
-      float vals[8] = {lo[it].x, lo[it].y, lo[it].z, lo[it].w, hi[it].x, hi[it].y, hi[it].z, hi[it].w};
-      // Pieces past `wrap` belong to the next image.
-      auto at = [&](int t) { return o + t + (t >= wrap ? next_img : 0); };
-      if (split_out) {
-        if (e.vec == 8 && nvalid == 8) {
-          *reinterpret_cast<float4*>(part + o) = lo[it];
-          *reinterpret_cast<float4*>(part + o + 4) = hi[it];
-        } else if (e.vec >= 4) {
-#pragma unroll
-          for (int t = 0; t < 8; t += 4)
-            if (t < nvalid)
-              *reinterpret_cast<float4*>(part + at(t)) = make_float4(vals[t], vals[t + 1], vals[t + 2], vals[t + 3]);
-        } else {
-#pragma unroll
-          for (int t = 0; t < 8; ++t)
-            if (t < nvalid) part[at(t)] = vals[t];
-        }
-        continue;
-      }
-      const float bv = bias ? elem<T>::load(bias + g * e.Kg + i) : 0.f;
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        vals[t] += bv;
-        if (e.relu) vals[t] = fmaxf(vals[t], 0.f);
-      }
-      if constexpr (sizeof(T) == 2) {
-        uint32_t w[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) w[q] = f32x2_to_bf16x2(vals[2 * q], vals[2 * q + 1]);
-        if (e.vec == 8 && nvalid == 8) {
-          *reinterpret_cast<uint4*>(y + o) = make_uint4(w[0], w[1], w[2], w[3]);
-        } else if (e.vec >= 4) {
-#pragma unroll
-          for (int t = 0; t < 8; t += 4)
-            if (t < nvalid) *reinterpret_cast<uint2*>(y + at(t)) = make_uint2(w[t / 2], w[t / 2 + 1]);
-        } else if (e.vec == 2) {
-#pragma unroll
-          for (int t = 0; t < 8; t += 2)
-            if (t < nvalid) *reinterpret_cast<uint32_t*>(y + at(t)) = w[t / 2];
-        } else {
-#pragma unroll
-          for (int t = 0; t < 8; ++t)
-            if (t < nvalid) elem<T>::store(y + at(t), vals[t]);
-        }
-      } else {
-        float* yf = reinterpret_cast<float*>(y);
-        if (e.vec == 8 && nvalid == 8) {
-          *reinterpret_cast<float4*>(yf + o) = make_float4(vals[0], vals[1], vals[2], vals[3]);
-          *reinterpret_cast<float4*>(yf + o + 4) = make_float4(vals[4], vals[5], vals[6], vals[7]);
-        } else if (e.vec >= 4) {
-#pragma unroll
-          for (int t = 0; t < 8; t += 4)
-            if (t < nvalid)
-              *reinterpret_cast<float4*>(yf + at(t)) = make_float4(vals[t], vals[t + 1], vals[t + 2], vals[t + 3]);
-        } else {
-#pragma unroll
-          for (int t = 0; t < 8; ++t)
-            if (t < nvalid) yf[at(t)] = vals[t];
-        }
-      }
-    }
-    __builtin_amdgcn_wave_barrier();  // the next block reuses this wave's stage
   }
+}
+
+// The epilogue of one BM x BN tile (rows k0.. of group g, pixels j0..)
+// computed by four waves in a 2 x 2 layout, each holding (BM/2) x 64; the
+// caller provides 32 KiB of LDS (8 KiB per wave).
+template <typename T, int BM>
+__device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / 64][BN / 64], vec16* smem, const EpiArgs& e,
+                                           int j0, int k0, int g, int split) {
+  static_assert(BN / 2 == 64, "staging layout assumes 64 pixels per wave row");
+  const int wave = (threadIdx.x >> 6) & 3;
+  const int wm = wave >> 1, wn = wave & 1;
+  float* stage = reinterpret_cast<float*>(smem) + wave * 32 * 64;
+  store_block<T, BM / 64, BN / 64>(acc, stage, e, k0 + wm * (BM / 2), j0 + wn * (BN / 2), g, split);
 }
 
 // s_waitcnt with vmcnt = n and the other counters at their maximum (gfx9 encoding).

@@ -1323,7 +1323,7 @@ std::string describe_typed(const Shape& s) {
 }  // namespace
 
 bool implicit_gemm_fits(const Shape& s) {
-  if (use_pointwise(s) || rows_applies(s)) return true;
+  if (use_pointwise(s) || rows_applies(s) || ws_applies(s)) return true;
   IgPlan pl;
   if (s.dtype == DT_F32) return make_plan<float>(s, pl);
   return make_plan<bf16_t>(s, pl);
@@ -1332,6 +1332,7 @@ bool implicit_gemm_fits(const Shape& s) {
 size_t implicit_gemm_packed_bytes(const Shape& s) {
   if (use_pointwise(s)) return (size_t)(s.K * s.C * s.esize());  // a plain copy of the filters
   if (rows_applies(s)) return rows_packed_bytes(s);
+  if (ws_applies(s)) return ws_packed_bytes(s);
   IgPlan pl;
   const bool ok = s.dtype == DT_F32 ? make_plan<float>(s, pl) : make_plan<bf16_t>(s, pl);
   return ok ? pl.wp_bytes : 0;
@@ -1339,6 +1340,7 @@ size_t implicit_gemm_packed_bytes(const Shape& s) {
 
 size_t implicit_gemm_split_bytes(const Shape& s) {
   if (rows_applies(s)) return 0;
+  if (ws_applies(s)) return ws_split_bytes(s);
   if (use_pointwise(s)) return s.dtype == DT_F32 ? pw_split_bytes<float>(s) : pw_split_bytes<bf16_t>(s);
   return s.dtype == DT_F32 ? split_bytes_typed<float>(s) : split_bytes_typed<bf16_t>(s);
 }
@@ -1349,6 +1351,7 @@ size_t implicit_gemm_workspace(const Shape& s) {
 
 hipError_t launch_implicit_pack(const Shape& s, const void* w, void* wp, hipStream_t stream) {
   if (rows_applies(s)) return rows_pack(s, w, wp, stream);
+  if (ws_applies(s)) return ws_pack(s, w, wp, stream);
   if (use_pointwise(s)) return launch_copy(w, wp, implicit_gemm_packed_bytes(s), stream);
   return s.dtype == DT_F32 ? pack_typed<float>(s, w, wp, stream) : pack_typed<bf16_t>(s, w, wp, stream);
 }
@@ -1356,6 +1359,7 @@ hipError_t launch_implicit_pack(const Shape& s, const void* w, void* wp, hipStre
 hipError_t launch_implicit_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* part,
                                 hipStream_t stream) {
   if (rows_applies(s)) return rows_main(s, x, wp, b, y, stream);
+  if (ws_applies(s)) return ws_main(s, x, wp, b, y, part, stream);
   if (use_pointwise(s))
     return s.dtype == DT_F32 ? pw_main_typed<float>(s, x, wp, b, y, part, stream)
                              : pw_main_typed<bf16_t>(s, x, wp, b, y, part, stream);
@@ -1378,6 +1382,7 @@ hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, co
 
 std::string implicit_gemm_describe(const Shape& s) {
   if (rows_applies(s)) return rows_describe(s);
+  if (ws_applies(s)) return ws_describe(s);
   if (use_pointwise(s)) return s.dtype == DT_F32 ? pw_describe<float>(s) : pw_describe<bf16_t>(s);
   return s.dtype == DT_F32 ? describe_typed<float>(s) : describe_typed<bf16_t>(s);
 }

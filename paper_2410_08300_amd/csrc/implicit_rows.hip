@@ -14,6 +14,8 @@
 // image of a 64-channel tile ([k][(c, r)][8 taps], odd row stride in 16-byte
 // units), which each workgroup copies with 16-byte loads.
 #include <stdio.h>
+
+#include <atomic>
 #include <string>
 
 #include "common.hpp"
@@ -295,6 +297,17 @@ hipError_t rows_main(const Shape& s, const void* x, const void* wp, const void* 
     a.e.b = b;
     a.e.vec = store_piece(s, a.e.y);
     const dim3 grid((unsigned)((a.NPQ + BN - 1) / BN), (unsigned)cur.ktiles);
+    // Raise the kernels' dynamic-LDS limit once (calls may be captured into
+    // a graph after the first one).
+    static std::atomic<int> lds_limit{64 * 1024};
+    if ((int)cur.lds > lds_limit.load()) {
+      for (const void* k : {reinterpret_cast<const void*>(implicit_rows_kernel<true>),
+                            reinterpret_cast<const void*>(implicit_rows_kernel<false>)}) {
+        const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsLimit);
+        if (e != hipSuccess) return e;
+      }
+      lds_limit.store((int)kLdsLimit);
+    }
     if (vec)
       hipLaunchKernelGGL(implicit_rows_kernel<true>, grid, dim3(kThreads), cur.lds, stream, a);
     else

@@ -57,6 +57,17 @@ hipError_t rows_pack(const Shape& s, const void* w, void* wp, hipStream_t stream
 hipError_t rows_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, hipStream_t stream);
 std::string rows_describe(const Shape& s);
 
+// Implicit GEMM with loader and compute waves (bf16, one group, nine taps,
+// C > 8): its own filter package ([16-channel chunk][K padded][19 units]),
+// plus split-K partials.
+bool ws_applies(const Shape& s);
+size_t ws_packed_bytes(const Shape& s);
+size_t ws_split_bytes(const Shape& s);
+hipError_t ws_pack(const Shape& s, const void* w, void* wp, hipStream_t stream);
+hipError_t ws_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* part_ws,
+                   hipStream_t stream);
+std::string ws_describe(const Shape& s);
+
 // direct convolution (VALU), all N images.
 hipError_t launch_direct(const Shape& s, const void* x, const void* w, const void* b, void* y,
                          hipStream_t stream);

@@ -114,17 +114,25 @@ def test_workspace_sizes():
     per_img = 112 * 112 * 512 * 9 * 2
     assert _lib.workspace_bytes(big, "im2col_gemm") == (1 << 30) // per_img * per_img
     assert _lib.workspace_bytes(_lib.make_desc(0, 4, 8, 8, 4, 3, 3), "im2col_gemm") == 0
-    # implicit GEMM: the filters repacked as [chunk][K padded to the tile]
-    # [tap][16-byte units], plus fp32 split partial sums for small grids.
-    # 64 -> 64 channels, 56x56, batch 32: 784 tiles of 64 x 128, no split;
-    # 4 chunks of 16 channels x 64 filters x 9 taps x 2 units x 16 bytes.
+    # implicit GEMM, bf16 3x3: the loader/compute-wave kernel's package is
+    # [16-channel chunk][K padded to the tile][19 units of 8 channels] (9
+    # taps x 2 channel groups + a zero unit), plus fp32 split partial sums
+    # for small grids.
+    # 64 -> 64 channels, 56x56, batch 32: 784 tiles of 64 x 128, no split.
     large = _lib.make_desc(32, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, "bf16")
-    assert _lib.workspace_bytes(large, "implicit_gemm") == 4 * 64 * 18 * 16
+    assert _lib.workspace_bytes(large, "implicit_gemm") == 4 * 64 * 19 * 16
+    assert "implicit_ws_kernel<64,1>" in _lib.describe(large, "implicit_gemm")
     # 512 -> 512 channels, 7x7, batch 32: 13 x 4 tiles of 128 x 128 leave
-    # most of 256 CUs idle, so the 32 chunks are split four ways.
+    # most of 256 CUs idle, so the 32 chunks are split four ways; the odd
+    # plane width takes the pixel-by-pixel halo loads.
     small = _lib.make_desc(32, 512, 7, 7, 512, 3, 3, 1, 1, 1, 1, "bf16")
-    packed = 32 * 512 * 18 * 16
+    packed = 32 * 512 * 19 * 16
     assert _lib.workspace_bytes(small, "implicit_gemm") == packed + 4 * 32 * 512 * 49 * 4
+    assert "implicit_ws_kernel<128,0>;splitk_reduce_kernel" in _lib.describe(small, "implicit_gemm")
+    # fp32 3x3 keeps the general kernel: [chunk][K padded][tap][units].
+    f32 = _lib.make_desc(32, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, "f32")
+    assert _lib.workspace_bytes(f32, "implicit_gemm") == 8 * 64 * 18 * 16
+    assert "implicit_gemm_kernel<f32,64,2,9>" in _lib.describe(f32, "implicit_gemm")
     # 1x1 layers: the package is a plain copy of the K x C filters.
     # 256 -> 64 channels, 56x56, batch 32: 784 pixel tiles, no split.
     pw = _lib.make_desc(32, 256, 56, 56, 64, 1, 1, 1, 0, 1, 1, "bf16")
