@@ -67,123 +67,126 @@ __device__ __forceinline__ void static_for(F&& f) {
 // The accumulators go through LDS (`stage`: this wave's 8 KiB), 32 rows x 64
 // pixels at a time, so that a lane then holds a run of 8 consecutive pixels
 // of one output channel: lane l takes pixels (l % 8) * 8 .. +7 of the 64 and
-// rows l / 8 + 8 * it, it = 0..3.  A run is stored in pieces of e.vec
-// elements (8, 4, 2 or 1: the largest that divides P*Q and keeps the stores
-// aligned), so no piece crosses an image boundary; a piece past the boundary
-// moves to the next image.
+// rows l / 8 + 8 * it, it = 0..3.  A run inside one image leaves as one
+// 16-byte store (2-byte alignment is enough on gfx950; the compiler emits
+// these for any 16-byte copy); a run that crosses an image boundary or ends
+// at the last pixel is stored element by element.  Bias values are loaded
+// before any store: loads and stores share one counter, so a load issued
+// after stores would wait for all of them.
 template <typename T, int MI, int NJ>
 __device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float* stage, const EpiArgs& e, int row0,
                                             int col0, int g, int split) {
   static_assert(NJ % 2 == 0, "blocks of 64 pixels");
   constexpr int EW = 64;  // pixels per staged row
   const int lane = threadIdx.x & 63;
-  const int l32 = lane & 31;
-  const int PQ = e.PQ;
+  const int l32 = lane & 31, h = lane >> 5;
+  const int PQ = e.PQ, span = e.span;
   const bool split_out = e.splits > 1;
-  float* part = split_out ? e.partial + static_cast<int64_t>(split) * e.slab : nullptr;
   const T* bias = reinterpret_cast<const T*>(e.b);
-  T* y = reinterpret_cast<T*>(e.y);
 
-  // Rows are unpadded; float4 f of row r sits at f ^ g(r), g(r) = (r & 1) |
-  // 8 * ((r >> 2) & 1): the two half-waves of a store (rows r and r+4) and
-  // the quarter-waves of a load (rows 2q, 2q+1) then touch distinct banks.
-  auto spos = [](int r, int px) { return r * EW + ((((px >> 2) ^ (r & 1) ^ (((r >> 2) & 1) << 3))) << 2) + (px & 3); };
-  const int cb = (lane & 7) * 8;
-  const int span = e.span;
-  const int64_t next_img = static_cast<int64_t>(e.K - 1) * PQ;
-  const int i0 = row0 + (lane >> 3);
+  // Staging layout: float4 f of row r sits at f ^ ((r & 1) | 8 ((r >> 2) & 1)),
+  // so the writes of two half-waves (rows r and r+4) and the reads of four
+  // quarter-waves (rows 2q, 2q+1) touch distinct banks.  For the row of
+  // accumulator v of this lane (8 (v/4) + 4 h + v % 4) the XOR term is
+  // (v & 1) | 8 h, so the write address is a per-lane base (one per parity
+  // of v and per 32-pixel half) plus a constant.
+  int wbase[2][2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int par = 0; par < 2; ++par) {
+      const int px = q * 32 + l32;
+      wbase[q][par] = 4 * h * EW + ((((px >> 2) ^ par ^ (h << 3))) << 2) + (px & 3);
+    }
+  const int rrow = lane >> 3, cb = (lane & 7) * 8;
+  const int rsw = (rrow & 1) | (((rrow >> 2) & 1) << 3);
+  const int rbase_lo = rrow * EW + (((cb >> 2) ^ rsw) << 2);
+  const int rbase_hi = rrow * EW + ((((cb + 4) >> 2) ^ rsw) << 2);
+
+  float bv[MI][4];
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int i = row0 + mi * 32 + rrow + 8 * it;
+      bv[mi][it] = (!split_out && bias && i < e.Kg) ? elem<T>::load(bias + g * e.Kg + i) : 0.f;
+    }
 
 #pragma unroll
-  for (int h = 0; h < NJ / 2; ++h) {
-    // Pixel j of the tile index space is pixel pq of image n.  With a padded
-    // plane (span > P*Q, a multiple of 8) a run never crosses an image and
-    // its pixels past P*Q are padding; otherwise a run may cross into the
-    // next image after `wrap` pixels.
-    const int j = col0 + h * EW + cb;
+  for (int hb = 0; hb < NJ / 2; ++hb) {
+    // Pixel j of the tile index space is pixel pq of image n; with a padded
+    // plane (span > P*Q) the pixels past P*Q are padding.
+    const int j = col0 + hb * EW + cb;
     const int n = j / span, pq = j - n * span;
-    const int nvalid = j >= e.NPQ ? 0 : span == PQ ? min(8, e.NPQ - j) : min(8, PQ - pq);  // <= 0: none
-    const int wrap = span == PQ ? PQ - pq : 8;
-    const int64_t obase = (static_cast<int64_t>(n) * e.K + g * e.Kg + i0) * PQ + pq;
+    // Pixels of this run's image from j on (<= 0: none; j >= NPQ lies past the last image).
+    const int last = j >= e.NPQ ? 0 : span == PQ ? e.NPQ - j : PQ - pq;
+    const int wrap = span == PQ ? PQ - pq : 8;           // a run crosses into the next image after `wrap` pixels
+    const bool full = last >= 8 && wrap >= 8;
+    const int nvalid = last < 8 ? last : 8;
+    const int64_t next_img = static_cast<int64_t>(e.K - 1) * PQ;
+    const int64_t obase = (static_cast<int64_t>(n) * e.K + g * e.Kg + row0 + rrow) * PQ + pq;
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
       for (int q = 0; q < 2; ++q)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) stage[spos(mfma_row(v, lane), q * 32 + l32)] = acc[mi][2 * h + q][v];
+        for (int v = 0; v < 16; ++v)
+          stage[wbase[q][v & 1] + (8 * (v >> 2) + (v & 3)) * EW] = acc[mi][2 * hb + q][v];
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
       __builtin_amdgcn_wave_barrier();
-      // All four runs of this block are read from LDS before any is stored,
-      // so the reads overlap instead of each waiting on the previous store.
       float4 lo[4], hi[4];
 #pragma unroll
       for (int it = 0; it < 4; ++it) {
-        const int row = (lane >> 3) + 8 * it;
-        lo[it] = *reinterpret_cast<const float4*>(stage + spos(row, cb));
-        hi[it] = *reinterpret_cast<const float4*>(stage + spos(row, cb + 4));
+        lo[it] = *reinterpret_cast<const float4*>(stage + rbase_lo + it * 8 * EW);
+        hi[it] = *reinterpret_cast<const float4*>(stage + rbase_hi + it * 8 * EW);
       }
 #pragma unroll
       for (int it = 0; it < 4; ++it) {
-        const int i = i0 + mi * 32 + 8 * it;
+        const int i = row0 + mi * 32 + rrow + 8 * it;
         if (i >= e.Kg || nvalid <= 0) continue;
         const int64_t o = obase + static_cast<int64_t>(mi * 32 + 8 * it) * PQ;
         float vals[8] = {lo[it].x, lo[it].y, lo[it].z, lo[it].w, hi[it].x, hi[it].y, hi[it].z, hi[it].w};
-        // Pieces past `wrap` belong to the next image.
-        auto at = [&](int t) { return o + t + (t >= wrap ? next_img : 0); };
         if (split_out) {
-          if (e.vec == 8 && nvalid == 8) {
-            *reinterpret_cast<float4*>(part + o) = lo[it];
-            *reinterpret_cast<float4*>(part + o + 4) = hi[it];
-          } else if (e.vec >= 4) {
-#pragma unroll
-            for (int t = 0; t < 8; t += 4)
-              if (t < nvalid)
-                *reinterpret_cast<float4*>(part + at(t)) = make_float4(vals[t], vals[t + 1], vals[t + 2], vals[t + 3]);
+          float* part = e.partial + static_cast<int64_t>(split) * e.slab;
+          if (full) {
+            __builtin_memcpy(part + o, &lo[it], 16);
+            __builtin_memcpy(part + o + 4, &hi[it], 16);
           } else {
 #pragma unroll
             for (int t = 0; t < 8; ++t)
-              if (t < nvalid) part[at(t)] = vals[t];
+              if (t < nvalid) part[o + t + (t >= wrap ? next_img : 0)] = vals[t];
           }
           continue;
         }
-        const float bv = bias ? elem<T>::load(bias + g * e.Kg + i) : 0.f;
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
-          vals[t] += bv;
+          vals[t] += bv[mi][it];
           if (e.relu) vals[t] = fmaxf(vals[t], 0.f);
         }
+        T* y = reinterpret_cast<T*>(e.y);
         if constexpr (sizeof(T) == 2) {
-          uint32_t w[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) w[q] = f32x2_to_bf16x2(vals[2 * q], vals[2 * q + 1]);
-          if (e.vec == 8 && nvalid == 8) {
-            *reinterpret_cast<uint4*>(y + o) = make_uint4(w[0], w[1], w[2], w[3]);
-          } else if (e.vec >= 4) {
-#pragma unroll
-            for (int t = 0; t < 8; t += 4)
-              if (t < nvalid) *reinterpret_cast<uint2*>(y + at(t)) = make_uint2(w[t / 2], w[t / 2 + 1]);
-          } else if (e.vec == 2) {
-#pragma unroll
-            for (int t = 0; t < 8; t += 2)
-              if (t < nvalid) *reinterpret_cast<uint32_t*>(y + at(t)) = w[t / 2];
+          if (full) {
+            uint4 w;
+            w.x = f32x2_to_bf16x2(vals[0], vals[1]);
+            w.y = f32x2_to_bf16x2(vals[2], vals[3]);
+            w.z = f32x2_to_bf16x2(vals[4], vals[5]);
+            w.w = f32x2_to_bf16x2(vals[6], vals[7]);
+            __builtin_memcpy(y + o, &w, 16);
           } else {
 #pragma unroll
             for (int t = 0; t < 8; ++t)
-              if (t < nvalid) elem<T>::store(y + at(t), vals[t]);
+              if (t < nvalid) elem<T>::store(y + o + t + (t >= wrap ? next_img : 0), vals[t]);
           }
         } else {
-          float* yf = reinterpret_cast<float*>(y);
-          if (e.vec == 8 && nvalid == 8) {
-            *reinterpret_cast<float4*>(yf + o) = make_float4(vals[0], vals[1], vals[2], vals[3]);
-            *reinterpret_cast<float4*>(yf + o + 4) = make_float4(vals[4], vals[5], vals[6], vals[7]);
-          } else if (e.vec >= 4) {
-#pragma unroll
-            for (int t = 0; t < 8; t += 4)
-              if (t < nvalid)
-                *reinterpret_cast<float4*>(yf + at(t)) = make_float4(vals[t], vals[t + 1], vals[t + 2], vals[t + 3]);
+          if (full) {
+            const float4 a = make_float4(vals[0], vals[1], vals[2], vals[3]);
+            const float4 b = make_float4(vals[4], vals[5], vals[6], vals[7]);
+            __builtin_memcpy(y + o, &a, 16);
+            __builtin_memcpy(y + o + 4, &b, 16);
           } else {
 #pragma unroll
             for (int t = 0; t < 8; ++t)
-              if (t < nvalid) yf[at(t)] = vals[t];
+              if (t < nvalid) elem<T>::store(y + o + t + (t >= wrap ? next_img : 0), vals[t]);
           }
         }
       }
