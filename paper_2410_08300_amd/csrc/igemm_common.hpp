@@ -195,6 +195,144 @@ __device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float
   }
 }
 
+// Epilogue of a wave that holds 32 output channels x 128 pixels as four
+// transposed 32 x 32 blocks (the MFMA computed pixels x channels: block nj,
+// accumulator v of lane l is channel l % 32, pixel nj*32 + 8 (v/4) +
+// 4 (l/32) + v % 4, so a lane holds runs of 4 consecutive pixels of one
+// channel).  Bias, ReLU and the rounding to T happen in registers; the block
+// is staged once in LDS (`stage`: 8 KiB, [channel][128 pixels] in 16-byte
+// units XOR-swizzled by the channel) and leaves as whole 256-byte channel
+// rows, four per store instruction, the pattern that reaches the HBM write
+// rate.  A run of 8 pixels inside one image is one 16-byte store (2-byte
+// alignment is enough on gfx950); a run that crosses an image boundary or
+// passes the last pixel is stored element by element.  Split-K partials
+// (fp32) are staged in two halves of 64 pixels.
+template <typename T>
+__device__ __forceinline__ void store_block128t(const f32x16_t (&acc)[1][4], float* stage_f, const EpiArgs& e,
+                                                int row0, int col0, int g, int split) {
+  const int lane = threadIdx.x & 63;
+  const int l32 = lane & 31, h = lane >> 5;
+  const int PQ = e.PQ, span = e.span;
+  char* stage = reinterpret_cast<char*>(stage_f);
+  const int64_t next_img = static_cast<int64_t>(e.K - 1) * PQ;
+  // A run of 8 pixels starting at tile pixel `px` of output channel
+  // `i = row0 + ch`: where it goes and whether it is whole.
+  struct Run {
+    int64_t o;
+    int nvalid, wrap;
+    bool full;
+  };
+  auto run_at = [&](int px) {
+    Run r;
+    const int j = col0 + px;
+    const int n = j / span, pq = j - n * span;
+    const int last = j >= e.NPQ ? 0 : span == PQ ? e.NPQ - j : PQ - pq;
+    r.wrap = span == PQ ? PQ - pq : 8;
+    r.full = last >= 8 && r.wrap >= 8;
+    r.nvalid = last < 8 ? last : 8;
+    r.o = (static_cast<int64_t>(n) * e.K + g * e.Kg + row0) * PQ + pq;
+    return r;
+  };
+
+  if (e.splits <= 1) {
+    const T* bias = reinterpret_cast<const T*>(e.b);
+    const int i_own = row0 + l32;
+    const float bv = (bias && i_own < e.Kg) ? elem<T>::load(bias + g * e.Kg + i_own) : 0.f;
+    // Channel l32, pixels px0 .. px0 + 3 (8 bytes of T = bf16; fp32 goes
+    // through the partial path's layout below).
+    static_assert(sizeof(T) == 2, "bf16 output");
+#pragma unroll
+    for (int nj = 0; nj < 4; ++nj)
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg) {
+        float v4[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          v4[k] = acc[0][nj][4 * gg + k] + bv;
+          if (e.relu) v4[k] = fmaxf(v4[k], 0.f);
+        }
+        uint2 w;
+        w.x = f32x2_to_bf16x2(v4[0], v4[1]);
+        w.y = f32x2_to_bf16x2(v4[2], v4[3]);
+        const int px0 = nj * 32 + 8 * gg + 4 * h;
+        *reinterpret_cast<uint2*>(stage + l32 * 256 + ((((px0 >> 3) ^ (l32 & 15))) << 4) + ((px0 >> 2) & 1) * 8) = w;
+      }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+    __builtin_amdgcn_wave_barrier();
+    // Lane l: channel rows l/16 + 4 it (it = 0..7), 16-byte unit l % 16.
+    const int rrow = lane >> 4, u = lane & 15;
+    const Run r = run_at(u * 8);
+    uint4 d[8];
+#pragma unroll
+    for (int it = 0; it < 8; ++it) {
+      const int row = rrow + 4 * it;
+      d[it] = *reinterpret_cast<const uint4*>(stage + row * 256 + ((u ^ (row & 15)) << 4));
+    }
+    T* y = reinterpret_cast<T*>(e.y);
+#pragma unroll
+    for (int it = 0; it < 8; ++it) {
+      const int row = rrow + 4 * it;
+      if (row0 + row >= e.Kg || r.nvalid <= 0) continue;
+      const int64_t o = r.o + static_cast<int64_t>(row) * PQ;
+      if (r.full) {
+        __builtin_memcpy(y + o, &d[it], 16);
+      } else {
+        const uint32_t wd[4] = {d[it].x, d[it].y, d[it].z, d[it].w};
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+          if (t < r.nvalid) reinterpret_cast<uint16_t*>(y)[o + t + (t >= r.wrap ? next_img : 0)] =
+              static_cast<uint16_t>(wd[t >> 1] >> (16 * (t & 1)));
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    return;
+  }
+
+  // fp32 partial sums: two passes of 32 channels x 64 pixels (256 bytes per
+  // channel row, 16-byte units swizzled by the channel).
+  float* part = e.partial + static_cast<int64_t>(split) * e.slab;
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg) {
+        const int px0 = q * 32 + 8 * gg + 4 * h;  // within the 64-pixel half
+        const float4 v = make_float4(acc[0][2 * pass + q][4 * gg], acc[0][2 * pass + q][4 * gg + 1],
+                                     acc[0][2 * pass + q][4 * gg + 2], acc[0][2 * pass + q][4 * gg + 3]);
+        *reinterpret_cast<float4*>(stage + l32 * 256 + (((px0 >> 2) ^ (l32 & 15)) << 4)) = v;
+      }
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_wave_barrier();
+    // Lane l: channel rows l/8 + 8 it (it = 0..3), pixels 8 (l % 8) .. +7 of the half.
+    const int rrow = lane >> 3, c = lane & 7;
+    const Run r = run_at(pass * 64 + c * 8);
+    float4 lo[4], hi[4];
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int row = rrow + 8 * it;
+      lo[it] = *reinterpret_cast<const float4*>(stage + row * 256 + (((2 * c) ^ (row & 15)) << 4));
+      hi[it] = *reinterpret_cast<const float4*>(stage + row * 256 + (((2 * c + 1) ^ (row & 15)) << 4));
+    }
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int row = rrow + 8 * it;
+      if (row0 + row >= e.Kg || r.nvalid <= 0) continue;
+      const int64_t o = r.o + static_cast<int64_t>(row) * PQ;
+      if (r.full) {
+        __builtin_memcpy(part + o, &lo[it], 16);
+        __builtin_memcpy(part + o + 4, &hi[it], 16);
+      } else {
+        const float vals[8] = {lo[it].x, lo[it].y, lo[it].z, lo[it].w, hi[it].x, hi[it].y, hi[it].z, hi[it].w};
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+          if (t < r.nvalid) part[o + t + (t >= r.wrap ? next_img : 0)] = vals[t];
+      }
+    }
+    __builtin_amdgcn_wave_barrier();  // the next pass reuses this wave's stage
+  }
+}
+
 // The epilogue of one BM x BN tile (rows k0.. of group g, pixels j0..)
 // computed by four waves in a 2 x 2 layout, each holding (BM/2) x 64; the
 // caller provides 32 KiB of LDS (8 KiB per wave).

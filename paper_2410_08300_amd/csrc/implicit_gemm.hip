@@ -618,7 +618,11 @@ constexpr int kDmaStages = 4;  // LDS stages of the 1x1 DMA kernel (plus 32 KiB 
 
 template <int UB, int NS>
 __global__ __launch_bounds__(2 * kThreads) void pointwise_dma_kernel(PwArgs a) {
-  constexpr int BM = 128, MI = 2, NJ = 2;
+  // Compute waves in a 4 x 1 layout: wave w holds rows 32 w .. 32 w + 31 of
+  // the 128 x 128 tile and all 128 pixels, as pixels x channels (the MFMA's
+  // A operand is the pixel fragment), so that its epilogue stores whole
+  // 256-byte channel rows.
+  constexpr int BM = 128, MI = 1, NJ = 4;
   constexpr int CC = 64;                                // channels per chunk
   constexpr int A_INS = 4;                              // A DMA instructions per loader wave per chunk
   constexpr int B_INS = (CC * BN * 2) / (64 * UB) / 4;  // B DMA instructions per loader wave per chunk
@@ -632,7 +636,6 @@ __global__ __launch_bounds__(2 * kThreads) void pointwise_dma_kernel(PwArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const bool loader = wave >= 4;                        // waves 4..7 issue the DMA, 0..3 multiply
   const int lw = wave & 3;
-  const int wm = lw >> 1, wn = lw & 1;
   const int half = lane >> 5, l32 = lane & 31;
 
   const int units = a.ptiles * a.ktiles * a.e.splits;
@@ -764,14 +767,14 @@ __global__ __launch_bounds__(2 * kThreads) void pointwise_dma_kernel(PwArgs a) {
     const int c_rel = 8 * (g >> 1) + (r >> 2);
 #pragma unroll
     for (int nj = 0; nj < NJ; ++nj) {
-      const int px = wn * 64 + nj * 32 + 16 * (g & 1) + 4 * (r & 3);
+      const int px = nj * 32 + 16 * (g & 1) + 4 * (r & 3);
       b_off[nj] = c_rel * 256 + ((((px >> 3) ^ (4 * (c_rel & 3)))) << 4) + ((px >> 2) & 1) * 8;
     }
   }
   int a_off[MI], a_swz[MI];
 #pragma unroll
   for (int mi = 0; mi < MI; ++mi) {
-    const int row = wm * 64 + mi * 32 + l32;
+    const int row = lw * 32 + mi * 32 + l32;
     a_off[mi] = row * 8;
     a_swz[mi] = (row >> 1) & 7;
   }
@@ -805,7 +808,7 @@ __global__ __launch_bounds__(2 * kThreads) void pointwise_dma_kernel(PwArgs a) {
       for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
         for (int nj = 0; nj < NJ; ++nj)
-          acc[mi][nj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mi], bfr[nj], acc[mi][nj], 0, 0, 0);
+          acc[mi][nj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[nj], af[mi], acc[mi][nj], 0, 0, 0);
     }
     lds_sync();  // B: the stage may be refilled
     cstage = cstage + 1 == NS ? 0 : cstage + 1;
@@ -813,7 +816,8 @@ __global__ __launch_bounds__(2 * kThreads) void pointwise_dma_kernel(PwArgs a) {
       // Tile done: each compute wave stages its part in its own region.
       const int tile = cu / a.e.splits;
       const int pt = tile / a.ktiles, kt = tile - pt * a.ktiles;
-      store_tile<bf16_t, BM>(acc, staging, a.e, pt * BN, kt * BM, 0, cu % a.e.splits);
+      store_block128t<bf16_t>(acc, reinterpret_cast<float*>(staging) + lw * 32 * 64, a.e, kt * BM + lw * 32, pt * BN,
+                              0, cu % a.e.splits);
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi)
 #pragma unroll

@@ -237,15 +237,21 @@ __global__ __launch_bounds__(2 * kThreads) void implicit_ws_kernel(WsArgs a) {
       // The register is refilled with the next chunk's fragment of this tap
       // as soon as this chunk is done with it.
       if (more) af[st] = __builtin_amdgcn_raw_buffer_load_b128(wr, aoff + 32 * st, so_next, 0);
+      // With 128 pixels per wave the accumulators hold pixels x channels
+      // (pixel fragment as the A operand), the layout of its epilogue.
 #pragma unroll
       for (int nj = 0; nj < NJW; ++nj)
-        acc[0][nj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, bfr[nj], acc[0][nj], 0, 0, 0);
+        acc[0][nj] = NJW == 4 ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[nj], a0, acc[0][nj], 0, 0, 0)
+                              : __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, bfr[nj], acc[0][nj], 0, 0, 0);
     }
     lds_sync();  // B(i)
   }
   // The loaders are done with LDS after B of the last chunk: stage there.
   float* stage = reinterpret_cast<float*>(smem) + wave * 32 * 64;
-  store_block<bf16_t, 1, NJW>(acc, stage, a.e, k0 + wm * 32, col0, 0, split);
+  if constexpr (NJW == 4)
+    store_block128t<bf16_t>(acc, stage, a.e, k0 + wm * 32, col0, 0, split);
+  else
+    store_block<bf16_t, 1, NJW>(acc, stage, a.e, k0 + wm * 32, col0, 0, split);
 }
 
 // Package: unit (ch, kp, u) with u = tap * 2 + cg holds channels
