@@ -1084,6 +1084,7 @@ struct PwPlan {
   bool gather;
   bool dma;              // bf16: the LDS-DMA kernel
   bool repack;           // ... on a repacked input (see repack_plane_kernel)
+  bool ub4;              // ... reading pixel pairs in place (4-byte DMA units)
   int span;              // pixels per image of the tile index space
   size_t repack_bytes;   // repacked input of one launch
   int64_t images_per_launch;
@@ -1096,11 +1097,14 @@ template <typename T>
 bool make_pw_plan(const Shape& s, PwPlan& pl, int64_t N1 = -1, bool allow_dma = true) {
   constexpr int UE = elem<T>::per16;
   if (s.R != 1 || s.S != 1 || s.G != 1 || s.C % UE != 0) return false;
-  // bf16: the DMA kernel, on the input as it is when its plane is a
-  // multiple of 8 pixels and the layer unstrided and unpadded, else on a
-  // repacked copy (plane = P*Q rounded up to 8).
+  // bf16: the DMA kernel, on the input as it is when the layer is
+  // unstrided and unpadded and its plane a multiple of 8 pixels (16-byte
+  // units) or of 2 (4-byte units: pixel pairs, as on 14 x 14 planes), else
+  // on a repacked copy (plane = P*Q rounded up to 8).
   pl.dma = sizeof(T) == 2 && allow_dma;
-  pl.repack = pl.dma && !(s.sh == 1 && s.sw == 1 && s.ph == 0 && s.pw == 0 && (s.H * s.W) % 8 == 0);
+  const bool plain = s.sh == 1 && s.sw == 1 && s.ph == 0 && s.pw == 0;
+  pl.ub4 = pl.dma && plain && (s.H * s.W) % 8 != 0 && (s.H * s.W) % 2 == 0;
+  pl.repack = pl.dma && !(plain && (s.H * s.W) % 8 == 0) && !pl.ub4;
   pl.span = pl.repack ? (int)((s.P * s.Q + 7) / 8 * 8) : pl.dma ? (int)(s.H * s.W) : (int)(s.P * s.Q);
   int64_t img_bytes = s.C * s.H * s.W * s.esize();
   if (pl.repack && s.C * pl.span * s.esize() > img_bytes) img_bytes = s.C * pl.span * s.esize();
@@ -1199,7 +1203,8 @@ hipError_t pw_main_typed(const Shape& s, const void* x, const void* w, const voi
   if (reinterpret_cast<uintptr_t>(w) % 16 != 0) return hipErrorInvalidValue;
   // An unaligned input that would be read in place cannot go through the
   // DMA: those calls take the register-transposing kernel.
-  if (pl.dma && !pl.repack && reinterpret_cast<uintptr_t>(x) % 16 != 0 && !make_pw_plan<T>(s, pl, -1, false))
+  if (pl.dma && !pl.repack && reinterpret_cast<uintptr_t>(x) % (pl.ub4 ? 4 : 16) != 0 &&
+      !make_pw_plan<T>(s, pl, -1, false))
     return hipErrorInvalidValue;
   char* ws = reinterpret_cast<char*>(part_ws);
   const int64_t img_elems = s.C * s.H * s.W, out_elems = s.K * s.P * s.Q;
@@ -1230,7 +1235,7 @@ hipError_t pw_main_typed(const Shape& s, const void* x, const void* w, const voi
         a.x = ws;
         a.x_bytes = (uint32_t)(cnt * s.C * cur.span * s.esize());
       }
-      e = pw_dma_launch<16>(cur, a, stream);
+      e = cur.ub4 ? pw_dma_launch<4>(cur, a, stream) : pw_dma_launch<16>(cur, a, stream);
     } else {
       // Pixel-quad loads need the input aligned to 4 elements.
       const bool gather = cur.gather || reinterpret_cast<uintptr_t>(a.x) % (4 * s.esize()) != 0;
@@ -1275,9 +1280,10 @@ std::string pw_describe(const Shape& s) {
   const char* tn = sizeof(T) == 2 ? "bf16" : "f32";
   if (pl.dma) {
     snprintf(buf, sizeof(buf),
-             "implicit_gemm kernels=%spointwise_dma_kernel<16,%d>%s tile=128x%d units=%dx%dx%d grid=%d chunk=64 "
+             "implicit_gemm kernels=%spointwise_dma_kernel<%d,%d>%s tile=128x%d units=%dx%dx%d grid=%d chunk=64 "
              "span=%d lds=%zu images_per_launch=%lld (1x1: filters used as given)",
-             pl.repack ? "repack_plane_kernel;" : "", kDmaStages, pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "",
+             pl.repack ? "repack_plane_kernel;" : "", pl.ub4 ? 4 : 16, kDmaStages,
+             pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "",
              BN, pl.a.ptiles, pl.a.ktiles, pl.a.e.splits, pw_dma_grid(pl.a), pl.span, pl.lds,
              (long long)pl.images_per_launch);
     return buf;

@@ -37,6 +37,10 @@ constexpr int kWsUnits = kWsTaps * kWsNG;  // 16-byte filter units per row and c
 constexpr int kWsUR = kWsUnits | 1;        // LDS / package row stride (odd)
 constexpr int kWsPS = kWsNG | 1;           // halo pixel stride in units (odd)
 constexpr int kWsMaxH = 4;                 // halo items per loader lane per chunk
+// One 32-row fragment per compute wave (4 x 1 layout at BM = 128): two
+// fragments per wave (2 x 2) halve the LDS operand reads but duplicate the
+// filter loads of each wave pair, and measured 10-20% slower.
+constexpr int kWsMW128 = 1;
 
 struct WsArgs {
   const void* x;        // first image of this launch
@@ -61,7 +65,8 @@ __device__ __forceinline__ int ws_vrow(int j, const WsArgs& a) {
 
 // PAIR: the halo is read as pixel pairs (W even: a pair at an even input
 // column is one aligned 32-bit word per channel); otherwise pixel by pixel.
-template <int BM, bool PAIR>
+// MW: 32-row filter fragments per compute wave (its rows: 32 MW).
+template <int BM, bool PAIR, int MW>
 __global__ __launch_bounds__(2 * kThreads) void implicit_ws_kernel(WsArgs a) {
   extern __shared__ __align__(16) vec16 smem[];
   char* lds = reinterpret_cast<char*>(smem);
@@ -183,8 +188,11 @@ __global__ __launch_bounds__(2 * kThreads) void implicit_ws_kernel(WsArgs a) {
   }
 
   // ---------------- compute waves ----------------
-  // Layout: WM x WN waves, each 32 filter rows x (BN / WN) pixels.
-  constexpr int WM = BM / 32, WN = 4 / WM, NJW = BN / 32 / WN;
+  // Layout: WM x WN waves, each 32 MW filter rows x (BN / WN) pixels.  With
+  // 128 pixels per wave (NJW = 4) the MFMA computes pixels x channels for
+  // the channel-row epilogue; otherwise channels x pixels.
+  constexpr int WM = BM / (32 * MW), WN = 4 / WM, NJW = BN / 32 / WN;
+  static_assert(WM * WN == 4 && (NJW != 4 || MW == 1), "four compute waves");
   const int wm = wave / WN, wn = wave - (wave / WN) * WN;
   const int half = lane >> 5, l32 = lane & 31;
   const int PQ = a.P * a.Q;
@@ -205,21 +213,27 @@ __global__ __launch_bounds__(2 * kThreads) void implicit_ws_kernel(WsArgs a) {
     const int r = t / a.S, s = t - r * a.S;
     tapoff[t] = (r * a.dh * a.Wv + s * a.dw) * kWsPS;
   }
-  // Filter fragments: lane l of tap t reads unit 2t + l/32 of row
-  // k0 + 32 wm + l%32 (the package is zero past K and C).
+  // Filter fragments: lane l of tap t, fragment m reads unit 2t + l/32 of
+  // row k0 + 32 (MW wm + m) + l%32 (the package is zero past K and C).
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.wp, a.wp_bytes);
-  const uint32_t aoff = static_cast<uint32_t>(((k0 + wm * 32 + l32) * kWsUR + half) * 16);
+  const uint32_t aoff = static_cast<uint32_t>(((k0 + wm * 32 * MW + l32) * kWsUR + half) * 16);
+  constexpr uint32_t kFragStride = 32 * kWsUR * 16;  // bytes between 32-row fragments
   auto chunk_soff = [&](int ch) { return static_cast<uint32_t>((ch_begin + ch) * a.Kpad * kWsUR * 16); };
-  u32x4_t af[kWsTaps];
+  u32x4_t af[kWsTaps][MW];
   {
     const uint32_t so = chunk_soff(0);
 #pragma unroll
-    for (int t = 0; t < kWsTaps; ++t) af[t] = __builtin_amdgcn_raw_buffer_load_b128(wr, aoff + 32 * t, so, 0);
+    for (int t = 0; t < kWsTaps; ++t)
+#pragma unroll
+      for (int m = 0; m < MW; ++m)
+        af[t][m] = __builtin_amdgcn_raw_buffer_load_b128(wr, aoff + m * kFragStride + 32 * t, so, 0);
   }
 
-  f32x16_t acc[1][NJW];
+  f32x16_t acc[MW][NJW];
 #pragma unroll
-  for (int nj = 0; nj < NJW; ++nj) acc[0][nj] = zero16();
+  for (int m = 0; m < MW; ++m)
+#pragma unroll
+    for (int nj = 0; nj < NJW; ++nj) acc[m][nj] = zero16();
 
   for (int i = 0; i < nchunks; ++i) {
     lds_sync();  // A(i)
@@ -230,19 +244,24 @@ __global__ __launch_bounds__(2 * kThreads) void implicit_ws_kernel(WsArgs a) {
     for (int st = 0; st < kWsTaps; ++st) {
       // Units 2st (channels 0-7) and 2st+1 (8-15) of tap st: lane half h
       // takes unit 2st+h, i.e. channel group h.
-      const bf16x8_t a0 = __builtin_bit_cast(bf16x8_t, af[st]);
+      bf16x8_t a0[MW];
+#pragma unroll
+      for (int m = 0; m < MW; ++m) a0[m] = __builtin_bit_cast(bf16x8_t, af[st][m]);
       bf16x8_t bfr[NJW];
 #pragma unroll
       for (int nj = 0; nj < NJW; ++nj) bfr[nj] = __builtin_bit_cast(bf16x8_t, Xs[pofs[nj] + tapoff[st]]);
-      // The register is refilled with the next chunk's fragment of this tap
-      // as soon as this chunk is done with it.
-      if (more) af[st] = __builtin_amdgcn_raw_buffer_load_b128(wr, aoff + 32 * st, so_next, 0);
-      // With 128 pixels per wave the accumulators hold pixels x channels
-      // (pixel fragment as the A operand), the layout of its epilogue.
+      // The registers are refilled with the next chunk's fragments of this
+      // tap as soon as this chunk is done with them.
+      if (more)
 #pragma unroll
-      for (int nj = 0; nj < NJW; ++nj)
-        acc[0][nj] = NJW == 4 ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[nj], a0, acc[0][nj], 0, 0, 0)
-                              : __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, bfr[nj], acc[0][nj], 0, 0, 0);
+        for (int m = 0; m < MW; ++m)
+          af[st][m] = __builtin_amdgcn_raw_buffer_load_b128(wr, aoff + m * kFragStride + 32 * st, so_next, 0);
+#pragma unroll
+      for (int m = 0; m < MW; ++m)
+#pragma unroll
+        for (int nj = 0; nj < NJW; ++nj)
+          acc[m][nj] = NJW == 4 ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[nj], a0[m], acc[m][nj], 0, 0, 0)
+                                : __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[m], bfr[nj], acc[m][nj], 0, 0, 0);
     }
     lds_sync();  // B(i)
   }
@@ -251,7 +270,7 @@ __global__ __launch_bounds__(2 * kThreads) void implicit_ws_kernel(WsArgs a) {
   if constexpr (NJW == 4)
     store_block128t<bf16_t>(acc, stage, a.e, k0 + wm * 32, col0, 0, split);
   else
-    store_block<bf16_t, 1, NJW>(acc, stage, a.e, k0 + wm * 32, col0, 0, split);
+    store_block<bf16_t, MW, NJW>(acc, stage, a.e, k0 + wm * 32 * MW, col0, 0, split);
 }
 
 // Package: unit (ch, kp, u) with u = tap * 2 + cg holds channels
@@ -328,9 +347,9 @@ bool make_ws_plan(const Shape& s, WsPlan& pl, int64_t N1 = -1) {
   return true;
 }
 
-template <int BM, bool PAIR>
+template <int BM, bool PAIR, int MW>
 hipError_t ws_launch(const WsPlan& pl, const WsArgs& a, hipStream_t stream) {
-  const auto kern = implicit_ws_kernel<BM, PAIR>;
+  const auto kern = implicit_ws_kernel<BM, PAIR, MW>;
   // Raise the dynamic-LDS limit once (calls may be captured into a graph
   // after the first one).
   static std::atomic<int> lds_limit{64 * 1024};
@@ -408,9 +427,9 @@ hipError_t ws_main(const Shape& s, const void* x, const void* wp, const void* b,
     const bool pair = cur.pair && reinterpret_cast<uintptr_t>(a.x) % 4 == 0;
     hipError_t e;
     if (cur.BM == 64)
-      e = pair ? ws_launch<64, true>(cur, a, stream) : ws_launch<64, false>(cur, a, stream);
+      e = pair ? ws_launch<64, true, 1>(cur, a, stream) : ws_launch<64, false, 1>(cur, a, stream);
     else
-      e = pair ? ws_launch<128, true>(cur, a, stream) : ws_launch<128, false>(cur, a, stream);
+      e = pair ? ws_launch<128, true, kWsMW128>(cur, a, stream) : ws_launch<128, false, kWsMW128>(cur, a, stream);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
@@ -421,10 +440,10 @@ std::string ws_describe(const Shape& s) {
   if (!make_ws_plan(s, pl)) return "implicit_gemm (loader/compute waves): not applicable";
   char buf[448];
   snprintf(buf, sizeof(buf),
-           "implicit_gemm kernels=pack_filters_ws_kernel;implicit_ws_kernel<%d,%d>%s tile=%dx%d grid=%dx%dx%d "
+           "implicit_gemm kernels=pack_filters_ws_kernel;implicit_ws_kernel<%d,%d,%d>%s tile=%dx%d grid=%dx%dx%d "
            "chunk=16 halo_rows=%d halo_items=%d lds=%zu images_per_launch=%lld (loader waves: halo %s loads "
            "into LDS; compute waves: filters from L2 into registers, MFMA)",
-           pl.BM, pl.pair ? 1 : 0, pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "", pl.BM, BN,
+           pl.BM, pl.pair ? 1 : 0, pl.BM == 128 ? kWsMW128 : 1, pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "", pl.BM, BN,
            (pl.a.NPQ + BN - 1) / BN, pl.a.Kpad / pl.BM, pl.a.e.splits, pl.a.VR, pl.a.items, pl.lds,
            (long long)pl.images_per_launch, pl.pair ? "pixel-pair" : "pixel");
   return buf;

@@ -121,14 +121,14 @@ def test_workspace_sizes():
     # 64 -> 64 channels, 56x56, batch 32: 784 tiles of 64 x 128, no split.
     large = _lib.make_desc(32, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, "bf16")
     assert _lib.workspace_bytes(large, "implicit_gemm") == 4 * 64 * 19 * 16
-    assert "implicit_ws_kernel<64,1>" in _lib.describe(large, "implicit_gemm")
+    assert "implicit_ws_kernel<64,1,1>" in _lib.describe(large, "implicit_gemm")
     # 512 -> 512 channels, 7x7, batch 32: 13 x 4 tiles of 128 x 128 leave
     # most of 256 CUs idle, so the 32 chunks are split four ways; the odd
     # plane width takes the pixel-by-pixel halo loads.
     small = _lib.make_desc(32, 512, 7, 7, 512, 3, 3, 1, 1, 1, 1, "bf16")
     packed = 32 * 512 * 19 * 16
     assert _lib.workspace_bytes(small, "implicit_gemm") == packed + 4 * 32 * 512 * 49 * 4
-    assert "implicit_ws_kernel<128,0>;splitk_reduce_kernel" in _lib.describe(small, "implicit_gemm")
+    assert "implicit_ws_kernel<128,0,1>;splitk_reduce_kernel" in _lib.describe(small, "implicit_gemm")
     # fp32 3x3 keeps the general kernel: [chunk][K padded][tap][units].
     f32 = _lib.make_desc(32, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, "f32")
     assert _lib.workspace_bytes(f32, "implicit_gemm") == 8 * 64 * 18 * 16
@@ -150,6 +150,11 @@ def test_workspace_sizes():
     pwf = _lib.make_desc(32, 256, 56, 56, 64, 1, 1, 1, 0, 1, 1, "f32")
     assert "pointwise_gemm_kernel<f32,64,0,2>" in _lib.describe(pwf, "implicit_gemm")
     assert "pointwise_dma_kernel<16,4>" in _lib.describe(pw, "implicit_gemm")
+    # A 14x14 plane (even, not a multiple of 8) is read in place as pixel
+    # pairs: no repack, 4-byte DMA units.
+    pw14 = _lib.make_desc(32, 256, 14, 14, 1024, 1, 1, 1, 0, 1, 1, "bf16")
+    assert "kernels=pointwise_dma_kernel<4,4>" in _lib.describe(pw14, "implicit_gemm")
+    assert _lib.prepacked_workspace_bytes(pw14, "implicit_gemm") == 0
     # The 7x7 stride-2 stem (bf16, 3 channels) takes the filter-row kernel:
     # its package is the LDS image of each 64-filter tile, 64 x 23 units of
     # 16 bytes (21 filter rows, rounded up to an odd count); no other

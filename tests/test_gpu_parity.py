@@ -257,6 +257,7 @@ POINTWISE = [
     (2, 1000, 7, 7, 300, 1, 0, "bf16", True, True, "channel split over workgroups, tail chunk"),
     (2, 40, 9, 12, 40, 1, 0, "f32", False, False, "K <= 64 tile"),
     (4, 24, 28, 28, 64, 1, 0, "bf16", False, False, "single partial chunk"),
+    (3, 256, 14, 14, 300, 1, 0, "bf16", True, False, "14x14 plane read in place as pixel pairs, tiles cross images"),
 ]
 
 
@@ -270,11 +271,13 @@ def test_pointwise_paths(idx):
     check_full(x, w, b, st, pd, 1, 1, relu, ("implicit_gemm", "im2col_gemm", "direct"), what)
 
 
-@pytest.mark.parametrize("which", ["x", "w"])
-def test_pointwise_unaligned_operands(which):
+@pytest.mark.parametrize("which,side", [("x", 12), ("w", 12), ("x", 14)])
+def test_pointwise_unaligned_operands(which, side):
     """1x1 layer with the input (gather variant) or the filters (copied into
-    the workspace first) one element past a 16-byte boundary."""
-    N, C, H, Wd, K = 2, 64, 12, 12, 80
+    the workspace first) one element past a 16-byte boundary; a 14 x 14
+    plane is otherwise read in place as pixel pairs, which needs 4-byte
+    alignment."""
+    N, C, H, Wd, K = 2, 64, side, side, 80
     g = torch.Generator().manual_seed(W.seed_for(12, 0 if which == "x" else 1))
     x = torch.randn(N, C, H, Wd, generator=g).to(torch.bfloat16)
     w = (torch.randn(K, C, 1, 1, generator=g) * (2.0 / C) ** 0.5).to(torch.bfloat16)
