@@ -275,24 +275,48 @@ __global__ __launch_bounds__(2 * kThreads) void implicit_ws_kernel(WsArgs a) {
 
 // Package: unit (ch, kp, u) with u = tap * 2 + cg holds channels
 // ch*16 + cg*8 .. +7 of filter kp at that tap; unit 18 of each row and
-// everything past K or C is zero.
-__global__ __launch_bounds__(256) void pack_filters_ws_kernel(const uint16_t* __restrict__ w, u32x4_t* __restrict__ wp,
-                                                             int K, int C, int Kpad, int total) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= total) return;
-  const int u = i % kWsUR, row = i / kWsUR;
+// everything past K or C is zero.  One thread per (row (ch, kp), channel
+// group cg): its source, channels ch*16 + cg*8 .. +7 x 9 taps of filter kp,
+// is 72 consecutive elements of w (144 bytes), read as 9 loads of 16 bytes
+// when w is 16-byte aligned and C % 16 == 0, and regrouped in registers into
+// the group's 9 units.
+constexpr int kPackWsThreads = 64;
+__global__ __launch_bounds__(kPackWsThreads) void pack_filters_ws_kernel(const uint16_t* __restrict__ w,
+                                                                        u32x4_t* __restrict__ wp, int K, int C,
+                                                                        int Kpad, int items, int vec) {
+  const int item = blockIdx.x * kPackWsThreads + threadIdx.x;
+  if (item >= items) return;
+  const int cg = item & 1, row = item >> 1;
   const int kp = row % Kpad, ch = row / Kpad;
-  const int tap = u / kWsNG, cg = u - tap * kWsNG;
-  uint32_t v[8];
+  u32x4_t* dst = wp + static_cast<int64_t>(row) * kWsUR;
+  uint32_t v[72];  // element i = (c - ch*16 - cg*8) * 9 + tap, zero-extended
+  if (kp < K && vec) {
+    const u32x4_t* src =
+        reinterpret_cast<const u32x4_t*>(w + (static_cast<int64_t>(kp) * C + ch * 16 + cg * 8) * kWsTaps);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int c = ch * 16 + cg * 8 + e;
-    v[e] = u < kWsUnits && kp < K && c < C ? w[(static_cast<int64_t>(kp) * C + c) * kWsTaps + tap] : 0u;
+    for (int q = 0; q < 9; ++q) {
+      const u32x4_t d = src[q];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[8 * q + 2 * e] = d[e] & 0xFFFFu;
+        v[8 * q + 2 * e + 1] = d[e] >> 16;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 72; ++i) {
+      const int c = ch * 16 + cg * 8 + i / kWsTaps;
+      v[i] = kp < K && c < C ? w[(static_cast<int64_t>(kp) * C + c) * kWsTaps + i % kWsTaps] : 0u;
+    }
   }
-  u32x4_t o;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) o[q] = v[2 * q] | (v[2 * q + 1] << 16);
-  wp[i] = o;
+  for (int tap = 0; tap < kWsTaps; ++tap) {
+    u32x4_t o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = v[(2 * q) * kWsTaps + tap] | (v[(2 * q + 1) * kWsTaps + tap] << 16);
+    dst[tap * kWsNG + cg] = o;
+  }
+  if (cg == 0) dst[kWsUnits] = u32x4_t{0u, 0u, 0u, 0u};
 }
 
 struct WsPlan {
@@ -397,10 +421,11 @@ size_t ws_split_bytes(const Shape& s) {
 hipError_t ws_pack(const Shape& s, const void* w, void* wp, hipStream_t stream) {
   WsPlan pl;
   if (!make_ws_plan(s, pl)) return hipErrorInvalidValue;
-  const int total = pl.a.nch * pl.a.Kpad * kWsUR;
-  hipLaunchKernelGGL(pack_filters_ws_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
-                     reinterpret_cast<const uint16_t*>(w), reinterpret_cast<u32x4_t*>(wp), (int)s.K, (int)s.C,
-                     pl.a.Kpad, total);
+  const int items = pl.a.nch * pl.a.Kpad * kWsNG;
+  const int vec = s.C % 16 == 0 && reinterpret_cast<uintptr_t>(w) % 16 == 0;
+  hipLaunchKernelGGL(pack_filters_ws_kernel, dim3((unsigned)((items + kPackWsThreads - 1) / kPackWsThreads)),
+                     dim3(kPackWsThreads), 0, stream, reinterpret_cast<const uint16_t*>(w), reinterpret_cast<u32x4_t*>(wp),
+                     (int)s.K, (int)s.C, pl.a.Kpad, items, vec);
   return hipGetLastError();
 }
 

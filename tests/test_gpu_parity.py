@@ -355,6 +355,26 @@ def test_filter_row_kernel_unaligned_filters_and_nonfinite_outside_taps():
     assert rel_err(f64(y), ref) <= tolerance("bf16", "implicit_gemm")
 
 
+@pytest.mark.parametrize("C", [64, 40])
+def test_3x3_unaligned_filters(C):
+    """bf16 3x3 layer whose filters start one element past a 16-byte
+    boundary: the package is built element by element (as for C % 16 != 0)
+    instead of from 16-byte loads."""
+    N, H, Wd, K = 2, 12, 12, 96
+    g = torch.Generator().manual_seed(W.seed_for(16, C))
+    x = torch.randn(N, C, H, Wd, generator=g).to(torch.bfloat16)
+    w = (torch.randn(K, C, 3, 3, generator=g) * (2.0 / (9 * C)) ** 0.5).to(torch.bfloat16)
+    ref = oracle.conv2d(f64(x), f64(w), None, 1, 1, 1, 1, False)
+    buf = torch.empty(w.numel() + 1, dtype=w.dtype, device=DEV)
+    buf[1:].copy_(w.reshape(-1).to(DEV))
+    wd = buf[1:].view(w.shape)
+    assert wd.data_ptr() % 16 != 0
+    say("case 3x3 unaligned filters", C)
+    y = cs.conv2d(x.to(DEV), wd, None, 1, 1, algo="implicit_gemm")
+    torch.cuda.synchronize()
+    assert rel_err(f64(y), ref) <= tolerance("bf16", "implicit_gemm")
+
+
 # Every byte a call writes must lie in y or in its workspace: the operands
 # and the workspace sit in one buffer between guard bands of a fill pattern,
 # and after the call the guards and the inputs must be unchanged.
