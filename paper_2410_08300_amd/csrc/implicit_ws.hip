@@ -116,17 +116,23 @@ __global__ __launch_bounds__(2 * kThreads) void implicit_ws_kernel(WsArgs a) {
       }
     }
     uint32_t hd[kWsMaxH][8];
+    // Channel c0 + e of an item lies at its channel-0 offset plus
+    // (c0 + e) * plane: the second part is the same for every lane, so it
+    // goes into the load's scalar offset and the per-lane offset stays fixed
+    // for the whole tile.  Only the last, partial chunk checks channels per
+    // lane.  An item outside the image has offset x_bytes, which stays past
+    // the buffer's end whatever is added.
     auto issue_halo = [&](int ch) {
       const int c0 = (ch_begin + ch) * 16;
       const bool tail = c0 + 16 > a.C;
-      const uint32_t so = static_cast<uint32_t>(c0) * plane;
 #pragma unroll
       for (int t = 0; t < kWsMaxH; ++t) {
         if (t < a.nh) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const bool ok = hvo[t] != a.x_bytes && !(tail && c0 + hcg[t] * 8 + e >= a.C);
-            const uint32_t vo = ok ? hvo[t] + static_cast<uint32_t>(e) * plane : a.x_bytes;
+            const uint32_t so = static_cast<uint32_t>(c0 + e) * plane;
+            uint32_t vo = hvo[t];
+            if (tail && c0 + hcg[t] * 8 + e >= a.C) vo = a.x_bytes;
             if constexpr (PAIR)
               hd[t][e] = __builtin_amdgcn_raw_buffer_load_b32(xr, vo, so, 0);
             else
