@@ -225,14 +225,22 @@ __global__ __launch_bounds__(2 * kThreads) void implicit_ws_kernel(WsArgs a) {
   const uint32_t aoff = static_cast<uint32_t>(((k0 + wm * 32 * MW + l32) * kWsUR + half) * 16);
   constexpr uint32_t kFragStride = 32 * kWsUR * 16;  // bytes between 32-row fragments
   auto chunk_soff = [&](int ch) { return static_cast<uint32_t>((ch_begin + ch) * a.Kpad * kWsUR * 16); };
-  u32x4_t af[kWsTaps][MW];
+  // At BM = 128 two fragment sets alternate by chunk parity: chunk i+1's
+  // fragments are requested into one set before chunk i multiplies with the
+  // other (with one set refilled in place the compiler shuffled registers
+  // and waited for every outstanding load at the top of each chunk).  At
+  // BM = 64 the second set would raise the kernel past 128 VGPRs and halve
+  // the workgroups per CU, which costs more: there one set is refilled tap
+  // by tap right after its last use.
+  constexpr bool kTwoSets = BM == 128;
+  u32x4_t afA[kWsTaps][MW], afB[kTwoSets ? kWsTaps : 1][MW];
   {
     const uint32_t so = chunk_soff(0);
 #pragma unroll
     for (int t = 0; t < kWsTaps; ++t)
 #pragma unroll
       for (int m = 0; m < MW; ++m)
-        af[t][m] = __builtin_amdgcn_raw_buffer_load_b128(wr, aoff + m * kFragStride + 32 * t, so, 0);
+        afA[t][m] = __builtin_amdgcn_raw_buffer_load_b128(wr, aoff + m * kFragStride + 32 * t, so, 0);
   }
 
   f32x16_t acc[MW][NJW];
@@ -241,27 +249,38 @@ __global__ __launch_bounds__(2 * kThreads) void implicit_ws_kernel(WsArgs a) {
 #pragma unroll
     for (int nj = 0; nj < NJW; ++nj) acc[m][nj] = zero16();
 
-  for (int i = 0; i < nchunks; ++i) {
+  // One chunk: LDS stage `par`, fragments `cur`; `nxt` receives chunk i+1's.
+  auto chunk = [&](int i, int par, u32x4_t(&cur)[kWsTaps][MW], u32x4_t(&nxt)[kWsTaps][MW]) {
     lds_sync();  // A(i)
-    const u32x4_t* Xs = reinterpret_cast<const u32x4_t*>(lds + (i & 1) * a.stage_bytes);
+    const u32x4_t* Xs = reinterpret_cast<const u32x4_t*>(lds + par * a.stage_bytes);
     const bool more = i + 1 < nchunks;
     const uint32_t so_next = chunk_soff(more ? i + 1 : i);
+    if constexpr (kTwoSets) {
+      // Requested on every chunk (the last one reloading its own, unused,
+      // so that the compiler can count the loads in flight); the scheduling
+      // barrier keeps them from being sunk to the end of the chunk.
+#pragma unroll
+      for (int st = 0; st < kWsTaps; ++st)
+#pragma unroll
+        for (int m = 0; m < MW; ++m)
+          nxt[st][m] = __builtin_amdgcn_raw_buffer_load_b128(wr, aoff + m * kFragStride + 32 * st, so_next, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
 #pragma unroll
     for (int st = 0; st < kWsTaps; ++st) {
       // Units 2st (channels 0-7) and 2st+1 (8-15) of tap st: lane half h
       // takes unit 2st+h, i.e. channel group h.
-      bf16x8_t a0[MW];
-#pragma unroll
-      for (int m = 0; m < MW; ++m) a0[m] = __builtin_bit_cast(bf16x8_t, af[st][m]);
-      bf16x8_t bfr[NJW];
+      bf16x8_t bfr[NJW], a0[MW];
 #pragma unroll
       for (int nj = 0; nj < NJW; ++nj) bfr[nj] = __builtin_bit_cast(bf16x8_t, Xs[pofs[nj] + tapoff[st]]);
-      // The registers are refilled with the next chunk's fragments of this
-      // tap as soon as this chunk is done with them.
-      if (more)
 #pragma unroll
-        for (int m = 0; m < MW; ++m)
-          af[st][m] = __builtin_amdgcn_raw_buffer_load_b128(wr, aoff + m * kFragStride + 32 * st, so_next, 0);
+      for (int m = 0; m < MW; ++m) a0[m] = __builtin_bit_cast(bf16x8_t, cur[st][m]);
+      if constexpr (!kTwoSets) {
+        if (more)
+#pragma unroll
+          for (int m = 0; m < MW; ++m)
+            cur[st][m] = __builtin_amdgcn_raw_buffer_load_b128(wr, aoff + m * kFragStride + 32 * st, so_next, 0);
+      }
 #pragma unroll
       for (int m = 0; m < MW; ++m)
 #pragma unroll
@@ -270,6 +289,14 @@ __global__ __launch_bounds__(2 * kThreads) void implicit_ws_kernel(WsArgs a) {
                                 : __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[m], bfr[nj], acc[m][nj], 0, 0, 0);
     }
     lds_sync();  // B(i)
+  };
+  if constexpr (kTwoSets) {
+    for (int i0 = 0; i0 < nchunks; i0 += 2) {
+      chunk(i0, 0, afA, afB);
+      if (i0 + 1 < nchunks) chunk(i0 + 1, 1, afB, afA);
+    }
+  } else {
+    for (int i = 0; i < nchunks; ++i) chunk(i, i & 1, afA, afA);
   }
   // The loaders are done with LDS after B of the last chunk: stage there.
   float* stage = reinterpret_cast<float*>(smem) + wave * 32 * 64;
