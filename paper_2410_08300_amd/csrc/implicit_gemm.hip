@@ -613,19 +613,25 @@ __global__ __launch_bounds__(kThreads) void pointwise_gemm_kernel(PwArgs a) {
 // staging are free of bank conflicts.
 // ---------------------------------------------------------------------------
 constexpr int kDmaStageBytes = 32 * 1024;
-constexpr int kDmaStages = 4;  // LDS stages of the 1x1 DMA kernel (plus 32 KiB of epilogue staging)
+constexpr int kDmaStages = 4;
+// Loader waves of the 1x1 DMA kernel.  Eight measured slower on most ResNet-50
+// 1x1 layers: at 768 threads the kernel must fit 168 VGPRs and spills.
+constexpr int kDmaLoaders = 4;  // LDS stages of the 1x1 DMA kernel (plus 32 KiB of epilogue staging)
 
 
-template <int UB, int NS>
-__global__ __launch_bounds__(2 * kThreads) void pointwise_dma_kernel(PwArgs a) {
+// NL loader waves (waves 4 .. 4+NL-1) share each chunk's DMA instructions.
+template <int UB, int NS, int NL>
+__global__ __launch_bounds__((4 + NL) * 64) void pointwise_dma_kernel(PwArgs a) {
   // Compute waves in a 4 x 1 layout: wave w holds rows 32 w .. 32 w + 31 of
   // the 128 x 128 tile and all 128 pixels, as pixels x channels (the MFMA's
   // A operand is the pixel fragment), so that its epilogue stores whole
   // 256-byte channel rows.
   constexpr int BM = 128, MI = 1, NJ = 4;
   constexpr int CC = 64;                                // channels per chunk
-  constexpr int A_INS = 4;                              // A DMA instructions per loader wave per chunk
-  constexpr int B_INS = (CC * BN * 2) / (64 * UB) / 4;  // B DMA instructions per loader wave per chunk
+  constexpr int A_INS = 16 / NL;                         // A DMA instructions per loader wave per chunk
+  constexpr int B_INS = (CC * BN * 2) / (64 * UB) / NL;  // B DMA instructions per loader wave per chunk
+  static_assert(A_INS * NL == 16 && B_INS * NL * 64 * UB == CC * BN * 2 && (UB == 16 || B_INS % 4 == 0),
+                "loader waves must split the chunk evenly");
   constexpr int INS = A_INS + B_INS;
   static_assert(UB == 16 || UB == 4, "DMA unit");
   static_assert((NS - 1) * INS <= 63, "vmcnt range");
@@ -634,8 +640,8 @@ __global__ __launch_bounds__(2 * kThreads) void pointwise_dma_kernel(PwArgs a) {
   vec16* staging = reinterpret_cast<vec16*>(lds + NS * kDmaStageBytes);  // 8 KiB per compute wave
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const bool loader = wave >= 4;                        // waves 4..7 issue the DMA, 0..3 multiply
-  const int lw = wave & 3;
+  const bool loader = wave >= 4;                        // waves 4.. issue the DMA, 0..3 multiply
+  const int lw = loader ? wave - 4 : wave;
   const int half = lane >> 5, l32 = lane & 31;
 
   const int units = a.ptiles * a.ktiles * a.e.splits;
@@ -1162,7 +1168,7 @@ int pw_grid(const PwArgs& a, int BM) {
 
 template <int UB>
 hipError_t pw_dma_launch(const PwPlan& pl, const PwArgs& a, hipStream_t stream) {
-  const auto kern = pointwise_dma_kernel<UB, kDmaStages>;
+  const auto kern = pointwise_dma_kernel<UB, kDmaStages, kDmaLoaders>;
   static std::atomic<int> lds_raised{0};
   if (!lds_raised.load()) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -1171,7 +1177,7 @@ hipError_t pw_dma_launch(const PwPlan& pl, const PwArgs& a, hipStream_t stream) 
     lds_raised.store(1);
   }
   const dim3 grid((unsigned)pw_dma_grid(a));
-  hipLaunchKernelGGL(kern, grid, dim3(2 * kThreads), pl.lds, stream, a);
+  hipLaunchKernelGGL(kern, grid, dim3((4 + kDmaLoaders) * 64), pl.lds, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.e.splits == 1) return e;
   // Outputs: images x K x P*Q (a.NPQ counts the padded pixel span).
