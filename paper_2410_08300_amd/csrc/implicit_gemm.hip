@@ -1286,9 +1286,9 @@ std::string pw_describe(const Shape& s) {
   const char* tn = sizeof(T) == 2 ? "bf16" : "f32";
   if (pl.dma) {
     snprintf(buf, sizeof(buf),
-             "implicit_gemm kernels=%spointwise_dma_kernel<%d,%d>%s tile=128x%d units=%dx%dx%d grid=%d chunk=64 "
+             "implicit_gemm kernels=%spointwise_dma_kernel<%d,%d,%d>%s tile=128x%d units=%dx%dx%d grid=%d chunk=64 "
              "span=%d lds=%zu images_per_launch=%lld (1x1: filters used as given)",
-             pl.repack ? "repack_plane_kernel;" : "", pl.ub4 ? 4 : 16, kDmaStages,
+             pl.repack ? "repack_plane_kernel;" : "", pl.ub4 ? 4 : 16, kDmaStages, kDmaLoaders,
              pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "",
              BN, pl.a.ptiles, pl.a.ktiles, pl.a.e.splits, pw_dma_grid(pl.a), pl.span, pl.lds,
              (long long)pl.images_per_launch);

@@ -145,15 +145,15 @@ def test_workspace_sizes():
     repack = 32 * 2048 * 56 * 2
     assert _lib.workspace_bytes(pws, "implicit_gemm") == 512 * 2048 * 2 + repack + 4 * 32 * 512 * 49 * 4
     assert _lib.prepacked_workspace_bytes(pws, "implicit_gemm") == repack + 4 * 32 * 512 * 49 * 4
-    assert "repack_plane_kernel;pointwise_dma_kernel<16,4>;splitk_reduce_kernel" in _lib.describe(pws, "implicit_gemm")
+    assert "repack_plane_kernel;pointwise_dma_kernel<16,4,4>;splitk_reduce_kernel" in _lib.describe(pws, "implicit_gemm")
     # fp32 1x1 layers keep the register-transposing kernel.
     pwf = _lib.make_desc(32, 256, 56, 56, 64, 1, 1, 1, 0, 1, 1, "f32")
     assert "pointwise_gemm_kernel<f32,64,0,2>" in _lib.describe(pwf, "implicit_gemm")
-    assert "pointwise_dma_kernel<16,4>" in _lib.describe(pw, "implicit_gemm")
+    assert "pointwise_dma_kernel<16,4,4>" in _lib.describe(pw, "implicit_gemm")
     # A 14x14 plane (even, not a multiple of 8) is read in place as pixel
     # pairs: no repack, 4-byte DMA units.
     pw14 = _lib.make_desc(32, 256, 14, 14, 1024, 1, 1, 1, 0, 1, 1, "bf16")
-    assert "kernels=pointwise_dma_kernel<4,4>" in _lib.describe(pw14, "implicit_gemm")
+    assert "kernels=pointwise_dma_kernel<4,4,4>" in _lib.describe(pw14, "implicit_gemm")
     assert _lib.prepacked_workspace_bytes(pw14, "implicit_gemm") == 0
     # The 7x7 stride-2 stem (bf16, 3 channels) takes the filter-row kernel:
     # its package is the LDS image of each 64-filter tile, 64 x 23 units of
