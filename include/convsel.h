@@ -18,9 +18,15 @@
  *
  * The algorithms are those the paper lets a user pick per layer (Sec. II-B and
  * Sec. V-B): direct convolution, implicit GEMM (no column matrix is formed),
- * IM2COL + GEMM (the column matrix is formed in a workspace, then multiplied),
- * and Winograd minimal filtering F(2x2, 3x3) for 3x3 stride-1 layers.  All of
- * them compute the same function; they differ in speed and workspace.
+ * implicit precomputed-index GEMM (the same, with the gather offsets of every
+ * reduction index and output pixel precomputed into tables), IM2COL + GEMM
+ * (the column matrix is formed in a workspace, then multiplied), KN2ROW (one
+ * GEMM of the tap-stacked filters with the input as it lies, then a
+ * shift-and-add of the R*S partial planes), SMM (the input zero-padded once,
+ * then every output plane accumulated as shifted input planes scaled by
+ * single filter values), and Winograd minimal filtering F(2x2, 3x3) for 3x3
+ * stride-1 layers.  All of them compute the same function; they differ in
+ * speed and workspace.
  *
  * Conventions shared by every entry point:
  *  - Layouts: x is N x C x H x W, w is K x Cg x R x S, b is K values, y is
@@ -63,7 +69,10 @@ typedef enum conv_algo {
   CONV_ALGO_DIRECT = 1,         /* paper Sec. II-B item (d) */
   CONV_ALGO_IMPLICIT_GEMM = 2,  /* paper Sec. V-B item (b) */
   CONV_ALGO_IM2COL_GEMM = 3,    /* paper Sec. II-B item (a), Sec. V-B item (c) */
-  CONV_ALGO_WINOGRAD = 4        /* paper Sec. V-B item (d): F(2x2,3x3) */
+  CONV_ALGO_WINOGRAD = 4,       /* paper Sec. V-B item (d): F(2x2,3x3) */
+  CONV_ALGO_IMPLICIT_PRECOMP_GEMM = 5,  /* paper Sec. V-B item (a) */
+  CONV_ALGO_KN2ROW = 6,         /* paper Sec. II-B item (b) */
+  CONV_ALGO_SMM = 7             /* paper Sec. II-B item (c): scalar MM with zero packing */
 } conv_algo_t;
 
 typedef enum conv_dtype {
@@ -90,7 +99,12 @@ typedef struct conv2d_desc {
 conv_status_t conv2d_output_shape(const conv2d_desc_t* desc, int64_t* p, int64_t* q);
 
 /* OK if `algo` can run this layer; UNSUPPORTED if the algorithm is not defined
- * for it (Winograd needs R = S = 3, stride 1, dilation 1, groups 1);
+ * for it (Winograd needs R = S = 3, stride 1, dilation 1, groups 1; implicit
+ * precomputed-index GEMM needs H + 2*pad_h and W + 2*pad_w below 16384, its
+ * coordinates being packed as 16-bit halves; KN2ROW needs R*S*K/groups*H*W
+ * below 2^31; SMM needs its zero-padded planes of one image below 2^31
+ * elements and groups * ceil(K/groups / 16) <= 65535) or for which implicit
+ * GEMM finds no tiling;
  * INVALID_ARG as conv2d_output_shape, or for an unknown algo value. */
 conv_status_t conv2d_check(const conv2d_desc_t* desc, conv_algo_t algo);
 
@@ -101,9 +115,15 @@ conv_status_t conv2d_check(const conv2d_desc_t* desc, conv_algo_t algo);
  *    for common layers), plus, for layers whose output tiles alone would
  *    leave compute units idle, S*N*K*P*Q fp32 partial sums of a channel
  *    split over S <= 8 workgroups (summed by a second, deterministic kernel).
+ *  - implicit precomputed-index GEMM: its package (zero-padded filters, one
+ *    8-byte table entry per reduction index and per output pixel of a launch).
  *  - IM2COL + GEMM and Winograd: the column matrix / transformed tiles, built
  *    for batches of images so the figure is capped near 1 GiB unless one
  *    image alone needs more.
+ *  - KN2ROW: the tap-stacked filters plus R*S*K*H*W fp32 partial planes per
+ *    image; SMM: the repacked filters plus the zero-padded input
+ *    (C x ((P-1)*stride_h + (R-1)*dil_h + 1) x ((Q-1)*stride_w + (S-1)*dil_w + 1)
+ *    per image); both batched over images with the same cap.
  * Same errors as conv2d_check. */
 conv_status_t conv2d_workspace_bytes(const conv2d_desc_t* desc, conv_algo_t algo, size_t* bytes);
 
@@ -123,8 +143,11 @@ conv_status_t conv2d(const void* x, const void* w, const void* b, void* y, const
                      conv_algo_t algo, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Filter packages.  Implicit GEMM and Winograd first rearrange the filters
- * (implicit GEMM: into its tile layout, zero-padded; Winograd: the filter
- * transform U below); conv2d() redoes that in its workspace on every call.
+ * (implicit GEMM: into its tile layout, zero-padded; implicit precomputed-
+ * index GEMM: zero-padded filters plus its index tables; KN2ROW: the
+ * tap-stacked filter matrix; SMM: blocks of 8 or 16 output channels with the
+ * channels innermost; Winograd: the filter transform U below); conv2d()
+ * redoes that in its workspace on every call.
  * An inference caller whose filters do not change can build the package
  * once and call conv2d_prepacked() instead, which then runs only the work
  * that depends on the input.  For direct and IM2COL + GEMM the package is a
@@ -177,7 +200,8 @@ const char* conv2d_status_string(conv_status_t status);
 const char* conv2d_algo_name(conv_algo_t algo);
 
 /* Parses "default", "direct", "implicit_gemm", "im2col_gemm" (alias "gemm"),
- * "winograd".  INVALID_ARG for NULL or any other name. */
+ * "winograd", "implicit_precomp_gemm", "kn2row", "smm".  INVALID_ARG for NULL
+ * or any other name. */
 conv_status_t conv2d_algo_from_name(const char* name, conv_algo_t* algo);
 
 #ifdef __cplusplus

@@ -16,7 +16,8 @@ CONV_ERR_UNSUPPORTED = 2
 CONV_ERR_WORKSPACE = 3
 CONV_ERR_DEVICE = 4
 
-ALGOS = {"default": 0, "direct": 1, "implicit_gemm": 2, "im2col_gemm": 3, "winograd": 4}
+ALGOS = {"default": 0, "direct": 1, "implicit_gemm": 2, "im2col_gemm": 3, "winograd": 4,
+         "implicit_precomp_gemm": 5, "kn2row": 6, "smm": 7}
 ALGO_NAMES = {v: k for k, v in ALGOS.items()}
 DTYPES = {"f32": 0, "bf16": 1}
 

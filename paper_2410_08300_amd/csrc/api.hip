@@ -70,6 +70,12 @@ conv_status_t support(const Shape& s, conv_algo_t algo) {
       return convsel::implicit_gemm_fits(s) ? CONV_OK : CONV_ERR_UNSUPPORTED;
     case CONV_ALGO_WINOGRAD:
       return winograd_ok(s) ? CONV_OK : CONV_ERR_UNSUPPORTED;
+    case CONV_ALGO_IMPLICIT_PRECOMP_GEMM:
+      return convsel::precomp_applies(s) ? CONV_OK : CONV_ERR_UNSUPPORTED;
+    case CONV_ALGO_KN2ROW:
+      return convsel::kn2row_applies(s) ? CONV_OK : CONV_ERR_UNSUPPORTED;
+    case CONV_ALGO_SMM:
+      return convsel::smm_applies(s) ? CONV_OK : CONV_ERR_UNSUPPORTED;
     default:
       return CONV_ERR_INVALID_ARG;
   }
@@ -128,6 +134,11 @@ size_t workspace_for(const Shape& s, conv_algo_t algo, bool prepacked = false) {
   if (algo == CONV_ALGO_WINOGRAD) return wino_layout(s, !prepacked).total;
   if (algo == CONV_ALGO_IMPLICIT_GEMM)
     return prepacked ? convsel::implicit_gemm_split_bytes(s) : convsel::implicit_gemm_workspace(s);
+  if (algo == CONV_ALGO_IMPLICIT_PRECOMP_GEMM) return prepacked ? 0 : convsel::precomp_packed_bytes(s);
+  if (algo == CONV_ALGO_KN2ROW)
+    return (prepacked ? 0 : align256(convsel::kn2row_packed_bytes(s))) + convsel::kn2row_z_bytes(s);
+  if (algo == CONV_ALGO_SMM)
+    return (prepacked ? 0 : align256(convsel::smm_packed_bytes(s))) + convsel::smm_zero_pack_bytes(s);
   return 0;
 }
 
@@ -135,6 +146,9 @@ size_t workspace_for(const Shape& s, conv_algo_t algo, bool prepacked = false) {
 size_t packed_filter_bytes(const Shape& s, conv_algo_t algo) {
   if (algo == CONV_ALGO_IMPLICIT_GEMM) return convsel::implicit_gemm_packed_bytes(s);
   if (algo == CONV_ALGO_WINOGRAD) return wino_u_bytes(s);
+  if (algo == CONV_ALGO_IMPLICIT_PRECOMP_GEMM) return convsel::precomp_packed_bytes(s);
+  if (algo == CONV_ALGO_KN2ROW) return convsel::kn2row_packed_bytes(s);
+  if (algo == CONV_ALGO_SMM) return convsel::smm_packed_bytes(s);
   return (size_t)s.K * s.Cg * s.R * s.S * s.esize();  // the filters themselves
 }
 
@@ -207,6 +221,7 @@ conv_status_t run(const Shape& s, conv_algo_t algo, const void* x, const void* w
         g.sBias1 = s.Kg;                               // group g's biases
         g.relu = s.relu ? 1 : 0;
         g.out_f32 = 0;
+        g.b_kmajor = 0;
         e = launch_gemm_nt(s.dtype, g, st);
         if (e != hipSuccess) return from_hip(e);
       }
@@ -239,12 +254,33 @@ conv_status_t run(const Shape& s, conv_algo_t algo, const void* x, const void* w
         g.sBias1 = 0;
         g.relu = 0;
         g.out_f32 = 1;
+        g.b_kmajor = 0;
         e = launch_gemm_nt(s.dtype, g, st);
         if (e != hipSuccess) return from_hip(e);
         e = launch_wino_output(s, M, b, (char*)y + (size_t)n0 * s.K * s.P * s.Q * s.esize(), 0, cnt, st);
         if (e != hipSuccess) return from_hip(e);
       }
       return CONV_OK;
+    }
+    case CONV_ALGO_IMPLICIT_PRECOMP_GEMM: {
+      if (!wpk) {
+        const hipError_t e = precomp_pack(s, w, ws, st);
+        if (e != hipSuccess) return from_hip(e);
+      }
+      return from_hip(precomp_main(s, x, wpk ? wpk : ws, b, y, st));
+    }
+    case CONV_ALGO_KN2ROW:
+    case CONV_ALGO_SMM: {
+      const bool kn = algo == CONV_ALGO_KN2ROW;
+      char* base = (char*)ws;
+      const void* pk = wpk;
+      if (!wpk) {
+        const hipError_t e = kn ? kn2row_pack(s, w, base, st) : smm_pack(s, w, base, st);
+        if (e != hipSuccess) return from_hip(e);
+        pk = base;
+        base += align256(kn ? kn2row_packed_bytes(s) : smm_packed_bytes(s));
+      }
+      return from_hip(kn ? kn2row_main(s, x, pk, b, y, base, st) : smm_main(s, x, pk, b, y, base, st));
     }
     default:
       return CONV_ERR_INVALID_ARG;
@@ -397,6 +433,9 @@ conv_status_t conv2d_pack_filters(const void* w, void* packed, const conv2d_desc
   const hipStream_t hs = (hipStream_t)stream;
   if (algo == CONV_ALGO_IMPLICIT_GEMM) return from_hip(convsel::launch_implicit_pack(s, w, packed, hs));
   if (algo == CONV_ALGO_WINOGRAD) return from_hip(convsel::launch_wino_filter(s, w, packed, hs));
+  if (algo == CONV_ALGO_IMPLICIT_PRECOMP_GEMM) return from_hip(convsel::precomp_pack(s, w, packed, hs));
+  if (algo == CONV_ALGO_KN2ROW) return from_hip(convsel::kn2row_pack(s, w, packed, hs));
+  if (algo == CONV_ALGO_SMM) return from_hip(convsel::smm_pack(s, w, packed, hs));
   return from_hip(convsel::launch_copy(w, packed, wbytes, hs));
 }
 
@@ -436,6 +475,15 @@ conv_status_t conv2d_describe(const conv2d_desc_t* desc, conv_algo_t algo, char*
           "images_per_batch=" + std::to_string(L.nb);
       break;
     }
+    case CONV_ALGO_IMPLICIT_PRECOMP_GEMM:
+      d = convsel::precomp_describe(s);
+      break;
+    case CONV_ALGO_KN2ROW:
+      d = convsel::kn2row_describe(s);
+      break;
+    case CONV_ALGO_SMM:
+      d = convsel::smm_describe(s);
+      break;
     default:
       return CONV_ERR_INVALID_ARG;
   }
@@ -507,6 +555,9 @@ const char* conv2d_algo_name(conv_algo_t algo) {
     case CONV_ALGO_IMPLICIT_GEMM: return "implicit_gemm";
     case CONV_ALGO_IM2COL_GEMM: return "im2col_gemm";
     case CONV_ALGO_WINOGRAD: return "winograd";
+    case CONV_ALGO_IMPLICIT_PRECOMP_GEMM: return "implicit_precomp_gemm";
+    case CONV_ALGO_KN2ROW: return "kn2row";
+    case CONV_ALGO_SMM: return "smm";
     default: return "unknown";
   }
 }
@@ -518,7 +569,9 @@ conv_status_t conv2d_algo_from_name(const char* name, conv_algo_t* algo) {
     conv_algo_t algo;
   } table[] = {{"default", CONV_ALGO_DEFAULT},         {"direct", CONV_ALGO_DIRECT},
                {"implicit_gemm", CONV_ALGO_IMPLICIT_GEMM}, {"im2col_gemm", CONV_ALGO_IM2COL_GEMM},
-               {"gemm", CONV_ALGO_IM2COL_GEMM},         {"winograd", CONV_ALGO_WINOGRAD}};
+               {"gemm", CONV_ALGO_IM2COL_GEMM},         {"winograd", CONV_ALGO_WINOGRAD},
+               {"implicit_precomp_gemm", CONV_ALGO_IMPLICIT_PRECOMP_GEMM},
+               {"kn2row", CONV_ALGO_KN2ROW},            {"smm", CONV_ALGO_SMM}};
   for (const auto& e : table)
     if (strcmp(name, e.name) == 0) {
       *algo = e.algo;

@@ -2,7 +2,10 @@
 //   C[b][i][j] = sum_k A[b][i][k] * B[b][j][k]  (+ bias[i], ReLU)
 // It is the multiply step of IM2COL + GEMM (A = filters, B = the column
 // matrix, C = one image's output planes) and the 16 elementwise-product
-// GEMMs of Winograd (A = U, B = V, C = M).
+// GEMMs of Winograd (A = U, B = V, C = M).  With `b_kmajor` set, B is read
+// as B[b][k][j] instead (column-contiguous: an NCHW image as channels x
+// pixels), which is the multiply step of KN2ROW; its tile is transposed on
+// the way into LDS.
 //
 // Tiling: 256 threads = 4 waves in a 2 x 2 grid; a BM x BN tile per
 // workgroup, (BM/2) x (BN/2) per wave as 32 x 32 MFMA blocks.  Each k-tile of
@@ -19,7 +22,7 @@ namespace {
 
 constexpr int kThreads = 256;
 
-template <typename T, int BM, int BN, bool VEC, bool OUT_F32>
+template <typename T, int BM, int BN, bool VEC, bool OUT_F32, bool BKM>
 __global__ __launch_bounds__(kThreads) void gemm_nt_kernel(GemmArgs g, int batch_base) {
   constexpr int UE = elem<T>::per16;  // elements per 16-byte unit
   constexpr int BK = 4 * UE;          // 32 bf16 or 16 fp32: two MFMA steps
@@ -82,9 +85,27 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_kernel(GemmArgs g, int batch
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
       const int id = tid + u * kThreads;
-      const int row = id / UPR, kc = (id % UPR) * UE;
-      const int gj = j0 + row, gk = k0 + kc;
-      rb[u] = load_unit(B, gj, gk, g.N, g.ldb);
+      if constexpr (BKM) {
+        // UE consecutive columns of reduction row kr.
+        const int kr = id / (BN / UE), jc = id % (BN / UE);
+        const int gk = k0 + kr, gj = j0 + jc * UE;
+        if (VEC && gk < g.Kred && gj + UE <= g.N) {
+          rb[u] = load16(B + gk * g.ldb + gj);
+        } else {
+          uint32_t e[UE];
+#pragma unroll
+          for (int i = 0; i < UE; ++i) {
+            const bool ok = gk < g.Kred && gj + i < g.N;
+            const uint32_t bits = load_bits(B + (ok ? gk * g.ldb + gj + i : 0));
+            e[i] = ok ? bits : 0u;
+          }
+          pack16<T>(rb[u], e);
+        }
+      } else {
+        const int row = id / UPR, kc = (id % UPR) * UE;
+        const int gj = j0 + row, gk = k0 + kc;
+        rb[u] = load_unit(B, gj, gk, g.N, g.ldb);
+      }
     }
   };
   auto stash = [&]() {
@@ -96,7 +117,13 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_kernel(GemmArgs g, int batch
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
       const int id = tid + u * kThreads;
-      store16(&Bs[(id / UPR) * KP + (id % UPR) * UE], rb[u]);
+      if constexpr (BKM) {
+        const int kr = id / (BN / UE), jc = id % (BN / UE);
+#pragma unroll
+        for (int i = 0; i < UE; ++i) Bs[(jc * UE + i) * KP + kr] = vec16_get<T>(rb[u], i);
+      } else {
+        store16(&Bs[(id / UPR) * KP + (id % UPR) * UE], rb[u]);
+      }
     }
   };
 
@@ -160,16 +187,16 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_kernel(GemmArgs g, int batch
   }
 }
 
-template <typename T, int BM, int BN, bool OUT_F32>
+template <typename T, int BM, int BN, bool OUT_F32, bool BKM>
 hipError_t launch_tile(const GemmArgs& g, bool vec, hipStream_t stream) {
   const dim3 block(kThreads);
   for (int base = 0; base < g.batch; base += 65535) {
     const int nb = g.batch - base < 65535 ? g.batch - base : 65535;
     const dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, nb);
     if (vec)
-      hipLaunchKernelGGL((gemm_nt_kernel<T, BM, BN, true, OUT_F32>), grid, block, 0, stream, g, base);
+      hipLaunchKernelGGL((gemm_nt_kernel<T, BM, BN, true, OUT_F32, BKM>), grid, block, 0, stream, g, base);
     else
-      hipLaunchKernelGGL((gemm_nt_kernel<T, BM, BN, false, OUT_F32>), grid, block, 0, stream, g, base);
+      hipLaunchKernelGGL((gemm_nt_kernel<T, BM, BN, false, OUT_F32, BKM>), grid, block, 0, stream, g, base);
   }
   return hipGetLastError();
 }
@@ -182,8 +209,12 @@ hipError_t launch_typed(const GemmArgs& g, hipStream_t stream) {
   const bool vec = aligned && g.lda % UE == 0 && g.ldb % UE == 0 && g.Kred % UE == 0 &&
                    g.sA0 % UE == 0 && g.sA1 % UE == 0 && g.sB0 % UE == 0 && g.sB1 % UE == 0;
   // Small M (filters per group) gets the 64-row tile so fewer MFMA rows idle.
-  if (g.M <= 64) return launch_tile<T, 64, 128, OUT_F32>(g, vec, stream);
-  return launch_tile<T, 128, 128, OUT_F32>(g, vec, stream);
+  if (g.b_kmajor) {
+    if (g.M <= 64) return launch_tile<T, 64, 128, OUT_F32, true>(g, vec, stream);
+    return launch_tile<T, 128, 128, OUT_F32, true>(g, vec, stream);
+  }
+  if (g.M <= 64) return launch_tile<T, 64, 128, OUT_F32, false>(g, vec, stream);
+  return launch_tile<T, 128, 128, OUT_F32, false>(g, vec, stream);
 }
 
 }  // namespace

@@ -24,7 +24,9 @@ struct Shape {
 
 // Batched "NT" GEMM on MFMA:  C[b][i][j] = sum_k A[b][i][k] * B[b][j][k]
 // (+ bias[b1*sBias1 + i], then ReLU), i < M, j < N, k < Kred.  Both operands
-// are reduction-contiguous (row-major with leading dimensions lda / ldb).
+// are reduction-contiguous (row-major with leading dimensions lda / ldb),
+// unless b_kmajor is set: then B is read as B[b][k][j] (leading dimension
+// ldb along k).
 // Batch b is split as b0 = b / bdiv, b1 = b % bdiv and every operand is
 // offset by b0*s?0 + b1*s?1 elements.  C is stored in the data type, or in
 // fp32 when out_f32 is set.
@@ -40,6 +42,7 @@ struct GemmArgs {
   int64_t sBias1;
   int relu;
   int out_f32;
+  int b_kmajor;
 };
 
 hipError_t launch_gemm_nt(int dtype, const GemmArgs& g, hipStream_t stream);
@@ -88,6 +91,34 @@ hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, co
                                 hipStream_t stream);
 std::string implicit_gemm_describe(const Shape& s);
 
+
+// Implicit precomputed-index GEMM: the package holds the zero-padded
+// filters and the reduction and pixel index tables; no other workspace.
+bool precomp_applies(const Shape& s);
+size_t precomp_packed_bytes(const Shape& s);
+hipError_t precomp_pack(const Shape& s, const void* w, void* pkg, hipStream_t stream);
+hipError_t precomp_main(const Shape& s, const void* x, const void* pkg, const void* b, void* y, hipStream_t stream);
+std::string precomp_describe(const Shape& s);
+
+// KN2ROW: the package is the tap-stacked filter matrix; the workspace holds
+// the fp32 partial planes Z of a batch of images (kn2row_z_bytes).
+bool kn2row_applies(const Shape& s);
+size_t kn2row_packed_bytes(const Shape& s);
+size_t kn2row_z_bytes(const Shape& s);
+hipError_t kn2row_pack(const Shape& s, const void* w, void* wst, hipStream_t stream);
+hipError_t kn2row_main(const Shape& s, const void* x, const void* wst, const void* b, void* y, void* z,
+                       hipStream_t stream);
+std::string kn2row_describe(const Shape& s);
+
+// SMM: the package holds the filters in blocks of output channels; the
+// workspace holds the zero-packed input of a batch of images.
+bool smm_applies(const Shape& s);
+size_t smm_packed_bytes(const Shape& s);
+size_t smm_zero_pack_bytes(const Shape& s);
+hipError_t smm_pack(const Shape& s, const void* w, void* wp, hipStream_t stream);
+hipError_t smm_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* zp,
+                    hipStream_t stream);
+std::string smm_describe(const Shape& s);
 
 // Column matrix [nb][G][P*Q][Cg*R*S] of images n0 .. n0+nb-1.
 hipError_t launch_im2col(const Shape& s, const void* x, void* col, int64_t n0, int64_t nb,

@@ -22,8 +22,9 @@ from torch import nn
 from . import _lib
 from .conv import conv2d, prepare, pack_filters, conv2d_prepacked, resolve_algo
 
-ALGO_CHOICES = ("default", "direct", "implicit_gemm", "im2col_gemm", "gemm", "winograd", "torch")
-CONCRETE_ALGOS = ("direct", "implicit_gemm", "im2col_gemm", "winograd")
+ALGO_CHOICES = ("default", "direct", "implicit_gemm", "implicit_precomp_gemm", "im2col_gemm", "gemm", "kn2row",
+                "smm", "winograd", "torch")
+CONCRETE_ALGOS = ("direct", "implicit_gemm", "implicit_precomp_gemm", "im2col_gemm", "kn2row", "smm", "winograd")
 
 
 def _canonical(name):

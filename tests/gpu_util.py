@@ -4,13 +4,13 @@ import torch
 
 import oracle
 
-ALGOS = ("direct", "implicit_gemm", "im2col_gemm", "winograd")
+ALGOS = ("direct", "implicit_gemm", "implicit_precomp_gemm", "im2col_gemm", "kn2row", "smm", "winograd")
 
 
 def tolerance(dtype, algo):
     """Max relative error allowed against the fp64 oracle: 1e-4 for fp32
-    direct / implicit GEMM / IM2COL+GEMM, 1e-3 for fp32 Winograd, 2e-2 for
-    bf16 data (any algorithm)."""
+    direct / implicit GEMM (both variants) / IM2COL+GEMM / KN2ROW / SMM, 1e-3
+    for fp32 Winograd, 2e-2 for bf16 data (any algorithm)."""
     if dtype in ("bf16", torch.bfloat16):
         return 2e-2
     return 1e-3 if algo == "winograd" else 1e-4

@@ -39,7 +39,7 @@ def test_algo_names_round_trip():
         assert _lib.algo_name(v) == name
     assert _lib.algo_id("gemm") == _lib.ALGOS["im2col_gemm"]
     with pytest.raises(ValueError):
-        _lib.algo_id("smm")
+        _lib.algo_id("fft")
     assert _lib.algo_name(99) == "unknown"
     assert _lib.status_string(0) == "ok" and _lib.status_string(42) == "unknown"
 
@@ -169,6 +169,64 @@ def test_workspace_sizes():
     assert "implicit_rows_kernel" not in _lib.describe(stem32, "implicit_gemm")
     s3 = _lib.make_desc(32, 3, 224, 224, 64, 3, 3, 2, 1, 1, 1, "bf16")
     assert "implicit_rows_kernel" not in _lib.describe(s3, "implicit_gemm")
+
+
+def _a256(v):
+    return (v + 255) // 256 * 256
+
+
+def test_precomp_kn2row_smm_workspaces():
+    # Implicit precomputed-index GEMM: package = filters [G][K padded to the
+    # tile][C/G*R*S padded to 32 (bf16) or 16 (fp32)], then one 8-byte entry
+    # per reduction index and per output pixel of a launch; nothing else.
+    d = _lib.make_desc(4, 6, 10, 12, 8, 3, 3, 2, 1, 1, 2, "bf16")
+    P, Q = _lib.output_shape(d)
+    krp = 32                                  # 3*9 = 27 -> 32
+    pk = _a256(_a256(2 * 64 * krp * 2) + krp * 8) + 4 * P * Q * 8
+    assert _lib.packed_filter_bytes(d, "implicit_precomp_gemm") == pk
+    assert _lib.workspace_bytes(d, "implicit_precomp_gemm") == pk
+    assert _lib.prepacked_workspace_bytes(d, "implicit_precomp_gemm") == 0
+    assert "implicit_precomp_kernel<bf16,64>" in _lib.describe(d, "implicit_precomp_gemm")
+    f = _lib.make_desc(2, 16, 9, 9, 200, 5, 5, 1, 2, 2, 1, "f32")
+    P, Q = _lib.output_shape(f)
+    krp = 400                                 # 16*25 = 400, a multiple of 16
+    pk = _a256(_a256(256 * krp * 4) + krp * 8) + 2 * P * Q * 8
+    assert _lib.workspace_bytes(f, "implicit_precomp_gemm") == pk
+    assert "implicit_precomp_kernel<f32,128>" in _lib.describe(f, "implicit_precomp_gemm")
+    # 16-bit coordinate packing: very wide planes are not supported.
+    wide = _lib.make_desc(1, 1, 4, 16384, 4, 1, 3, 1, 1, 1, 1, "f32")
+    assert _lib.check(wide, "implicit_precomp_gemm") == _lib.CONV_ERR_UNSUPPORTED
+    assert _lib.check(wide, "direct") == _lib.CONV_OK
+    # KN2ROW: tap-stacked filters (same size as the filters) + fp32 partial
+    # planes R*S*K*H*W per image.
+    d = _lib.make_desc(4, 6, 10, 12, 8, 3, 3, 2, 1, 1, 2, "bf16")
+    wbytes = 8 * 3 * 9 * 2
+    assert _lib.packed_filter_bytes(d, "kn2row") == wbytes
+    assert _lib.workspace_bytes(d, "kn2row") == _a256(wbytes) + 4 * 9 * 8 * 10 * 12 * 4
+    assert _lib.prepacked_workspace_bytes(d, "kn2row") == 4 * 9 * 8 * 10 * 12 * 4
+    assert "kn2row_shift_add_kernel" in _lib.describe(d, "kn2row")
+    big = _lib.make_desc(128, 512, 112, 112, 256, 3, 3, 1, 1, 1, 1, "bf16")
+    per_img = 9 * 256 * 112 * 112 * 4
+    assert _lib.prepacked_workspace_bytes(big, "kn2row") == (1 << 30) // per_img * per_img
+    # SMM: filters in blocks of 8 (K/G < 16) or 16 output channels + the
+    # zero-padded input, ((P-1)*sh + (R-1)*dh + 1) x ((Q-1)*sw + (S-1)*dw + 1)
+    # per plane.
+    P, Q = _lib.output_shape(d)
+    hz, wz = (P - 1) * 2 + 3, (Q - 1) * 2 + 3
+    pk = 2 * 8 * 3 * 9 * 2                    # 2 groups x one block of 8 (4 real rows)
+    assert _lib.packed_filter_bytes(d, "smm") == pk
+    assert _lib.workspace_bytes(d, "smm") == _a256(pk) + 4 * 6 * hz * wz * 2
+    assert "smm_kernel<8>" in _lib.describe(d, "smm")
+    e = _lib.make_desc(2, 8, 9, 9, 40, 3, 3, 1, 1, 1, 1, "f32")
+    assert _lib.packed_filter_bytes(e, "smm") == 48 * 8 * 9 * 4
+    assert "smm_kernel<16>" in _lib.describe(e, "smm")
+    # every new algorithm runs every valid shape of the support sweep
+    for kw in [dict(r=5), dict(stride=2), dict(dilation=2), dict(groups=2), dict(r=1)]:
+        args = dict(r=3, stride=1, dilation=1, groups=1)
+        args.update(kw)
+        dd = _lib.make_desc(2, 8, 9, 9, 8, args["r"], args["r"], args["stride"], 1, args["dilation"], args["groups"])
+        for a in ("implicit_precomp_gemm", "kn2row", "smm"):
+            assert _lib.check(dd, a) == _lib.CONV_OK
 
 
 def test_default_rule():

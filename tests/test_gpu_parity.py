@@ -389,6 +389,9 @@ GUARDED = [
     (3, 3, 29, 23, 64, 7, 2, 3, "bf16", ("implicit_gemm",)),
     (2, 96, 9, 11, 40, 1, 1, 0, "f32", ("implicit_gemm", "direct")),
     (2, 64, 10, 10, 64, 3, 1, 1, "f32", ("implicit_gemm", "winograd")),
+    (2, 40, 13, 11, 70, 3, 2, 1, "f32", ("implicit_precomp_gemm", "kn2row", "smm")),
+    (3, 24, 9, 17, 130, 5, 1, 2, "bf16", ("implicit_precomp_gemm", "kn2row", "smm")),
+    (1, 3, 33, 33, 64, 7, 2, 3, "bf16", ("implicit_precomp_gemm", "kn2row", "smm")),
 ]
 
 

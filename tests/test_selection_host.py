@@ -108,7 +108,7 @@ def test_selector_errors():
     with pytest.raises(ValueError):
         cs.swap_conv2d(ConvNet(), ["direct"])                 # list length mismatch
     with pytest.raises(ValueError):
-        cs.swap_conv2d(ConvNet(), "smm")                      # unknown name
+        cs.swap_conv2d(ConvNet(), "fft")                      # unknown name
     with pytest.raises(ValueError):
         cs.swap_conv2d(Deep(), "winograd")                    # 5x5 stem cannot use F(2x2,3x3)
     with pytest.raises(ValueError):
