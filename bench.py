@@ -203,17 +203,24 @@ def cpu_baseline(workload, budget_s=20.0):
                       "with OpenMP" % (len(layers), workload, images, flops / 1e9, t_total)}
 
 
-def sweep(path, steps):
-    """Every algorithm on every unique layer of all five workloads: JSONL rows."""
+def sweep(path, steps, fit_seeds=0):
+    """Every algorithm on every unique layer of all five workloads (or, with
+    fit_seeds = S > 0, of the fitting set: the 20-layer random chain at seeds
+    1..S and the mixed independent layers at seeds 0..S-1): JSONL rows."""
     import torch
     import paper_2410_08300_amd as cs
     from paper_2410_08300_amd import workloads as W
 
     dev = torch.device("cuda:0")
+    if fit_seeds > 0:
+        sets = [("random20/s%d" % sd, W.random20(128, sd)) for sd in range(1, fit_seeds + 1)]
+        sets += [("mixed/s%d" % sd, W.mixed(sd)) for sd in range(fit_seeds)]
+    else:
+        sets = [(wl, W.layers(wl)) for wl in W.WORKLOADS]
     with open(path, "w") as f:
-        for wi, wl in enumerate(W.WORKLOADS):
-            for li, (L, count) in enumerate(W.unique_layers(W.layers(wl))):
-                x, w, b = W.make_tensors(L, (wi, li, 4), device=dev)
+        for wi, (wl, wl_layers) in enumerate(sets):
+            for li, (L, count) in enumerate(W.unique_layers(wl_layers)):
+                x, w, b = W.make_tensors(L, (wi + (100 if fit_seeds else 0), li, 4), device=dev)
                 for algo in cs.supported_algos(x, w, b, L.stride, L.pad, L.dilation, L.groups, L.relu):
                     ms = cs.time_conv(x, w, b, L.stride, L.pad, L.dilation, L.groups, algo, L.relu,
                                       warmup=2, reps=steps)
@@ -245,6 +252,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--sweep", default=None, help="write per-layer, per-algorithm timings to this JSONL file")
+    ap.add_argument("--sweep-fit-seeds", type=int, default=0, metavar="S",
+                    help="with --sweep: time the algorithm-choice fitting set (random chains at seeds 1..S, "
+                         "mixed layers at seeds 0..S-1) instead of the five workloads")
     ap.add_argument("--table", default=None,
                     help="JSON {layer name: algorithm} to use instead of measuring (e.g. a saved --save-table)")
     ap.add_argument("--save-table", default=None, help="write the per-layer algorithm table to this JSON file")
@@ -265,7 +275,7 @@ def main():
     torch.cuda.set_device(dev)
 
     if args.sweep:
-        sweep(args.sweep, max(args.steps, 3))
+        sweep(args.sweep, max(args.steps, 3), args.sweep_fit_seeds)
         return
 
     wl = args.workload
@@ -411,6 +421,16 @@ def main():
                                "tflops": f3 / (t3 * 1e-3) / 1e12, "frac_peak": f3 / (t3 * 1e-3) / 1e12 / peak}
     extra["sum_layer_ms"] = sum(layer_ms)
     extra["algos"] = {a: v[2] for a, v in by_algo.items()}
+    # Whole network with the per-layer selection versus every single-algorithm
+    # network, all from the selection's own per-layer timings (a network is
+    # listed only if its algorithm runs every layer).
+    if all(p["timings"] for p in plan):
+        import paper_2410_08300_amd as cs
+        nets = {"selected": sum(min(p["timings"].values()) for p in plan)}
+        for a in cs.CONCRETE_ALGOS:
+            if all(a in p["timings"] for p in plan):
+                nets[a] = sum(p["timings"][a] for p in plan)
+        extra["network_ms_from_selection_timings"] = nets
     extra["steps"] = {m: {"ms_per_step": t, "tflops": total_flops / (t * 1e-3) / 1e12} for m, t in modes.items()}
 
     if args.calibrate_copy > 0:

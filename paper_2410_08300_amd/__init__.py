@@ -1,5 +1,6 @@
 """Forward 2-D convolution for AMD MI355X (gfx950) with per-layer choice of
-algorithm -- direct, implicit GEMM, IM2COL + GEMM and Winograd F(2x2,3x3) --
+algorithm -- direct, implicit GEMM, implicit precomputed-index GEMM, IM2COL +
+GEMM, KN2ROW, SMM and Winograd F(2x2,3x3) --
 after the framework of "A Framework to Enable Algorithmic Design Choice
 Exploration in DNNs" (arXiv 2410.08300).
 
@@ -10,7 +11,9 @@ streams.
 from ._lib import Conv2dError, ALGOS
 from .conv import (conv2d, conv2d_prepacked, pack_filters, describe, im2col, winograd_filter_transform,
                    winograd_input_transform)
-from .selection import AlgoTable, Conv2dSwap, swap_conv2d, select_fastest, tune, time_conv, supported_algos
+from .selection import (AlgoTable, Conv2dSwap, swap_conv2d, select_fastest, tune, time_conv, supported_algos,
+                        CONCRETE_ALGOS)
 
 __all__ = ["Conv2dError", "ALGOS", "conv2d", "conv2d_prepacked", "pack_filters", "describe", "im2col", "winograd_filter_transform", "winograd_input_transform",
-           "AlgoTable", "Conv2dSwap", "swap_conv2d", "select_fastest", "tune", "time_conv", "supported_algos"]
+           "AlgoTable", "Conv2dSwap", "swap_conv2d", "select_fastest", "tune", "time_conv", "supported_algos",
+           "CONCRETE_ALGOS"]

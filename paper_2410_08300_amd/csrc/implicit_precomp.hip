@@ -238,6 +238,7 @@ bool make_pc_plan(const Shape& s, PcPlan& pl) {
   pl.BM = s.Kg <= 64 ? 64 : 128;
   pl.ktiles = (int)((s.Kg + pl.BM - 1) / pl.BM);
   pl.Kpad = pl.ktiles * pl.BM;
+  if ((int64_t)pl.ktiles * s.G > 65535) return false;  // grid rows
   pl.wp_bytes = (size_t)s.G * pl.Kpad * pl.KRp * s.esize();
   if (pl.wp_bytes > (size_t)kMaxLaunchBytes) return false;
   pl.ktab_off = align256(pl.wp_bytes);

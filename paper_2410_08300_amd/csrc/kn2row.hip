@@ -91,7 +91,7 @@ int64_t z_batch(const Shape& s, size_t* bytes) {
 bool kn2row_applies(const Shape& s) {
   // One image's partial planes must be indexable in 32 bits per group GEMM.
   const int64_t rows = s.R * s.S * s.Kg;
-  return rows < ((int64_t)1 << 31) / (s.H * s.W);
+  return rows < ((int64_t)1 << 31) / (s.H * s.W) && (rows + 63) / 64 <= 65535;  // GEMM grid rows
 }
 
 size_t kn2row_packed_bytes(const Shape& s) { return (size_t)s.K * s.Cg * s.R * s.S * s.esize(); }

@@ -171,6 +171,49 @@ def random20(n=128, seed=0):
     return L
 
 
+def mixed(seed=0, count=20):
+    """Seeded independent layers of mixed kind, for fitting an algorithm-choice
+    rule (not a network: each layer stands alone).  Per layer, drawn in this
+    order: dtype (bf16 or fp32), kind (dense 70%, depthwise 20%, grouped 10%),
+    C and K from {3, 16, 32, 64, 96, 128, 256, 512, 1024} (depthwise: K = C =
+    groups; grouped: groups from {2, 4, 32} dividing both), kernel from
+    {1, 3, 5, 7} (depthwise {3, 5}), stride from {1, 2}, dilation 1 (2 with
+    probability 0.1), H = W from {7, 14, 28, 56, 112, 224}, N from
+    {1, 8, 32, 64, 128}, bias and ReLU each with probability 0.5; pad =
+    dilation * (R // 2).  A draw is rejected (and redrawn) when the output is
+    empty, the input exceeds 2^28 elements, or the layer exceeds 1 TFLOP."""
+    rng = np.random.default_rng(seed_for(77, seed))
+    chans = [3, 16, 32, 64, 96, 128, 256, 512, 1024]
+    out = []
+    while len(out) < count:
+        dtype = "bf16" if rng.random() < 0.5 else "f32"
+        u = rng.random()
+        kind = "dense" if u < 0.7 else ("dw" if u < 0.9 else "grouped")
+        c = int(rng.choice(chans))
+        k = int(rng.choice(chans))
+        g = 1
+        if kind == "dw":
+            k, g = c, c
+        elif kind == "grouped":
+            g = int(rng.choice([2, 4, 32]))
+        r = int(rng.choice([3, 5])) if kind == "dw" else int(rng.choice([1, 3, 5, 7]))
+        st = int(rng.choice([1, 2]))
+        dl = 2 if rng.random() < 0.1 else 1
+        hw = int(rng.choice([7, 14, 28, 56, 112, 224]))
+        n = int(rng.choice([1, 8, 32, 64, 128]))
+        bias = bool(rng.random() < 0.5)
+        relu = bool(rng.random() < 0.5)
+        if c % g or k % g:
+            continue
+        pad = dl * (r // 2)
+        L = Layer("mix%d_%d" % (seed, len(out)), n, c, hw, hw, k, r, r, st, pad, dl, g, bias=bias, relu=relu,
+                  dtype=dtype)
+        if L.p < 1 or L.q < 1 or n * c * hw * hw > (1 << 28) or L.flops > 1e12:
+            continue
+        out.append(L)
+    return out
+
+
 def layers(workload, n=None, seed=0):
     if workload == "toy":
         return toy()
