@@ -386,8 +386,17 @@ def main():
         ks = main_kernel(p["describe"])
         if len(ks) == 1:
             share[ks[0]] = share.get(ks[0], 0.0) + ms
-    dom = max(share, key=share.get)
-    single = [(p, ms) for p, ms in zip(plan, lms_pk) if main_kernel(p["describe"]) == [dom]]
+    if share:
+        dom = max(share, key=share.get)
+        single = [(p, ms) for p, ms in zip(plan, lms_pk) if main_kernel(p["describe"]) == [dom]]
+    else:
+        # No layer runs a single main kernel (every call launches several,
+        # e.g. Winograd's transforms and products): price whole calls of the
+        # algorithm with the largest share instead.
+        for p, ms in zip(plan, lms_pk):
+            share[p["algo"] + " (whole call)"] = share.get(p["algo"] + " (whole call)", 0.0) + ms
+        dom = max(share, key=share.get)
+        single = [(p, ms) for p, ms in zip(plan, lms_pk) if p["algo"] + " (whole call)" == dom]
     dom_ms = sum(ms for _, ms in single)
     dom_flops = sum(p["layer"].flops for p, _ in single)
     dom_bytes = sum(p["layer"].compulsory_bytes() for p, _ in single)

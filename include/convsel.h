@@ -127,8 +127,14 @@ conv_status_t conv2d_check(const conv2d_desc_t* desc, conv_algo_t algo);
  * Same errors as conv2d_check. */
 conv_status_t conv2d_workspace_bytes(const conv2d_desc_t* desc, conv_algo_t algo, size_t* bytes);
 
-/* The concrete algorithm CONV_ALGO_DEFAULT resolves to for this layer (a fixed
- * rule on the layer shape; the paper's "default" selector, Sec. IV).  Returns
+/* The concrete algorithm CONV_ALGO_DEFAULT resolves to for this layer: the
+ * library's prediction of the fastest algorithm without timing anything (the
+ * "default" selector of Sec. IV, playing the part of the heuristic "guess"
+ * of Sec. V-B).  A decision tree over shape features (dtype, depthwise,
+ * taps, stride, log2 of C/groups, K/groups, N*P*Q and P*Q, Winograd
+ * eligibility, dilation, grouping), fitted offline to measured timings of
+ * every algorithm on random layers, ranks the algorithms; the first one
+ * that supports the layer is returned.  Host only, deterministic.  Returns
  * CONV_ALGO_DEFAULT itself only for an invalid descriptor. */
 conv_algo_t conv2d_default_algo(const conv2d_desc_t* desc);
 

@@ -11,9 +11,9 @@ streams.
 from ._lib import Conv2dError, ALGOS
 from .conv import (conv2d, conv2d_prepacked, pack_filters, describe, im2col, winograd_filter_transform,
                    winograd_input_transform)
-from .selection import (AlgoTable, Conv2dSwap, swap_conv2d, select_fastest, tune, time_conv, supported_algos,
+from .selection import (AlgoTable, AlgoCache, Conv2dSwap, swap_conv2d, select_fastest, tune, time_conv, supported_algos,
                         CONCRETE_ALGOS)
 
 __all__ = ["Conv2dError", "ALGOS", "conv2d", "conv2d_prepacked", "pack_filters", "describe", "im2col", "winograd_filter_transform", "winograd_input_transform",
-           "AlgoTable", "Conv2dSwap", "swap_conv2d", "select_fastest", "tune", "time_conv", "supported_algos",
+           "AlgoTable", "AlgoCache", "Conv2dSwap", "swap_conv2d", "select_fastest", "tune", "time_conv", "supported_algos",
            "CONCRETE_ALGOS"]

@@ -2,6 +2,7 @@
 // validation, algorithm support, workspace sizes, the default-algorithm rule
 // and dispatch to the kernel launchers.  All checks run on the host before
 // the first HIP call.
+#include <math.h>
 #include <mutex>
 #include <stdio.h>
 #include <string.h>
@@ -81,11 +82,42 @@ conv_status_t support(const Shape& s, conv_algo_t algo) {
   }
 }
 
+// The default choice: a decision tree over shape features, fitted offline to
+// measured per-layer timings of every algorithm (the heuristic "guess" of the
+// paper's comparison, Sec. V-B); a leaf ranks the algorithms and the first
+// one that supports the layer is taken.
+struct GuessNode {
+  int feature;
+  double threshold;
+  int left, right, leaf;
+};
+#include "guess_tree.inc"
+
+// Features in the fitted order: bf16, depthwise, taps, stride, log2(C/G),
+// log2(K/G), log2(N*P*Q), log2(P*Q), Winograd-eligible, dilated, grouped.
+void guess_features(const Shape& s, double f[11]) {
+  f[0] = s.dtype == convsel::DT_BF16 ? 1.0 : 0.0;
+  f[1] = s.Cg == 1 ? 1.0 : 0.0;
+  f[2] = (double)(s.R * s.S);
+  f[3] = (double)(s.sh > s.sw ? s.sh : s.sw);
+  f[4] = log2((double)s.Cg);
+  f[5] = log2((double)s.Kg);
+  f[6] = log2((double)(s.N > 0 ? s.N : 1) * (double)(s.P * s.Q));
+  f[7] = log2((double)(s.P * s.Q));
+  f[8] = winograd_ok(s) ? 1.0 : 0.0;
+  f[9] = (s.dh > 1 || s.dw > 1) ? 1.0 : 0.0;
+  f[10] = (s.G > 1 && s.Cg > 1) ? 1.0 : 0.0;
+}
+
 conv_algo_t default_rule(const Shape& s) {
-  // One input channel per group (depthwise): the HBM-bound direct kernel.
-  if (s.Cg == 1) return CONV_ALGO_DIRECT;
-  if (convsel::implicit_gemm_fits(s)) return CONV_ALGO_IMPLICIT_GEMM;
-  return CONV_ALGO_IM2COL_GEMM;
+  double f[11];
+  guess_features(s, f);
+  int i = 0;
+  while (kGuessNodes[i].feature >= 0)
+    i = f[kGuessNodes[i].feature] <= kGuessNodes[i].threshold ? kGuessNodes[i].left : kGuessNodes[i].right;
+  for (int a : kGuessRank[kGuessNodes[i].leaf])
+    if (support(s, (conv_algo_t)a) == CONV_OK) return (conv_algo_t)a;
+  return CONV_ALGO_DIRECT;  // defined for every valid layer
 }
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }

@@ -12,6 +12,13 @@
   is; "default" lets the library pick per call.
 * ``select_fastest`` / ``tune``: measured selection -- time every algorithm
   that supports a layer and record the fastest in the table.
+* ``AlgoCache``: measured choices keyed by layer shape and persisted as JSON,
+  so each shape is timed once per device and deployment; passed as the
+  selector of ``swap_conv2d`` it makes every layer "cached": the first call
+  of a shape measures, later calls (and later processes that load the file)
+  reuse the pick.  "default" is the library's own prediction without any
+  timing (a decision tree fitted to measured sweeps, see
+  ``conv2d_default_algo``).
 """
 import collections
 import json
@@ -23,7 +30,7 @@ from . import _lib
 from .conv import conv2d, prepare, pack_filters, conv2d_prepacked, resolve_algo
 
 ALGO_CHOICES = ("default", "direct", "implicit_gemm", "implicit_precomp_gemm", "im2col_gemm", "gemm", "kn2row",
-                "smm", "winograd", "torch")
+                "smm", "winograd", "torch", "cached")
 CONCRETE_ALGOS = ("direct", "implicit_gemm", "implicit_precomp_gemm", "im2col_gemm", "kn2row", "smm", "winograd")
 
 
@@ -33,8 +40,91 @@ def _canonical(name):
     return "im2col_gemm" if name == "gemm" else name
 
 
+def _pair(v):
+    return tuple(v) if isinstance(v, (tuple, list)) else (v, v)
+
+
+class AlgoCache:
+    """Measured algorithm choices keyed by layer shape, persisted as JSON.
+
+    A key holds everything the choice depends on: dtype, input N x C x H x W,
+    filter K x C/groups x R x S, stride, padding, dilation, groups, bias and
+    fused ReLU.  ``select`` returns the recorded algorithm of a shape, or
+    times every supported algorithm (``select_fastest``) and records the
+    fastest.  The file also names the device the timings were taken on.
+    """
+    VERSION = 1
+
+    def __init__(self, device=None):
+        self.device = device
+        self.entries = collections.OrderedDict()   # key -> {"algo": name, "ms": {algo: ms}}
+
+    @staticmethod
+    def key(x_shape, w_shape, stride=1, padding=0, dilation=1, groups=1, dtype="f32", bias=False, relu=False):
+        n, c, h, w = (int(v) for v in x_shape)
+        k, cg, r, s = (int(v) for v in w_shape)
+        if c != cg * groups:
+            raise ValueError("filter channels %d x groups %d != input channels %d" % (cg, groups, c))
+        sh, sw = _pair(stride)
+        ph, pw = _pair(padding)
+        dh, dw = _pair(dilation)
+        return "%s n%d c%d h%d w%d k%d r%d s%d st%dx%d pad%dx%d dil%dx%d g%d bias%d relu%d" % (
+            dtype, n, c, h, w, k, r, s, sh, sw, ph, pw, dh, dw, groups, int(bool(bias)), int(bool(relu)))
+
+    @staticmethod
+    def key_for(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, relu=False):
+        dt = {torch.float32: "f32", torch.bfloat16: "bf16"}.get(x.dtype, str(x.dtype))
+        return AlgoCache.key(x.shape, w.shape, stride, padding, dilation, groups, dt, b is not None, relu)
+
+    def __len__(self):
+        return len(self.entries)
+
+    def lookup(self, key):
+        e = self.entries.get(key)
+        return None if e is None else e["algo"]
+
+    def record(self, key, algo, timings=None):
+        algo = _canonical(algo)
+        if algo not in CONCRETE_ALGOS:
+            raise ValueError("a cache entry must name a concrete algorithm, not %r" % algo)
+        self.entries[key] = {"algo": algo, "ms": dict(timings or {})}
+
+    def select(self, x, w, b=None, stride=1, padding=0, dilation=1, groups=1, relu=False, warmup=2, reps=5):
+        key = self.key_for(x, w, b, stride, padding, dilation, groups, relu)
+        algo = self.lookup(key)
+        if algo is None:
+            algo, timings = select_fastest(x, w, b, stride, padding, dilation, groups, relu, warmup=warmup, reps=reps)
+            self.record(key, algo, timings)
+        return algo
+
+    def to_json(self):
+        return json.dumps({"version": self.VERSION, "device": self.device, "entries": self.entries}, indent=1)
+
+    @classmethod
+    def from_json(cls, text):
+        d = json.loads(text)
+        if d.get("version") != cls.VERSION:
+            raise ValueError("unsupported algorithm cache version %r" % d.get("version"))
+        c = cls(d.get("device"))
+        for k, e in d["entries"].items():
+            c.record(k, e["algo"], e.get("ms"))
+        return c
+
+    def save(self, path):
+        with open(path, "w") as f:
+            f.write(self.to_json())
+
+    @classmethod
+    def load(cls, path):
+        with open(path) as f:
+            return cls.from_json(f.read())
+
+
 class AlgoTable(collections.OrderedDict):
-    """qualified module name -> algorithm name."""
+    """qualified module name -> algorithm name.  Entries "cached" resolve per
+    call through ``cache`` (an AlgoCache)."""
+
+    cache = None
 
     def set(self, name, algo):
         self[name] = _canonical(algo)
@@ -71,7 +161,7 @@ def _padding_pair(m):
 
 def _static_check(name, m, algo):
     """Reject, at swap time, picks that cannot run whatever the input shape."""
-    if algo in ("torch", "default"):
+    if algo in ("torch", "default", "cached"):
         return
     if m.padding_mode != "zeros":
         raise ValueError("%s: padding_mode=%r is not supported (zero padding only)" % (name, m.padding_mode))
@@ -115,6 +205,12 @@ class Conv2dSwap(nn.Module):
         if algo == "torch":
             return self._torch_conv(x)
         w = self.weight
+        if algo == "cached":
+            if self.table.cache is None:
+                raise ValueError("%s: the table has no AlgoCache for its 'cached' entries" % self.name)
+            with torch.no_grad():
+                algo = self.table.cache.select(x, w.detach(), None if self.bias is None else self.bias.detach(),
+                                               self.stride, self.padding, self.dilation, self.groups)
         if not self.cache_filters or (torch.is_grad_enabled() and w.requires_grad) or not x.is_cuda:
             return conv2d(x, w, self.bias, self.stride, self.padding, self.dilation, self.groups, algo=algo)
         algo = resolve_algo(x, w, self.bias, self.stride, self.padding, self.dilation, self.groups, algo)
@@ -152,9 +248,13 @@ def swap_conv2d(model, selector="default"):
         raise ValueError("selector list has %d entries but the model has %d Conv2d modules"
                          % (len(selector), len(all_convs)))
     table = AlgoTable()
+    if isinstance(selector, AlgoCache):
+        table.cache = selector
     for idx, (name, m) in enumerate(all_convs):
         base = m._torch_conv if isinstance(m, Conv2dSwap) else m
-        if isinstance(selector, str):
+        if isinstance(selector, AlgoCache):
+            algo = "cached"
+        elif isinstance(selector, str):
             algo = selector
         elif isinstance(selector, (list, tuple)):
             algo = selector[idx]
@@ -163,7 +263,7 @@ def swap_conv2d(model, selector="default"):
         elif callable(selector):
             algo = selector(base)
         else:
-            raise ValueError("selector must be a name, a list of names, a callable or a table")
+            raise ValueError("selector must be a name, a list of names, a callable, a table or an AlgoCache")
         algo = _canonical(algo)
         _static_check(name, base, algo)
         table[name] = algo
@@ -243,10 +343,12 @@ def select_fastest(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, relu
     return best, timings
 
 
-def tune(model, example_input, table=None, warmup=2, reps=5):
+def tune(model, example_input, table=None, warmup=2, reps=5, cache=None):
     """Measured per-layer selection on a swapped model: capture every
     Conv2dSwap's input with one forward pass, time each supported algorithm
-    on it and write the fastest into the table.  Returns the table."""
+    on it and write the fastest into the table.  With ``cache`` (an
+    AlgoCache) shapes already recorded are not timed again, and new ones are
+    recorded.  Returns the table."""
     mods = [(n, m) for n, m in model.named_modules() if isinstance(m, Conv2dSwap)]
     if table is None:
         table = mods[0][1].table if mods else AlgoTable()
@@ -263,7 +365,11 @@ def tune(model, example_input, table=None, warmup=2, reps=5):
         for n, m in mods:
             if n not in captured or table.get_algo(n) == "torch":
                 continue
-            best, _ = select_fastest(captured[n], m.weight, m.bias, m.stride, m.padding, m.dilation, m.groups,
-                                     warmup=warmup, reps=reps)
+            if cache is not None:
+                best = cache.select(captured[n], m.weight, m.bias, m.stride, m.padding, m.dilation, m.groups,
+                                    warmup=warmup, reps=reps)
+            else:
+                best, _ = select_fastest(captured[n], m.weight, m.bias, m.stride, m.padding, m.dilation,
+                                         m.groups, warmup=warmup, reps=reps)
             table[n] = best
     return table

@@ -230,8 +230,15 @@ def test_precomp_kn2row_smm_workspaces():
 
 
 def test_default_rule():
+    # depthwise fp32: the direct kernel; a ResNet-50 stage-1 3x3 in bf16:
+    # implicit GEMM; a VGG-16 3x3 in fp32 at 112x112: Winograd.
     assert _lib.default_algo(_lib.make_desc(2, 32, 16, 16, 32, 3, 3, 1, 1, 1, 32)) == "direct"
-    assert _lib.default_algo(_lib.make_desc(2, 32, 16, 16, 64, 3, 3, 1, 1, 1, 1)) == "implicit_gemm"
+    assert _lib.default_algo(_lib.make_desc(32, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, "bf16")) == "implicit_gemm"
+    assert _lib.default_algo(_lib.make_desc(8, 128, 112, 112, 128, 3, 3, 1, 1, 1, 1, "f32")) == "winograd"
+    # whatever the tree says, the pick supports the layer
+    for d in (_lib.make_desc(1, 3, 9, 11, 2, 5, 3, 2, 1, 2, 1), _lib.make_desc(4, 64, 9, 9, 64, 3, 3, 1, 1, 1, 2),
+              _lib.make_desc(1, 1, 4, 16384, 4, 1, 3, 1, 1, 1, 1)):
+        assert _lib.check(d, _lib.default_algo(d)) == _lib.CONV_OK
 
 
 def test_argument_errors_before_any_device_call():
@@ -264,3 +271,28 @@ def test_valid_call_without_device_reports_device_error():
     d = _lib.make_desc(1, 4, 8, 8, 4, 3, 3, 1, 1, 1, 1, "f32")
     assert _lib.conv2d_raw(1 << 20, 2 << 20, None, 4 << 20, d, "direct", None, 0, None) == _lib.CONV_ERR_DEVICE
     assert _lib.im2col_raw(1 << 20, 4 << 20, d, None) == _lib.CONV_ERR_DEVICE
+
+
+def test_default_choice_walks_the_fitted_tree():
+    """conv2d_default_algo follows the tree that fit_guess.py fits to the
+    committed sweep timings: the generated table is reproduced byte for byte,
+    and the library's pick equals the script's walk (first supported
+    algorithm of the leaf's ranking) on every swept layer shape."""
+    pytest.importorskip("sklearn")
+    import tempfile
+    from paper_2410_08300_amd import fit_guess as F
+    nodes, ranks = F.fit(F.load(F.TRAIN))
+    with tempfile.TemporaryDirectory() as d:
+        path = os.path.join(d, "tree.inc")
+        F.write_inc(nodes, ranks, path)
+        assert open(path).read() == open(F.OUT).read(), "guess_tree.inc is stale: rerun fit_guess.py"
+    checked = 0
+    for src in (F.TRAIN, F.HELD_OUT):
+        for (_, _), e in F.load(src).items():
+            sh = e["shape"]
+            d = _lib.make_desc(sh["n"], sh["c"], sh["h"], sh["w"], sh["k"], sh["r"], sh["s"], sh["stride"],
+                               sh["pad"], sh["dilation"], sh["groups"], sh["dtype"], sh["bias"], sh["relu"])
+            supported = [a for a in F.ALGOS if _lib.check(d, a) == _lib.CONV_OK]
+            assert _lib.default_algo(d) == F.predict(nodes, ranks, sh, supported), sh
+            checked += 1
+    assert checked > 200

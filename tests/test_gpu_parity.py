@@ -240,6 +240,29 @@ def test_swapped_model_matches_oracle_chain_and_caches_packages():
         assert torch.equal(out, out2)
     convs = [m for m in model.modules() if isinstance(m, cs.Conv2dSwap)]
     assert all(len(m._packages) >= 1 for m in convs)
+    # Cached selector: the first forward measures every supported algorithm
+    # per shape and records the fastest; the second reuses the record, and
+    # so does a model swapped with the cache read back from its JSON.
+    cache = cs.AlgoCache(device=torch.cuda.get_device_name(0))
+    table = cs.swap_conv2d(model, cache)
+    with torch.no_grad():
+        out = model(x.to(DEV))
+    torch.cuda.synchronize()
+    assert rel_err(f64(out), ref) <= 1e-3
+    assert len(cache) == 2
+    for e in cache.entries.values():
+        assert e["algo"] == min(e["ms"], key=e["ms"].get) and len(e["ms"]) >= 6
+    before = {k: dict(v) for k, v in cache.entries.items()}
+    with torch.no_grad():
+        out2 = model(x.to(DEV))
+    torch.cuda.synchronize()
+    assert cache.entries == before and torch.equal(out, out2)
+    back = cs.AlgoCache.from_json(cache.to_json())
+    cs.swap_conv2d(model, back)
+    with torch.no_grad():
+        out3 = model(x.to(DEV))
+    torch.cuda.synchronize()
+    assert back.entries == before and torch.equal(out, out3)
 
 
 # 1x1 layers take their own kernel (filters used as given, pixel-quad loads

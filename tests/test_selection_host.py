@@ -122,3 +122,62 @@ def test_selector_errors():
 def test_cpu_tensors_are_refused():
     with pytest.raises(ValueError):
         cs.conv2d(torch.randn(1, 3, 8, 8), torch.randn(4, 3, 3, 3))
+
+
+def test_algo_cache_measures_each_shape_once_and_persists(fake_backend, monkeypatch, tmp_path):
+    timed = []
+
+    def fake_select(x, w, b=None, stride=1, padding=0, dilation=1, groups=1, relu=False, **kw):
+        timed.append(tuple(x.shape))
+        return "smm", {"smm": 1.0, "direct": 2.0}
+
+    monkeypatch.setattr(selection, "select_fastest", fake_select)
+    torch.manual_seed(3)
+    m = ConvNet()
+    x = torch.randn(2, 3, 16, 16)
+    ref = m(x)
+    cache = cs.AlgoCache(device="test")
+    t = cs.swap_conv2d(m, cache)
+    assert list(t.values()) == ["cached", "cached"] and t.cache is cache
+    fake_backend.clear()
+    assert torch.allclose(m(x), ref, atol=1e-5)
+    assert fake_backend == ["smm", "smm"] and len(timed) == 2 and len(cache) == 2
+    m(x)                                                   # same shapes: no new timing
+    assert len(timed) == 2
+    m(torch.randn(1, 3, 16, 16))                           # new batch size: a new shape
+    assert len(timed) == 4 and len(cache) == 4
+    path = tmp_path / "cache.json"
+    cache.save(str(path))
+    back = cs.AlgoCache.load(str(path))
+    assert back.entries == cache.entries and back.device == "test"
+    key = cs.AlgoCache.key_for(x, m.conv1.weight, m.conv1.bias, (1, 1), (1, 1), (1, 1), 1)
+    assert back.lookup(key) == "smm"
+    # a loaded cache answers without timing
+    m2 = ConvNet()
+    cs.swap_conv2d(m2, back)
+    timed.clear()
+    m2(x)
+    assert timed == []
+
+
+def test_algo_cache_keys_and_errors():
+    k1 = cs.AlgoCache.key((2, 8, 9, 9), (4, 8, 3, 3), 1, 1, 1, 1, "bf16", True, False)
+    k2 = cs.AlgoCache.key((2, 8, 9, 9), (4, 8, 3, 3), (1, 1), (1, 1), (1, 1), 1, "bf16", True, False)
+    assert k1 == k2
+    assert k1 != cs.AlgoCache.key((2, 8, 9, 9), (4, 8, 3, 3), 2, 1, 1, 1, "bf16", True, False)
+    assert k1 != cs.AlgoCache.key((2, 8, 9, 9), (4, 8, 3, 3), 1, 1, 1, 1, "f32", True, False)
+    with pytest.raises(ValueError):
+        cs.AlgoCache.key((2, 8, 9, 9), (4, 3, 3, 3), 1, 1, 1, 1)    # channels do not match groups
+    c = cs.AlgoCache()
+    with pytest.raises(ValueError):
+        c.record(k1, "default")                                     # entries are concrete algorithms
+    c.record(k1, "gemm")
+    assert c.lookup(k1) == "im2col_gemm"
+    with pytest.raises(ValueError):
+        cs.AlgoCache.from_json('{"version": 99, "entries": {}}')
+    t = cs.AlgoTable()
+    t.set("conv1", "cached")
+    m = ConvNet()
+    cs.swap_conv2d(m, {"conv1": "cached"})
+    with pytest.raises(ValueError):
+        m(torch.randn(1, 3, 8, 8))                                  # "cached" without a cache
