@@ -13,7 +13,8 @@ from .conv import (conv2d, conv2d_prepacked, pack_filters, describe, im2col, win
                    winograd_input_transform)
 from .selection import (AlgoTable, AlgoCache, Conv2dSwap, swap_conv2d, select_fastest, tune, time_conv, supported_algos,
                         CONCRETE_ALGOS)
+from .backend import swap_backend, Model
 
 __all__ = ["Conv2dError", "ALGOS", "conv2d", "conv2d_prepacked", "pack_filters", "describe", "im2col", "winograd_filter_transform", "winograd_input_transform",
            "AlgoTable", "AlgoCache", "Conv2dSwap", "swap_conv2d", "select_fastest", "tune", "time_conv", "supported_algos",
-           "CONCRETE_ALGOS"]
+           "CONCRETE_ALGOS", "swap_backend", "Model"]

@@ -28,6 +28,13 @@ EXPORTED = ("conv2d_output_shape", "conv2d_check", "conv2d_workspace_bytes", "co
             "conv2d_algo_from_name")
 
 
+EXPORTED_MODEL = ("convsel_model_create", "convsel_model_destroy", "convsel_model_conv", "convsel_model_linear",
+                  "convsel_model_relu", "convsel_model_pool", "convsel_model_global_avgpool", "convsel_model_add",
+                  "convsel_model_flatten", "convsel_model_set_output", "convsel_model_plan",
+                  "convsel_model_output_shape", "convsel_model_value_placement", "convsel_model_bind",
+                  "convsel_model_forward", "convsel_model_describe")
+
+
 class Desc(ctypes.Structure):
     """conv2d_desc_t."""
     _fields_ = [("n", ctypes.c_int64), ("c", ctypes.c_int64), ("h", ctypes.c_int64), ("w", ctypes.c_int64),
@@ -94,6 +101,31 @@ def lib():
         L.conv2d_algo_name.restype = ctypes.c_char_p
         L.conv2d_algo_from_name.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int)]
         L.conv2d_algo_from_name.restype = i32
+        # model executor (include/convsel_model.h)
+        mp = ctypes.c_void_p
+        i64 = ctypes.c_int64
+        pi32 = ctypes.POINTER(ctypes.c_int32)
+        L.convsel_model_create.argtypes = [i32, ctypes.POINTER(ctypes.c_void_p)]
+        L.convsel_model_destroy.argtypes = [mp]
+        L.convsel_model_destroy.restype = None
+        L.convsel_model_conv.argtypes = [mp, i32, i64, i64, i64, i64, i32, i32, i32, i32, i32, i32, i32, i32, vp, vp,
+                                         i32, pi32]
+        L.convsel_model_linear.argtypes = [mp, i32, i64, i64, i32, vp, vp, i32, pi32]
+        L.convsel_model_relu.argtypes = [mp, i32, pi32]
+        L.convsel_model_pool.argtypes = [mp, i32, i32, i32, i32, i32, i32, i32, i32, pi32]
+        L.convsel_model_global_avgpool.argtypes = [mp, i32, pi32]
+        L.convsel_model_add.argtypes = [mp, i32, i32, i32, pi32]
+        L.convsel_model_flatten.argtypes = [mp, i32, pi32]
+        L.convsel_model_set_output.argtypes = [mp, i32]
+        L.convsel_model_plan.argtypes = [mp, i64, i64, i64, i64, ctypes.POINTER(ctypes.c_size_t)]
+        L.convsel_model_output_shape.argtypes = [mp, ctypes.POINTER(i64), pi32]
+        L.convsel_model_value_placement.argtypes = [mp, i32, ctypes.POINTER(i64), ctypes.POINTER(i64)]
+        L.convsel_model_bind.argtypes = [mp, vp, ctypes.c_size_t, vp]
+        L.convsel_model_forward.argtypes = [mp, vp, vp, vp]
+        L.convsel_model_describe.argtypes = [mp, ctypes.c_char_p, ctypes.c_size_t]
+        for n in EXPORTED_MODEL:
+            if n != "convsel_model_destroy":
+                getattr(L, n).restype = i32
         _lib = L
     return _lib
 
@@ -220,3 +252,102 @@ class PreparedCall:
         st = self._fn(*self._args)
         if st != CONV_OK:
             raise Conv2dError(st, "conv2d")
+
+
+class NativeModel:
+    """Owner of one convsel_model_t (include/convsel_model.h): the calls
+    marshal arguments only; every check and the planning run in the library."""
+
+    def __init__(self, dtype):
+        h = ctypes.c_void_p()
+        st = lib().convsel_model_create(DTYPES[dtype], ctypes.byref(h))
+        if st != CONV_OK:
+            raise Conv2dError(st, "convsel_model_create")
+        self._h = h
+        self.dtype = dtype
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value and _lib is not None:
+            _lib.convsel_model_destroy(h)
+            self._h = None
+
+    def _add(self, fn, *args):
+        out = ctypes.c_int32()
+        st = getattr(lib(), fn)(self._h, *args, ctypes.byref(out))
+        if st != CONV_OK:
+            raise Conv2dError(st, fn)
+        return out.value
+
+    def conv(self, v, c, k, r, s, stride, padding, dilation, groups, algo, w_ptr, b_ptr, relu):
+        sh, sw = _pair(stride)
+        ph, pw = _pair(padding)
+        dh, dw = _pair(dilation)
+        return self._add("convsel_model_conv", v, c, k, r, s, sh, sw, ph, pw, dh, dw, groups, algo_id(algo),
+                         w_ptr, b_ptr or None, int(bool(relu)))
+
+    def linear(self, v, in_features, out_features, algo, w_ptr, b_ptr, relu):
+        return self._add("convsel_model_linear", v, in_features, out_features, algo_id(algo), w_ptr, b_ptr or None,
+                         int(bool(relu)))
+
+    def relu(self, v):
+        return self._add("convsel_model_relu", v)
+
+    def pool(self, v, kind, kernel, stride, padding):
+        kh, kw = _pair(kernel)
+        sh, sw = _pair(stride)
+        ph, pw = _pair(padding)
+        return self._add("convsel_model_pool", v, {"max": 0, "avg": 1}[kind], kh, kw, sh, sw, ph, pw)
+
+    def global_avgpool(self, v):
+        return self._add("convsel_model_global_avgpool", v)
+
+    def add(self, a, b, relu):
+        return self._add("convsel_model_add", a, b, int(bool(relu)))
+
+    def flatten(self, v):
+        return self._add("convsel_model_flatten", v)
+
+    def set_output(self, v):
+        st = lib().convsel_model_set_output(self._h, v)
+        if st != CONV_OK:
+            raise Conv2dError(st, "convsel_model_set_output")
+
+    def plan(self, n, c, h, w):
+        nb = ctypes.c_size_t()
+        st = lib().convsel_model_plan(self._h, n, c, h, w, ctypes.byref(nb))
+        if st != CONV_OK:
+            raise Conv2dError(st, "convsel_model_plan")
+        return nb.value
+
+    def output_shape(self):
+        dims = (ctypes.c_int64 * 4)()
+        nd = ctypes.c_int32()
+        st = lib().convsel_model_output_shape(self._h, dims, ctypes.byref(nd))
+        if st != CONV_OK:
+            raise Conv2dError(st, "convsel_model_output_shape")
+        return tuple(dims[i] for i in range(nd.value))
+
+    def placement(self, v):
+        off, nb = ctypes.c_int64(), ctypes.c_int64()
+        st = lib().convsel_model_value_placement(self._h, v, ctypes.byref(off), ctypes.byref(nb))
+        if st != CONV_OK:
+            raise Conv2dError(st, "convsel_model_value_placement")
+        return off.value, nb.value
+
+    def bind(self, arena_ptr, nbytes, stream):
+        st = lib().convsel_model_bind(self._h, arena_ptr, nbytes, stream)
+        if st != CONV_OK:
+            raise Conv2dError(st, "convsel_model_bind")
+
+    def forward(self, x_ptr, y_ptr, stream):
+        st = lib().convsel_model_forward(self._h, x_ptr, y_ptr, stream)
+        if st != CONV_OK:
+            raise Conv2dError(st, "convsel_model_forward")
+
+    def describe(self):
+        buf = ctypes.create_string_buffer(1 << 16)
+        st = lib().convsel_model_describe(self._h, buf, len(buf))
+        if st != CONV_OK:
+            raise Conv2dError(st, "convsel_model_describe")
+        return buf.value.decode()
