@@ -203,6 +203,104 @@ def cpu_baseline(workload, budget_s=20.0):
                       "with OpenMP" % (len(layers), workload, images, flops / 1e9, t_total)}
 
 
+def resnet50_module(classes=1000):
+    """ResNet-50 v1.5 as an nn.Module whose convolutions carry the layer names
+    of ``workloads.resnet50`` (stem, layerS.B.conv1/2/3, layerS.B.downsample),
+    with batch norm after every convolution, the 3x3/2 max-pool, residual
+    adds, global average pooling and the 2048 -> 1000 linear head."""
+    import torch
+    from torch import nn
+
+    class Bottleneck(nn.Module):
+        def __init__(self, cin, width, stride):
+            super().__init__()
+            cout = 4 * width
+            self.conv1, self.bn1 = nn.Conv2d(cin, width, 1, bias=False), nn.BatchNorm2d(width)
+            self.conv2, self.bn2 = nn.Conv2d(width, width, 3, stride, 1, bias=False), nn.BatchNorm2d(width)
+            self.conv3, self.bn3 = nn.Conv2d(width, cout, 1, bias=False), nn.BatchNorm2d(cout)
+            self.downsample = None
+            if stride != 1 or cin != cout:
+                self.downsample = nn.Conv2d(cin, cout, 1, stride, bias=False)
+                self.down_bn = nn.BatchNorm2d(cout)
+            self.relu = nn.ReLU(inplace=True)
+
+        def forward(self, x):
+            out = self.relu(self.bn1(self.conv1(x)))
+            out = self.relu(self.bn2(self.conv2(out)))
+            out = self.bn3(self.conv3(out))
+            idt = x if self.downsample is None else self.down_bn(self.downsample(x))
+            out += idt
+            return self.relu(out)
+
+    class ResNet50(nn.Module):
+        def __init__(self):
+            super().__init__()
+            self.stem, self.bn = nn.Conv2d(3, 64, 7, 2, 3, bias=False), nn.BatchNorm2d(64)
+            self.relu = nn.ReLU(inplace=True)
+            self.maxpool = nn.MaxPool2d(3, 2, 1)
+            cin = 64
+            for si, (width, blocks) in enumerate([(64, 3), (128, 4), (256, 6), (512, 3)]):
+                layer = []
+                for bi in range(blocks):
+                    layer.append(Bottleneck(cin, width, 2 if (bi == 0 and si > 0) else 1))
+                    cin = 4 * width
+                setattr(self, "layer%d" % (si + 1), nn.Sequential(*layer))
+            self.avgpool = nn.AdaptiveAvgPool2d((1, 1))
+            self.fc = nn.Linear(2048, classes)
+
+        def forward(self, x):
+            x = self.maxpool(self.relu(self.bn(self.stem(x))))
+            x = self.layer4(self.layer3(self.layer2(self.layer1(x))))
+            return self.fc(torch.flatten(self.avgpool(x), 1))
+
+    net = ResNet50()
+    g = torch.Generator().manual_seed(50)
+    for m in net.modules():
+        if isinstance(m, nn.BatchNorm2d):
+            c = m.num_features
+            m.running_mean.copy_(torch.randn(c, generator=g) * 0.1)
+            m.running_var.copy_(torch.rand(c, generator=g) + 0.5)
+            m.weight.data.copy_(torch.rand(c, generator=g) + 0.5)
+            m.bias.data.copy_(torch.randn(c, generator=g) * 0.1)
+    return net.eval()
+
+
+def executor_forward(plan, steps, warmup):
+    """The whole ResNet-50 network (convolutions with the plan's algorithms,
+    folded batch norm, pooling, residual adds, the linear head) through
+    swap_backend, one HIP graph per forward: ms per forward."""
+    import torch
+    import paper_2410_08300_amd as cs
+
+    dev = plan[0]["x"].device
+    net = resnet50_module().to(torch.bfloat16).to(dev)
+    model = cs.swap_backend(net, {p["layer"].name: p["algo"] for p in plan})
+    x = plan[0]["x"]
+    with torch.no_grad():
+        model(x)
+        s = torch.cuda.Stream(dev)
+        s.wait_stream(torch.cuda.current_stream(dev))
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(s):
+            model(x)
+            s.synchronize()
+            with torch.cuda.graph(g, stream=s):
+                model(x)
+        torch.cuda.synchronize()
+        for _ in range(warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            g.replay()
+        torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    return {"ms_per_forward": ms, "ops": len(model.ops),
+            "what": "ResNet-50 v1.5 inference forward (53 convolutions with the step's algorithms, folded batch "
+                    "norm, max-pool, 16 residual adds, global average pool, 2048x1000 linear) through swap_backend, "
+                    "one HIP graph per forward"}
+
+
 def sweep(path, steps, fit_seeds=0):
     """Every algorithm on every unique layer of all five workloads (or, with
     fit_seeds = S > 0, of the fitting set: the 20-layer random chain at seeds
@@ -250,6 +348,8 @@ def main():
                     help="time the step with filter packages built before timing (conv2d_prepacked); by default "
                          "every call rebuilds them from the filters")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-executor", action="store_true",
+                    help="skip the whole-network swap_backend forward (ResNet-50 only)")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--sweep", default=None, help="write per-layer, per-algorithm timings to this JSONL file")
     ap.add_argument("--sweep-fit-seeds", type=int, default=0, metavar="S",
@@ -441,6 +541,10 @@ def main():
                 nets[a] = sum(p["timings"][a] for p in plan)
         extra["network_ms_from_selection_timings"] = nets
     extra["steps"] = {m: {"ms_per_step": t, "tflops": total_flops / (t * 1e-3) / 1e12} for m, t in modes.items()}
+
+    if wl == "resnet50" and not args.no_executor:
+        extra["executor"] = executor_forward(plan, args.steps, args.warmup)
+        extra["executor"]["conv_step_prepacked_ms"] = modes["graph_prepacked"]
 
     if args.calibrate_copy > 0:
         calibration_copy(args.calibrate_copy, dev)

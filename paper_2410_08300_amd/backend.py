@@ -12,7 +12,9 @@ way:
   folded into that convolution's filters and bias (inference statistics);
 * a ReLU that is the only user of a convolution, linear layer or add is
   fused into that operation's epilogue;
-* Dropout and Identity are dropped (inference).
+* Dropout and Identity are dropped (inference);
+* a linear layer runs as a 1 x 1 convolution with the library's default
+  algorithm, or the one a dict selector names for it.
 
 Anything else raises ``NotImplementedError`` at swap time, naming the node.
 The returned ``Model`` plans on the first call for each input shape, takes
@@ -207,7 +209,8 @@ def swap_backend(module, selector="default"):
             ops.append(("conv", n.target))
         elif isinstance(m, nn.Linear):
             relu = fuse_relu_after(n)
-            v = native.linear(val[n.args[0]], m.in_features, m.out_features, "default", keep(m.weight),
+            lin_algo = _canonical(selector.get(n.target, "default")) if isinstance(selector, dict) else "default"
+            v = native.linear(val[n.args[0]], m.in_features, m.out_features, lin_algo, keep(m.weight),
                               keep(m.bias) if m.bias is not None else None, relu)
             ops.append(("linear", n.target))
         elif isinstance(m, (nn.Dropout, nn.Identity)):

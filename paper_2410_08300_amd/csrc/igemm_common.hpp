@@ -61,6 +61,15 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
+// Offset, from a run's first element, of element t of a run of 8 tile
+// pixels that crosses into the next image after `wrap` pixels: every PQ
+// pixels after that it moves one more image (K*PQ elements on, of which the
+// t itself covers PQ).  A run crosses more than one boundary only when
+// PQ < 8.
+__device__ __forceinline__ int64_t run_offset(int t, int wrap, int PQ, int64_t next_img) {
+  return t + (t >= wrap ? (1 + (t - wrap) / PQ) * next_img : 0);
+}
+
 // Bias, ReLU and the NCHW store of one wave's MI x NJ blocks of 32 x 32
 // accumulators (NJ even): rows row0 + 32 mi + .. of group g, pixels col0 +
 // 32 nj + .., or their raw fp32 partial sums when the channels are split.
@@ -154,7 +163,7 @@ __device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float
           } else {
 #pragma unroll
             for (int t = 0; t < 8; ++t)
-              if (t < nvalid) part[o + t + (t >= wrap ? next_img : 0)] = vals[t];
+              if (t < nvalid) part[o + run_offset(t, wrap, PQ, next_img)] = vals[t];
           }
           continue;
         }
@@ -175,7 +184,7 @@ __device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float
           } else {
 #pragma unroll
             for (int t = 0; t < 8; ++t)
-              if (t < nvalid) elem<T>::store(y + o + t + (t >= wrap ? next_img : 0), vals[t]);
+              if (t < nvalid) elem<T>::store(y + o + run_offset(t, wrap, PQ, next_img), vals[t]);
           }
         } else {
           if (full) {
@@ -186,7 +195,7 @@ __device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float
           } else {
 #pragma unroll
             for (int t = 0; t < 8; ++t)
-              if (t < nvalid) elem<T>::store(y + o + t + (t >= wrap ? next_img : 0), vals[t]);
+              if (t < nvalid) elem<T>::store(y + o + run_offset(t, wrap, PQ, next_img), vals[t]);
           }
         }
       }
@@ -280,7 +289,7 @@ __device__ __forceinline__ void store_block128t(const f32x16_t (&acc)[1][4], flo
         const uint32_t wd[4] = {d[it].x, d[it].y, d[it].z, d[it].w};
 #pragma unroll
         for (int t = 0; t < 8; ++t)
-          if (t < r.nvalid) reinterpret_cast<uint16_t*>(y)[o + t + (t >= r.wrap ? next_img : 0)] =
+          if (t < r.nvalid) reinterpret_cast<uint16_t*>(y)[o + run_offset(t, r.wrap, PQ, next_img)] =
               static_cast<uint16_t>(wd[t >> 1] >> (16 * (t & 1)));
       }
     }
@@ -326,7 +335,7 @@ __device__ __forceinline__ void store_block128t(const f32x16_t (&acc)[1][4], flo
         const float vals[8] = {lo[it].x, lo[it].y, lo[it].z, lo[it].w, hi[it].x, hi[it].y, hi[it].z, hi[it].w};
 #pragma unroll
         for (int t = 0; t < 8; ++t)
-          if (t < r.nvalid) part[o + t + (t >= r.wrap ? next_img : 0)] = vals[t];
+          if (t < r.nvalid) part[o + run_offset(t, r.wrap, PQ, next_img)] = vals[t];
       }
     }
     __builtin_amdgcn_wave_barrier();  // the next pass reuses this wave's stage

@@ -180,6 +180,33 @@ def test_edge_cases():
         assert float(buf[0]) == 0.0
 
 
+# Output planes smaller than one 8-pixel store run (P*Q < 8) with several
+# images: a run of a tile then crosses several image boundaries, which the
+# epilogues must follow one element at a time.  A linear layer run as a
+# 1x1 convolution (H = W = 1) is the common case.
+TINY = [
+    # N, C, H, W, K, R, S, stride, pad
+    (3, 32, 1, 1, 10, 1, 1, 1, 0),
+    (4, 300, 1, 1, 70, 1, 1, 1, 0),
+    (4, 24, 2, 3, 40, 3, 3, 1, 1),
+    (5, 16, 3, 3, 72, 3, 3, 2, 1),
+    (3, 64, 7, 7, 64, 7, 7, 1, 0),
+    (6, 8, 5, 5, 130, 5, 5, 1, 0),
+    (9, 40, 2, 2, 24, 1, 1, 1, 0),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("idx", range(len(TINY)), ids=lambda i: "x".join(map(str, TINY[i][:7])))
+def test_tiny_planes_several_images(idx, dtype):
+    N, C, H, Wd, K, R, S, st, pd = TINY[idx]
+    g = torch.Generator().manual_seed(W.seed_for(17, idx))
+    x = torch.randn(N, C, H, Wd, generator=g).to(TDT[dtype])
+    w = (torch.randn(K, C, R, S, generator=g) * (2.0 / (C * R * S)) ** 0.5).to(TDT[dtype])
+    b = (torch.randn(K, generator=g) * 0.1).to(TDT[dtype])
+    check_full(x, w, b, st, pd, 1, 1, False, ALGOS, "tiny %s %s" % (TINY[idx], dtype))
+
+
 def test_unsupported_and_invalid_calls_raise():
     x = torch.randn(1, 4, 8, 8, device=DEV)
     with pytest.raises(cs.Conv2dError):
