@@ -67,7 +67,12 @@ __device__ __forceinline__ void static_for(F&& f) {
 // t itself covers PQ).  A run crosses more than one boundary only when
 // PQ < 8.
 __device__ __forceinline__ int64_t run_offset(int t, int wrap, int PQ, int64_t next_img) {
-  return t + (t >= wrap ? (1 + (t - wrap) / PQ) * next_img : 0);
+  int64_t o = t + (t >= wrap ? next_img : 0);
+  if (PQ < 8) {  // uniform; t - wrap <= 6, so at most six more boundaries
+#pragma unroll
+    for (int m = 1; m <= 6; ++m) o += (t - wrap >= m * PQ) ? next_img : 0;
+  }
+  return o;
 }
 
 // Bias, ReLU and the NCHW store of one wave's MI x NJ blocks of 32 x 32
