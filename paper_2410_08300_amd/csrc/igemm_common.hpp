@@ -61,19 +61,26 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
-// Offset, from a run's first element, of element t of a run of 8 tile
-// pixels that crosses into the next image after `wrap` pixels: every PQ
-// pixels after that it moves one more image (K*PQ elements on, of which the
-// t itself covers PQ).  A run crosses more than one boundary only when
-// PQ < 8.
-__device__ __forceinline__ int64_t run_offset(int t, int wrap, int PQ, int64_t next_img) {
-  int64_t o = t + (t >= wrap ? next_img : 0);
-  if (PQ < 8) {  // uniform; t - wrap <= 6, so at most six more boundaries
-#pragma unroll
-    for (int m = 1; m <= 6; ++m) o += (t - wrap >= m * PQ) ? next_img : 0;
+// Element offsets of a run of 8 tile pixels that crosses into the next
+// image after `wrap` pixels, and then again every PQ pixels: each crossing
+// moves the destination (K-1)*PQ elements further than the pixel count
+// alone.  With PQ >= 8 a run crosses at most once and the stores use that
+// directly; planes smaller than a run use this cursor, per element t = 0..7
+// in order:  RunCursor c(wrap, PQ, next_img);  ...  dst[o + c.at(t)] = v[t];
+struct RunCursor {
+  int64_t add;
+  int next;
+  const int PQ;
+  const int64_t step;
+  __device__ __forceinline__ RunCursor(int wrap, int pq, int64_t next_img) : add(0), next(wrap), PQ(pq), step(next_img) {}
+  __device__ __forceinline__ int64_t at(int t) {
+    if (t == next) {
+      add += step;
+      next += PQ;
+    }
+    return t + add;
   }
-  return o;
-}
+};
 
 // Bias, ReLU and the NCHW store of one wave's MI x NJ blocks of 32 x 32
 // accumulators (NJ even): rows row0 + 32 mi + .. of group g, pixels col0 +
@@ -166,9 +173,18 @@ __device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float
             __builtin_memcpy(part + o, &lo[it], 16);
             __builtin_memcpy(part + o + 4, &hi[it], 16);
           } else {
+            if (PQ >= 8) {
 #pragma unroll
-            for (int t = 0; t < 8; ++t)
-              if (t < nvalid) part[o + run_offset(t, wrap, PQ, next_img)] = vals[t];
+              for (int t = 0; t < 8; ++t)
+                if (t < nvalid) part[o + t + (t >= wrap ? next_img : 0)] = vals[t];
+            } else {
+              RunCursor rc(wrap, PQ, next_img);
+#pragma unroll
+              for (int t = 0; t < 8; ++t) {
+                const int64_t ot = rc.at(t);
+                if (t < nvalid) part[o + ot] = vals[t];
+              }
+            }
           }
           continue;
         }
@@ -187,9 +203,18 @@ __device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float
             w.w = f32x2_to_bf16x2(vals[6], vals[7]);
             __builtin_memcpy(y + o, &w, 16);
           } else {
+            if (PQ >= 8) {
 #pragma unroll
-            for (int t = 0; t < 8; ++t)
-              if (t < nvalid) elem<T>::store(y + o + run_offset(t, wrap, PQ, next_img), vals[t]);
+              for (int t = 0; t < 8; ++t)
+                if (t < nvalid) elem<T>::store(y + o + t + (t >= wrap ? next_img : 0), vals[t]);
+            } else {
+              RunCursor rc(wrap, PQ, next_img);
+#pragma unroll
+              for (int t = 0; t < 8; ++t) {
+                const int64_t ot = rc.at(t);
+                if (t < nvalid) elem<T>::store(y + o + ot, vals[t]);
+              }
+            }
           }
         } else {
           if (full) {
@@ -198,9 +223,18 @@ __device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float
             __builtin_memcpy(y + o, &a, 16);
             __builtin_memcpy(y + o + 4, &b, 16);
           } else {
+            if (PQ >= 8) {
 #pragma unroll
-            for (int t = 0; t < 8; ++t)
-              if (t < nvalid) elem<T>::store(y + o + run_offset(t, wrap, PQ, next_img), vals[t]);
+              for (int t = 0; t < 8; ++t)
+                if (t < nvalid) elem<T>::store(y + o + t + (t >= wrap ? next_img : 0), vals[t]);
+            } else {
+              RunCursor rc(wrap, PQ, next_img);
+#pragma unroll
+              for (int t = 0; t < 8; ++t) {
+                const int64_t ot = rc.at(t);
+                if (t < nvalid) elem<T>::store(y + o + ot, vals[t]);
+              }
+            }
           }
         }
       }
@@ -220,7 +254,9 @@ __device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float
 // rate.  A run of 8 pixels inside one image is one 16-byte store (2-byte
 // alignment is enough on gfx950); a run that crosses an image boundary or
 // passes the last pixel is stored element by element.  Split-K partials
-// (fp32) are staged in two halves of 64 pixels.
+// (fp32) are staged in two halves of 64 pixels.  Precondition (the callers'
+// plans guarantee it): a run crosses at most one image boundary, i.e.
+// P*Q >= 8 or the tile index space pads planes to a multiple of 8.
 template <typename T>
 __device__ __forceinline__ void store_block128t(const f32x16_t (&acc)[1][4], float* stage_f, const EpiArgs& e,
                                                 int row0, int col0, int g, int split) {
@@ -294,8 +330,9 @@ __device__ __forceinline__ void store_block128t(const f32x16_t (&acc)[1][4], flo
         const uint32_t wd[4] = {d[it].x, d[it].y, d[it].z, d[it].w};
 #pragma unroll
         for (int t = 0; t < 8; ++t)
-          if (t < r.nvalid) reinterpret_cast<uint16_t*>(y)[o + run_offset(t, r.wrap, PQ, next_img)] =
-              static_cast<uint16_t>(wd[t >> 1] >> (16 * (t & 1)));
+          if (t < r.nvalid)
+            reinterpret_cast<uint16_t*>(y)[o + t + (t >= r.wrap ? next_img : 0)] =
+                static_cast<uint16_t>(wd[t >> 1] >> (16 * (t & 1)));
       }
     }
     __builtin_amdgcn_wave_barrier();
@@ -340,7 +377,7 @@ __device__ __forceinline__ void store_block128t(const f32x16_t (&acc)[1][4], flo
         const float vals[8] = {lo[it].x, lo[it].y, lo[it].z, lo[it].w, hi[it].x, hi[it].y, hi[it].z, hi[it].w};
 #pragma unroll
         for (int t = 0; t < 8; ++t)
-          if (t < r.nvalid) part[o + run_offset(t, r.wrap, PQ, next_img)] = vals[t];
+          if (t < r.nvalid) part[o + t + (t >= r.wrap ? next_img : 0)] = vals[t];
       }
     }
     __builtin_amdgcn_wave_barrier();  // the next pass reuses this wave's stage

@@ -1109,7 +1109,9 @@ bool make_pw_plan(const Shape& s, PwPlan& pl, int64_t N1 = -1, bool allow_dma = 
   // on a repacked copy (plane = P*Q rounded up to 8).
   pl.dma = sizeof(T) == 2 && allow_dma;
   const bool plain = s.sh == 1 && s.sw == 1 && s.ph == 0 && s.pw == 0;
-  pl.ub4 = pl.dma && plain && (s.H * s.W) % 8 != 0 && (s.H * s.W) % 2 == 0;
+  // (In place as pixel pairs only for planes of at least 8 pixels: the
+  // epilogue's runs of 8 may cross one image boundary, not several.)
+  pl.ub4 = pl.dma && plain && (s.H * s.W) % 8 != 0 && (s.H * s.W) % 2 == 0 && s.H * s.W > 8;
   pl.repack = pl.dma && !(plain && (s.H * s.W) % 8 == 0) && !pl.ub4;
   pl.span = pl.repack ? (int)((s.P * s.Q + 7) / 8 * 8) : pl.dma ? (int)(s.H * s.W) : (int)(s.P * s.Q);
   int64_t img_bytes = s.C * s.H * s.W * s.esize();

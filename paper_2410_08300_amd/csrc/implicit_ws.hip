@@ -362,6 +362,7 @@ struct WsPlan {
 
 bool make_ws_plan(const Shape& s, WsPlan& pl, int64_t N1 = -1) {
   if (s.dtype != DT_BF16 || s.G != 1 || s.R * s.S != kWsTaps || s.C <= 8) return false;
+  if (s.P * s.Q < 8) return false;  // the channel-row epilogue's runs cross at most one image
   const int64_t img_bytes = s.C * s.H * s.W * 2;
   if (img_bytes > kMaxLaunchBytes) return false;
   if (N1 < 0) {

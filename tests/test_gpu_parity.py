@@ -193,6 +193,8 @@ TINY = [
     (3, 64, 7, 7, 64, 7, 7, 1, 0),
     (6, 8, 5, 5, 130, 5, 5, 1, 0),
     (9, 40, 2, 2, 24, 1, 1, 1, 0),
+    (5, 64, 2, 3, 96, 1, 1, 1, 0),
+    (7, 48, 2, 2, 64, 3, 3, 1, 1),
 ]
 
 
