@@ -104,6 +104,7 @@ __device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float
   const int PQ = e.PQ, span = e.span;
   const bool split_out = e.splits > 1;
   const T* bias = reinterpret_cast<const T*>(e.b);
+  const bool has_bias = bias != nullptr;
 
   // Staging layout: float4 f of row r sits at f ^ ((r & 1) | 8 ((r >> 2) & 1)),
   // so the writes of two half-waves (rows r and r+4) and the reads of four
@@ -188,11 +189,12 @@ __device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float
           }
           continue;
         }
+        if (has_bias)  // uniform
 #pragma unroll
-        for (int t = 0; t < 8; ++t) {
-          vals[t] += bv[mi][it];
-          if (e.relu) vals[t] = fmaxf(vals[t], 0.f);
-        }
+          for (int t = 0; t < 8; ++t) vals[t] += bv[mi][it];
+        if (e.relu)  // uniform
+#pragma unroll
+          for (int t = 0; t < 8; ++t) vals[t] = fmaxf(vals[t], 0.f);
         T* y = reinterpret_cast<T*>(e.y);
         if constexpr (sizeof(T) == 2) {
           if (full) {
@@ -289,24 +291,36 @@ __device__ __forceinline__ void store_block128t(const f32x16_t (&acc)[1][4], flo
     const int i_own = row0 + l32;
     const float bv = (bias && i_own < e.Kg) ? elem<T>::load(bias + g * e.Kg + i_own) : 0.f;
     // Channel l32, pixels px0 .. px0 + 3 (8 bytes of T = bf16; fp32 goes
-    // through the partial path's layout below).
+    // through the partial path's layout below).  Bias and ReLU are uniform
+    // choices: without them the 64 values per lane only need rounding, and
+    // the per-value add and select are not issued at all.
     static_assert(sizeof(T) == 2, "bf16 output");
+    auto stage_all = [&](auto with_bias, auto with_relu) {
 #pragma unroll
-    for (int nj = 0; nj < 4; ++nj)
+      for (int nj = 0; nj < 4; ++nj)
 #pragma unroll
-      for (int gg = 0; gg < 4; ++gg) {
-        float v4[4];
+        for (int gg = 0; gg < 4; ++gg) {
+          float v4[4];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          v4[k] = acc[0][nj][4 * gg + k] + bv;
-          if (e.relu) v4[k] = fmaxf(v4[k], 0.f);
+          for (int k = 0; k < 4; ++k) {
+            v4[k] = acc[0][nj][4 * gg + k];
+            if constexpr (decltype(with_bias)::value) v4[k] += bv;
+            if constexpr (decltype(with_relu)::value) v4[k] = fmaxf(v4[k], 0.f);
+          }
+          uint2 w;
+          w.x = f32x2_to_bf16x2(v4[0], v4[1]);
+          w.y = f32x2_to_bf16x2(v4[2], v4[3]);
+          const int px0 = nj * 32 + 8 * gg + 4 * h;
+          *reinterpret_cast<uint2*>(stage + l32 * 256 + ((((px0 >> 3) ^ (l32 & 15))) << 4) + ((px0 >> 2) & 1) * 8) = w;
         }
-        uint2 w;
-        w.x = f32x2_to_bf16x2(v4[0], v4[1]);
-        w.y = f32x2_to_bf16x2(v4[2], v4[3]);
-        const int px0 = nj * 32 + 8 * gg + 4 * h;
-        *reinterpret_cast<uint2*>(stage + l32 * 256 + ((((px0 >> 3) ^ (l32 & 15))) << 4) + ((px0 >> 2) & 1) * 8) = w;
-      }
+    };
+    using F = std::false_type;
+    using Tr = std::true_type;
+    if (bias) {
+      if (e.relu) stage_all(Tr{}, Tr{}); else stage_all(Tr{}, F{});
+    } else {
+      if (e.relu) stage_all(F{}, Tr{}); else stage_all(F{}, F{});
+    }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
     __builtin_amdgcn_wave_barrier();
     // Lane l: channel rows l/16 + 4 it (it = 0..7), 16-byte unit l % 16.
