@@ -613,3 +613,22 @@ conv_status_t conv2d_algo_from_name(const char* name, conv_algo_t* algo) {
 }
 
 }  // extern "C"
+
+namespace convsel {
+
+// For the model executor (not part of the public ABI): conv2d_prepacked() of
+// an implicit GEMM layer whose epilogue also adds `res` (N x K x P x Q, the
+// layer's dtype) before the ReLU.
+conv_status_t conv2d_prepacked_residual(const void* x, const void* packed, const void* b, const void* res, void* y,
+                                        const conv2d_desc_t* desc, conv_algo_t algo, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+  Shape s;
+  const conv_status_t st = prepare_call(desc, &algo, &s, x, packed, b, y, workspace, workspace_bytes, true);
+  if (st != CONV_OK || s.N == 0) return st;
+  if (algo != CONV_ALGO_IMPLICIT_GEMM) return CONV_ERR_UNSUPPORTED;
+  const size_t ybytes = (size_t)s.N * s.K * s.P * s.Q * s.esize();
+  if (!res || overlaps(y, ybytes, res, ybytes)) return CONV_ERR_INVALID_ARG;
+  return from_hip(launch_implicit_main(s, x, packed, b, y, workspace, (hipStream_t)stream, res));
+}
+
+}  // namespace convsel

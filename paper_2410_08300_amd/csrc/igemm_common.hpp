@@ -29,7 +29,49 @@ struct EpiArgs {
   int splits;          // workgroups sharing one output tile along the channels
   int slab;            // floats per split of `partial` (N*K*P*Q rounded up to 4)
   int vec;             // store piece in elements (8, 4, 2 or 1; see store_tile)
+  // Residual added after the bias and before the ReLU (same layout and type
+  // as y; NULL: none).  With bf16 the convolution's value is rounded to bf16
+  // first, so y = round(relu(round(conv + b) + res)) -- the rounding steps
+  // of a convolution followed by a separate add.
+  const void* res = nullptr;
 };
+
+// Adds the residual to the 8 values of a run (offsets as for its stores).
+template <typename T>
+__device__ __forceinline__ void add_residual_run(float (&v)[8], const EpiArgs& e, int64_t o, bool full, int nvalid,
+                                                 int wrap, int PQ, int64_t next_img) {
+  const T* rp = reinterpret_cast<const T*>(e.res);
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) v[t] = bf16_to_f32(f32_to_bf16(v[t]));
+  }
+  if (full) {
+    if constexpr (sizeof(T) == 2) {
+      uint4 r;
+      __builtin_memcpy(&r, rp + o, 16);
+      const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+      for (int t = 0; t < 8; ++t) v[t] += __uint_as_float((w[t >> 1] >> (16 * (t & 1))) << 16);
+    } else {
+      float4 a, b;
+      __builtin_memcpy(&a, rp + o, 16);
+      __builtin_memcpy(&b, rp + o + 4, 16);
+      v[0] += a.x; v[1] += a.y; v[2] += a.z; v[3] += a.w;
+      v[4] += b.x; v[5] += b.y; v[6] += b.z; v[7] += b.w;
+    }
+    return;
+  }
+  int64_t add = 0;
+  int next = wrap;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    if (t == next) {
+      add += next_img;
+      next += PQ;
+    }
+    if (t < nvalid) v[t] += elem<T>::load(rp + o + t + add);
+  }
+}
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, (int)kRsrcWord3);
@@ -192,6 +234,8 @@ __device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float
         if (has_bias)  // uniform
 #pragma unroll
           for (int t = 0; t < 8; ++t) vals[t] += bv[mi][it];
+        if (e.res)  // uniform
+          add_residual_run<T>(vals, e, o, full, nvalid, wrap, PQ, next_img);
         if (e.relu)  // uniform
 #pragma unroll
           for (int t = 0; t < 8; ++t) vals[t] = fmaxf(vals[t], 0.f);
@@ -259,32 +303,37 @@ __device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float
 // (fp32) are staged in two halves of 64 pixels.  Precondition (the callers'
 // plans guarantee it): a run crosses at most one image boundary, i.e.
 // P*Q >= 8 or the tile index space pads planes to a multiple of 8.
+// A run of 8 pixels starting at tile pixel `px` (tile origin col0, channel
+// block row0 of group g): where its first channel row goes and whether it is
+// whole.
+struct Run128t {
+  int64_t o;
+  int nvalid, wrap;
+  bool full;
+};
+__device__ __forceinline__ Run128t run128t(const EpiArgs& e, int row0, int col0, int g, int px) {
+  Run128t r;
+  const int PQ = e.PQ, span = e.span;
+  const int j = col0 + px;
+  const int n = j / span, pq = j - n * span;
+  const int last = j >= e.NPQ ? 0 : span == PQ ? e.NPQ - j : PQ - pq;
+  r.wrap = span == PQ ? PQ - pq : 8;
+  r.full = last >= 8 && r.wrap >= 8;
+  r.nvalid = last < 8 ? last : 8;
+  r.o = (static_cast<int64_t>(n) * e.K + g * e.Kg + row0) * PQ + pq;
+  return r;
+}
+
 template <typename T>
 __device__ __forceinline__ void store_block128t(const f32x16_t (&acc)[1][4], float* stage_f, const EpiArgs& e,
                                                 int row0, int col0, int g, int split) {
   const int lane = threadIdx.x & 63;
   const int l32 = lane & 31, h = lane >> 5;
-  const int PQ = e.PQ, span = e.span;
+  const int PQ = e.PQ;
   char* stage = reinterpret_cast<char*>(stage_f);
   const int64_t next_img = static_cast<int64_t>(e.K - 1) * PQ;
-  // A run of 8 pixels starting at tile pixel `px` of output channel
-  // `i = row0 + ch`: where it goes and whether it is whole.
-  struct Run {
-    int64_t o;
-    int nvalid, wrap;
-    bool full;
-  };
-  auto run_at = [&](int px) {
-    Run r;
-    const int j = col0 + px;
-    const int n = j / span, pq = j - n * span;
-    const int last = j >= e.NPQ ? 0 : span == PQ ? e.NPQ - j : PQ - pq;
-    r.wrap = span == PQ ? PQ - pq : 8;
-    r.full = last >= 8 && r.wrap >= 8;
-    r.nvalid = last < 8 ? last : 8;
-    r.o = (static_cast<int64_t>(n) * e.K + g * e.Kg + row0) * PQ + pq;
-    return r;
-  };
+  using Run = Run128t;
+  auto run_at = [&](int px) { return run128t(e, row0, col0, g, px); };
 
   if (e.splits <= 1) {
     const T* bias = reinterpret_cast<const T*>(e.b);
@@ -317,9 +366,9 @@ __device__ __forceinline__ void store_block128t(const f32x16_t (&acc)[1][4], flo
     using F = std::false_type;
     using Tr = std::true_type;
     if (bias) {
-      if (e.relu) stage_all(Tr{}, Tr{}); else stage_all(Tr{}, F{});
+      if (e.relu && !e.res) stage_all(Tr{}, Tr{}); else stage_all(Tr{}, F{});
     } else {
-      if (e.relu) stage_all(F{}, Tr{}); else stage_all(F{}, F{});
+      if (e.relu && !e.res) stage_all(F{}, Tr{}); else stage_all(F{}, F{});
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
     __builtin_amdgcn_wave_barrier();
@@ -333,6 +382,44 @@ __device__ __forceinline__ void store_block128t(const f32x16_t (&acc)[1][4], flo
       d[it] = *reinterpret_cast<const uint4*>(stage + row * 256 + ((u ^ (row & 15)) << 4));
     }
     T* y = reinterpret_cast<T*>(e.y);
+    if (e.res) {  // uniform: residual add (and the ReLU after it), then the same stores
+      // Whole runs: all eight rows are requested before any is used, so the
+      // loads overlap (one memory round trip per tile, not one per row).
+      uint4 rr[8];
+      if (r.full) {
+        const uint16_t* rp = reinterpret_cast<const uint16_t*>(e.res);
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+          const int row = rrow + 4 * it;
+          rr[it] = make_uint4(0u, 0u, 0u, 0u);
+          if (row0 + row < e.Kg) __builtin_memcpy(&rr[it], rp + r.o + static_cast<int64_t>(row) * PQ, 16);
+        }
+      }
+#pragma unroll
+      for (int it = 0; it < 8; ++it) {
+        const int row = rrow + 4 * it;
+        if (row0 + row >= e.Kg || r.nvalid <= 0) continue;
+        const int64_t o = r.o + static_cast<int64_t>(row) * PQ;
+        const uint32_t w[4] = {d[it].x, d[it].y, d[it].z, d[it].w};
+        float v[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) v[t] = __uint_as_float((w[t >> 1] >> (16 * (t & 1))) << 16);
+        if (r.full) {  // the staged values are bf16 already
+          const uint32_t q[4] = {rr[it].x, rr[it].y, rr[it].z, rr[it].w};
+#pragma unroll
+          for (int t = 0; t < 8; ++t) v[t] += __uint_as_float((q[t >> 1] >> (16 * (t & 1))) << 16);
+        } else {
+          add_residual_run<T>(v, e, o, false, r.nvalid, r.wrap, PQ, next_img);
+        }
+        if (e.relu)
+#pragma unroll
+          for (int t = 0; t < 8; ++t) v[t] = fmaxf(v[t], 0.f);
+        d[it].x = f32x2_to_bf16x2(v[0], v[1]);
+        d[it].y = f32x2_to_bf16x2(v[2], v[3]);
+        d[it].z = f32x2_to_bf16x2(v[4], v[5]);
+        d[it].w = f32x2_to_bf16x2(v[6], v[7]);
+      }
+    }
 #pragma unroll
     for (int it = 0; it < 8; ++it) {
       const int row = rrow + 4 * it;
@@ -431,7 +518,7 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 template <typename T>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, const T* __restrict__ bias,
                                                             T* __restrict__ y, int total, int slab, int PQ, int K,
-                                                            int splits, int relu) {
+                                                            int splits, int relu, const T* __restrict__ res) {
   const int i0 = (blockIdx.x * 256 + threadIdx.x) * 4;
   if (i0 >= total) return;
   const int n4 = total - i0 < 4 ? total - i0 : 4;
@@ -449,6 +536,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     const int i = i0 + e;
     float v = sum[e];
     if (bias) v += elem<T>::load(bias + (i / PQ) % K);
+    if (res) v = elem<T>::to_f32(elem<T>::from_f32(v)) + elem<T>::load(res + i);  // see EpiArgs::res
     if (relu) v = fmaxf(v, 0.f);
     elem<T>::store(y + i, v);
   }

@@ -1025,7 +1025,7 @@ hipError_t launch_one(const IgPlan& pl, const IgArgs& a, hipStream_t stream) {
   const int total = a.N * a.K * a.P * a.Q;
   hipLaunchKernelGGL(splitk_reduce_kernel<T>, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, stream,
                      a.e.partial, reinterpret_cast<const T*>(a.e.b), reinterpret_cast<T*>(a.e.y), total, a.e.slab,
-                     a.P * a.Q, a.K, a.e.splits, a.e.relu);
+                     a.P * a.Q, a.K, a.e.splits, a.e.relu, reinterpret_cast<const T*>(a.e.res));
   return hipGetLastError();
 }
 
@@ -1050,7 +1050,7 @@ hipError_t pack_typed(const Shape& s, const void* w, void* wp, hipStream_t strea
 
 template <typename T>
 hipError_t main_typed(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* part_ws,
-                      hipStream_t stream) {
+                      hipStream_t stream, const void* res) {
   IgPlan pl;
   if (!make_plan<T>(s, pl)) return hipErrorInvalidValue;
   float* part = reinterpret_cast<float*>(part_ws);
@@ -1066,6 +1066,7 @@ hipError_t main_typed(const Shape& s, const void* x, const void* wp, const void*
     IgArgs a = cur.a;
     a.x = reinterpret_cast<const T*>(x) + n0 * img_elems;
     a.e.y = reinterpret_cast<T*>(y) + n0 * out_elems;
+    a.e.res = res ? reinterpret_cast<const T*>(res) + n0 * out_elems : nullptr;
     a.x_bytes = (uint32_t)(cnt * img_elems * s.esize());
     a.wp = wp;
     a.wp_bytes = (uint32_t)pl.wp_bytes;
@@ -1186,7 +1187,7 @@ hipError_t pw_dma_launch(const PwPlan& pl, const PwArgs& a, hipStream_t stream) 
   const int total = (int)((int64_t)(a.NPQ / a.e.span) * a.e.PQ * a.e.K);
   hipLaunchKernelGGL(splitk_reduce_kernel<bf16_t>, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, stream,
                      a.e.partial, reinterpret_cast<const bf16_t*>(a.e.b), reinterpret_cast<bf16_t*>(a.e.y), total,
-                     a.e.slab, a.e.PQ, a.e.K, a.e.splits, a.e.relu);
+                     a.e.slab, a.e.PQ, a.e.K, a.e.splits, a.e.relu, reinterpret_cast<const bf16_t*>(a.e.res));
   return hipGetLastError();
 }
 
@@ -1199,13 +1200,13 @@ hipError_t pw_launch(const PwPlan& pl, const PwArgs& a, hipStream_t stream) {
   const int total = (int)((int64_t)a.NPQ * a.e.K);
   hipLaunchKernelGGL(splitk_reduce_kernel<T>, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, stream,
                      a.e.partial, reinterpret_cast<const T*>(a.e.b), reinterpret_cast<T*>(a.e.y), total, a.e.slab,
-                     a.e.PQ, a.e.K, a.e.splits, a.e.relu);
+                     a.e.PQ, a.e.K, a.e.splits, a.e.relu, reinterpret_cast<const T*>(a.e.res));
   return hipGetLastError();
 }
 
 template <typename T>
 hipError_t pw_main_typed(const Shape& s, const void* x, const void* w, const void* b, void* y, void* part_ws,
-                         hipStream_t stream) {
+                         const void* res, hipStream_t stream) {
   PwPlan pl;
   if (!make_pw_plan<T>(s, pl)) return hipErrorInvalidValue;
   if (reinterpret_cast<uintptr_t>(w) % 16 != 0) return hipErrorInvalidValue;
@@ -1227,6 +1228,7 @@ hipError_t pw_main_typed(const Shape& s, const void* x, const void* w, const voi
     a.x_bytes = (uint32_t)(cnt * img_elems * s.esize());
     a.w_bytes = (uint32_t)(s.K * s.C * s.esize());
     a.e.y = reinterpret_cast<T*>(y) + n0 * out_elems;
+    a.e.res = res ? reinterpret_cast<const T*>(res) + n0 * out_elems : nullptr;
     a.e.b = b;
     a.e.partial = reinterpret_cast<float*>(ws + align256(cur.repack_bytes));
     a.e.vec = store_piece(s, a.e.y);
@@ -1375,14 +1377,14 @@ hipError_t launch_implicit_pack(const Shape& s, const void* w, void* wp, hipStre
 }
 
 hipError_t launch_implicit_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* part,
-                                hipStream_t stream) {
-  if (rows_applies(s)) return rows_main(s, x, wp, b, y, stream);
-  if (ws_applies(s)) return ws_main(s, x, wp, b, y, part, stream);
+                                hipStream_t stream, const void* res) {
+  if (rows_applies(s)) return rows_main(s, x, wp, b, y, stream, res);
+  if (ws_applies(s)) return ws_main(s, x, wp, b, y, part, stream, res);
   if (use_pointwise(s))
-    return s.dtype == DT_F32 ? pw_main_typed<float>(s, x, wp, b, y, part, stream)
-                             : pw_main_typed<bf16_t>(s, x, wp, b, y, part, stream);
-  return s.dtype == DT_F32 ? main_typed<float>(s, x, wp, b, y, part, stream)
-                           : main_typed<bf16_t>(s, x, wp, b, y, part, stream);
+    return s.dtype == DT_F32 ? pw_main_typed<float>(s, x, wp, b, y, part, res, stream)
+                             : pw_main_typed<bf16_t>(s, x, wp, b, y, part, res, stream);
+  return s.dtype == DT_F32 ? main_typed<float>(s, x, wp, b, y, part, stream, res)
+                           : main_typed<bf16_t>(s, x, wp, b, y, part, stream, res);
 }
 
 hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, const void* b, void* y, void* ws,

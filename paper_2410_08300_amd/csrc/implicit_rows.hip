@@ -280,7 +280,8 @@ hipError_t rows_pack(const Shape& s, const void* w, void* wp, hipStream_t stream
   return hipGetLastError();
 }
 
-hipError_t rows_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, hipStream_t stream) {
+hipError_t rows_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, hipStream_t stream,
+                     const void* res) {
   RowPlan pl;
   if (!make_row_plan(s, pl)) return hipErrorInvalidValue;
   const int64_t img_elems = s.C * s.H * s.W, out_elems = s.K * s.P * s.Q;
@@ -294,6 +295,7 @@ hipError_t rows_main(const Shape& s, const void* x, const void* wp, const void* 
     a.x_bytes = (uint32_t)(cnt * img_elems * 2);
     a.wp = wp;
     a.e.y = reinterpret_cast<uint16_t*>(y) + n0 * out_elems;
+    a.e.res = res ? reinterpret_cast<const uint16_t*>(res) + n0 * out_elems : nullptr;
     a.e.b = b;
     a.e.vec = store_piece(s, a.e.y);
     const dim3 grid((unsigned)((a.NPQ + BN - 1) / BN), (unsigned)cur.ktiles);

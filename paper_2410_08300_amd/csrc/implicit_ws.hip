@@ -424,7 +424,7 @@ hipError_t ws_launch(const WsPlan& pl, const WsArgs& a, hipStream_t stream) {
   const int total = a.N * a.K * a.P * a.Q;
   hipLaunchKernelGGL(splitk_reduce_kernel<bf16_t>, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, stream,
                      a.e.partial, reinterpret_cast<const bf16_t*>(a.e.b), reinterpret_cast<bf16_t*>(a.e.y), total,
-                     a.e.slab, a.P * a.Q, a.K, a.e.splits, a.e.relu);
+                     a.e.slab, a.P * a.Q, a.K, a.e.splits, a.e.relu, reinterpret_cast<const bf16_t*>(a.e.res));
   return hipGetLastError();
 }
 
@@ -464,7 +464,7 @@ hipError_t ws_pack(const Shape& s, const void* w, void* wp, hipStream_t stream) 
 }
 
 hipError_t ws_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* part_ws,
-                   hipStream_t stream) {
+                   hipStream_t stream, const void* res) {
   WsPlan pl;
   if (!make_ws_plan(s, pl)) return hipErrorInvalidValue;
   const int64_t img_elems = s.C * s.H * s.W, out_elems = s.K * s.P * s.Q;
@@ -479,6 +479,7 @@ hipError_t ws_main(const Shape& s, const void* x, const void* wp, const void* b,
     a.wp = wp;
     a.wp_bytes = (uint32_t)cur.wp_bytes;
     a.e.y = reinterpret_cast<uint16_t*>(y) + n0 * out_elems;
+    a.e.res = res ? reinterpret_cast<const uint16_t*>(res) + n0 * out_elems : nullptr;
     a.e.b = b;
     a.e.partial = reinterpret_cast<float*>(part_ws);
     a.e.vec = store_piece(s, a.e.y);

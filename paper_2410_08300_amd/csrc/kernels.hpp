@@ -57,7 +57,8 @@ hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t str
 bool rows_applies(const Shape& s);
 size_t rows_packed_bytes(const Shape& s);
 hipError_t rows_pack(const Shape& s, const void* w, void* wp, hipStream_t stream);
-hipError_t rows_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, hipStream_t stream);
+hipError_t rows_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, hipStream_t stream,
+                     const void* res = nullptr);
 std::string rows_describe(const Shape& s);
 
 // Implicit GEMM with loader and compute waves (bf16, one group, nine taps,
@@ -68,7 +69,7 @@ size_t ws_packed_bytes(const Shape& s);
 size_t ws_split_bytes(const Shape& s);
 hipError_t ws_pack(const Shape& s, const void* w, void* wp, hipStream_t stream);
 hipError_t ws_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* part_ws,
-                   hipStream_t stream);
+                   hipStream_t stream, const void* res = nullptr);
 std::string ws_describe(const Shape& s);
 
 // direct convolution (VALU), all N images.
@@ -86,7 +87,7 @@ size_t implicit_gemm_split_bytes(const Shape& s);
 size_t implicit_gemm_workspace(const Shape& s);  // packed filters (256-aligned) + split partials
 hipError_t launch_implicit_pack(const Shape& s, const void* w, void* wp, hipStream_t stream);
 hipError_t launch_implicit_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* part,
-                                hipStream_t stream);
+                                hipStream_t stream, const void* res = nullptr);
 hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, const void* b, void* y, void* ws,
                                 hipStream_t stream);
 std::string implicit_gemm_describe(const Shape& s);

@@ -18,6 +18,12 @@
 using convsel::bf16_t;
 using convsel::elem;
 
+namespace convsel {
+conv_status_t conv2d_prepacked_residual(const void* x, const void* packed, const void* b, const void* res, void* y,
+                                        const conv2d_desc_t* desc, conv_algo_t algo, void* workspace,
+                                        size_t workspace_bytes, void* stream);
+}
+
 namespace {
 
 // ---- kernels -------------------------------------------------------------
@@ -93,6 +99,7 @@ struct Value {
   int64_t d[4] = {0, 0, 0, 0};
   int producer = -1;  // op index; -1 for the input
   int alias = -1;     // flatten: the value whose storage this one shares
+  int falias = -1;    // planned: a fused add's output shares its convolution's storage
   int64_t offset = -1;
   int64_t bytes = 0;
   int64_t elems() const {
@@ -113,6 +120,12 @@ struct Op {
   const void* w = nullptr;
   const void* b = nullptr;
   int relu = 0;
+  // planned: residual value added in this convolution's epilogue (an add
+  // fused into it; -1: none), the ReLU that then follows it, and whether this
+  // op (a fused add) is skipped
+  int res = -1;
+  int relu_eff = 0;
+  bool skip = false;
   conv2d_desc_t desc{};
   int64_t pk_off = -1, pk_bytes = 0, bias_off = -1, ws_bytes = 0;
   // pooling
@@ -134,8 +147,11 @@ struct convsel_model {
   int64_t arena_bytes = 0, ws_off = 0, ws_bytes = 0;
   int64_t esize() const { return dtype == CONV_F32 ? 4 : 2; }
   int root(int v) const {
-    while (vals[v].alias >= 0) v = vals[v].alias;
-    return v;
+    for (;;) {
+      if (vals[v].alias >= 0) v = vals[v].alias;
+      else if (vals[v].falias >= 0) v = vals[v].falias;
+      else return v;
+    }
   }
 };
 
@@ -306,6 +322,12 @@ conv_status_t convsel_model_plan(convsel_model_t* model, int64_t n, int64_t c, i
   convsel_model_t& m = *model;
   m.planned = m.bound = false;
   const int64_t es = m.esize();
+  for (Op& op : m.ops) {
+    op.res = -1;
+    op.relu_eff = op.relu;
+    op.skip = false;
+  }
+  for (Value& v : m.vals) v.falias = -1;
   Value& in = m.vals[0];
   in.ndim = 4;
   in.d[0] = n; in.d[1] = c; in.d[2] = h; in.d[3] = w;
@@ -392,6 +414,43 @@ conv_status_t convsel_model_plan(convsel_model_t* model, int64_t n, int64_t c, i
     if (o.elems() >= ((int64_t)1 << 31)) return CONV_ERR_INVALID_ARG;
     o.bytes = o.elems() * es;
   }
+  // Residual adds into implicit GEMM convolutions: an add of a convolution's
+  // output X (read by nothing else, no ReLU of its own) and a value Y that
+  // exists before that convolution runs becomes that convolution's epilogue
+  // residual, y = relu(conv + b + Y); the add's output then shares X's storage.
+  {
+    const int nv0 = (int)m.vals.size();
+    std::vector<int> uses(nv0, 0);
+    for (const Op& op : m.ops) {
+      ++uses[op.in];
+      if (op.kind == OP_ADD) ++uses[op.in2];
+    }
+    ++uses[m.output];
+    for (int i = 0; i < (int)m.ops.size(); ++i) {
+      Op& add = m.ops[i];
+      if (add.kind != OP_ADD) continue;
+      int best = -1, other = -1;
+      for (int side = 0; side < 2; ++side) {
+        const int X = side == 0 ? add.in : add.in2, Y = side == 0 ? add.in2 : add.in;
+        const int p = m.vals[X].producer;
+        if (p < 0 || m.vals[X].alias >= 0 || uses[X] != 1) continue;
+        const Op& c = m.ops[p];
+        if (c.kind != OP_CONV || c.algo_run != CONV_ALGO_IMPLICIT_GEMM || c.relu_eff || c.res >= 0) continue;
+        if (m.vals[m.root(Y)].producer >= p) continue;  // Y must exist when the convolution runs
+        if (best < 0 || p > m.vals[best].producer) {
+          best = X;
+          other = Y;
+        }
+      }
+      if (best < 0) continue;
+      Op& c = m.ops[m.vals[best].producer];
+      c.res = other;
+      c.relu_eff = add.relu;
+      c.desc.fuse_relu = add.relu;
+      add.skip = true;
+      m.vals[add.out].falias = best;
+    }
+  }
   // The output must come out of an operation, not be the input itself.
   const int out_root = m.root(m.output);
   if (out_root == 0) return CONV_ERR_UNSUPPORTED;
@@ -399,11 +458,13 @@ conv_status_t convsel_model_plan(convsel_model_t* model, int64_t n, int64_t c, i
   const int nv = (int)m.vals.size();
   std::vector<int> last(nv, -1), first(nv, -1);
   for (int i = 0; i < nv; ++i)
-    if (m.vals[i].alias < 0) first[i] = last[i] = m.vals[i].producer;
+    if (m.vals[i].alias < 0 && m.vals[i].falias < 0) first[i] = last[i] = m.vals[i].producer;
   for (int i = 0; i < (int)m.ops.size(); ++i) {
     const Op& op = m.ops[i];
+    if (op.skip) continue;
     last[m.root(op.in)] = std::max(last[m.root(op.in)], i);
     if (op.kind == OP_ADD) last[m.root(op.in2)] = std::max(last[m.root(op.in2)], i);
+    if (op.res >= 0) last[m.root(op.res)] = std::max(last[m.root(op.res)], i);
   }
   // The workspace, then the activations.
   m.ws_off = off;
@@ -411,7 +472,7 @@ conv_status_t convsel_model_plan(convsel_model_t* model, int64_t n, int64_t c, i
   const int64_t act_base = off;
   std::vector<int> order;
   for (int i = 1; i < nv; ++i)
-    if (m.vals[i].alias < 0 && i != out_root) order.push_back(i);
+    if (m.vals[i].alias < 0 && m.vals[i].falias < 0 && i != out_root) order.push_back(i);
   std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return m.vals[a].bytes > m.vals[b].bytes; });
   std::vector<int> placed;
   int64_t act_top = 0;
@@ -495,11 +556,17 @@ conv_status_t convsel_model_forward(convsel_model_t* model, const void* x, void*
     const Value& vin = m.vals[op.in];
     const Value& vout = m.vals[op.out];
     conv_status_t s = CONV_OK;
+    if (op.skip) continue;  // an add fused into its convolution
     switch (op.kind) {
       case OP_CONV:
-        s = conv2d_prepacked(ptr(op.in), m.arena + op.pk_off, op.b ? m.arena + op.bias_off : nullptr, ptr(op.out),
-                             &op.desc, op.algo_run, op.ws_bytes ? m.arena + m.ws_off : nullptr, (size_t)op.ws_bytes,
-                             stream);
+        if (op.res >= 0)
+          s = convsel::conv2d_prepacked_residual(
+              ptr(op.in), m.arena + op.pk_off, op.b ? m.arena + op.bias_off : nullptr, ptr(op.res), ptr(op.out),
+              &op.desc, op.algo_run, op.ws_bytes ? m.arena + m.ws_off : nullptr, (size_t)op.ws_bytes, stream);
+        else
+          s = conv2d_prepacked(ptr(op.in), m.arena + op.pk_off, op.b ? m.arena + op.bias_off : nullptr, ptr(op.out),
+                               &op.desc, op.algo_run, op.ws_bytes ? m.arena + m.ws_off : nullptr, (size_t)op.ws_bytes,
+                               stream);
         break;
       case OP_FLATTEN:
         break;
@@ -530,7 +597,9 @@ conv_status_t convsel_model_describe(const convsel_model_t* model, char* buf, si
              (long long)o.d[0], (long long)o.d[1], (long long)o.d[2], (long long)o.d[3]);
     d += line;
     if (op.kind == OP_CONV) d += std::string(" algo=") + conv2d_algo_name(model->planned ? op.algo_run : op.algo);
-    if (op.relu) d += " relu";
+    if (model->planned && op.res >= 0) d += " + v" + std::to_string(op.res);
+    if (model->planned ? (op.kind == OP_CONV ? op.relu_eff : op.relu) : op.relu) d += " relu";
+    if (model->planned && op.skip) d += " fused";
     if (model->planned) {
       snprintf(line, sizeof(line), " offset=%lld", (long long)(model->root(op.out) == model->root(model->output)
                                                                      ? -1

@@ -65,6 +65,22 @@ class ResNetSmall(nn.Module):
         return self.fc(self.drop(torch.flatten(self.gap(x), 1)))
 
 
+class ConvPlusResidual(nn.Module):
+    """One convolution plus the input (or a 1 x 1 projection of it when the
+    shapes differ), optionally followed by a ReLU."""
+
+    def __init__(self, c, k, r, stride, pad, relu):
+        super().__init__()
+        self.proj = None if (c == k and stride == 1) else nn.Conv2d(c, k, 1, stride, 0)
+        self.conv = nn.Conv2d(c, k, r, stride, pad)
+        self.relu = relu
+
+    def forward(self, x):
+        idt = x if self.proj is None else self.proj(x)
+        y = self.conv(x) + idt
+        return torch.relu(y) if self.relu else y
+
+
 def randomize_bn(model, seed):
     """Non-trivial running statistics and affine parameters."""
     g = torch.Generator().manual_seed(seed)

@@ -39,19 +39,38 @@ def test_residual_net_lowering_fuses_and_folds():
     d = m._native.describe().splitlines()
     assert d[0].startswith("0 conv v0 -> v1 [3 16 32 32]") and d[0].split()[-2] == "relu"
     assert "add v" in d[4] and " relu " in d[4] + " "
+    # Both residual adds are fused into the epilogue of the convolution that
+    # produces one operand; that convolution reads the other operand and takes
+    # over the add's ReLU, and the add's output is the convolution's output.
+    fused = [line for line in d if " add " in " " + line]
+    assert len(fused) == 2 and all(line.split()[-2] == "fused" for line in fused)
+    for line in fused:
+        toks = line.split()
+        a, b = int(toks[2][1:]), int(toks[4][1:])
+        convs = [c for c in d if c.split()[1] == "conv" and c.split()[4] in ("v%d" % a, "v%d" % b)
+                 and " + v" in c]
+        assert len(convs) == 1
+        ctoks = convs[0].split()
+        x = int(ctoks[4][1:])
+        y = b if x == a else a
+        assert ctoks[ctoks.index("+") + 1] == "v%d" % y and ctoks[ctoks.index("+") + 2] == "relu"
     # Arena plan: values live at the same time never share bytes, all within
-    # the arena, 256-byte aligned.
-    reads, prod = [], {}
+    # the arena, 256-byte aligned.  A fused add's output is stored where the
+    # convolution's output is, so its reads extend that value's lifetime.
+    reads, prod, alias = [], {}, {}
     for i, line in enumerate(d[:-1]):
         toks = line.split()
         ins = [int(t[1:]) for t in toks[2:toks.index("->")] if t.startswith("v")]
         out = int(toks[toks.index("->") + 1][1:])
         reads.append(ins)
         prod[out] = i
+        if toks[-2] == "fused":
+            alias[out] = [v for v in ins if "+ v" in d[prod[v]]][0]
     last = dict(prod)
     for i, ins in enumerate(reads):
         for v in ins:
-            last[v] = max(last.get(v, -1), i)
+            r = alias.get(v, v)
+            last[r] = max(last.get(r, -1), i)
     place = {}
     for v in prod:
         off, nb = m._native.placement(v)
@@ -61,7 +80,9 @@ def test_residual_net_lowering_fuses_and_folds():
     # flatten's output shares its input's storage
     fl = [i for i, (k, _) in enumerate(m.ops) if k == "flatten"][0]
     assert m._native.placement(fl + 1)[0] == m._native.placement(fl)[0]
-    roots = {v: p for v, p in place.items() if m.ops[prod[v]][0] != "flatten"}
+    for v, x in alias.items():
+        assert place[v] == place[x]
+    roots = {v: p for v, p in place.items() if m.ops[prod[v]][0] != "flatten" and v not in alias}
     for a, b in itertools.combinations(roots, 2):
         la, lb = (prod[a], last[a]), (prod[b], last[b])
         if la[0] <= lb[1] and lb[0] <= la[1]:

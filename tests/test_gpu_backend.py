@@ -8,14 +8,17 @@ that do not amplify relative error, stays within their sum; bf16 networks
 4e-2 -- each of up to eight layers rounds its output to bf16 (relative
 2^-9 ~ 2e-3), the folded batch-norm filters are rounded once more, and the
 reference keeps every intermediate in float64, so the rounding adds up over
-the chain (twice the single-layer bf16 bar)."""
+the chain (twice the single-layer bf16 bar).  A single convolution with a
+fused residual add is held to the single-layer bars: 1e-4 (fp32) and 2e-2
+(bf16: the convolution's output and the sum are each rounded once)."""
 import numpy as np
 import pytest
 import torch
 
 import paper_2410_08300_amd as cs
 from gpu_util import rel_err, f64, say
-from nets import ConvNet, ResNetSmall, randomize_bn
+from paper_2410_08300_amd import _lib
+from nets import ConvNet, ConvPlusResidual, ResNetSmall, randomize_bn
 
 pytestmark = pytest.mark.gpu
 
@@ -98,3 +101,55 @@ def test_new_shape_replans_and_graph_replays_match_eager():
         assert torch.equal(out, eager), "replay %d" % i
         _ = model(torch.randn(5, 3, 64, 64, device=DEV))   # eager work in between
         torch.cuda.synchronize()
+
+
+# One convolution whose output is added to the network input (or to a 1 x 1
+# projection of it): every implicit GEMM kernel variant the library picks,
+# with and without split-K, planes below eight pixels over several images,
+# with and without the ReLU after the add.  (dtype, N, C, H, W, K, R, stride,
+# pad, ReLU, kernel the convolution runs)
+RESIDUAL = [
+    ("bf16", 4, 64, 14, 14, 256, 1, 1, 0, True, "pointwise_dma_kernel<4,4,4>"),
+    ("bf16", 4, 256, 14, 14, 64, 1, 1, 0, False, "pointwise_dma_kernel<4,4,4>;splitk_reduce_kernel"),
+    ("bf16", 5, 64, 2, 3, 96, 1, 1, 0, True, "pointwise_dma_kernel<16,4,4>"),
+    ("bf16", 4, 1024, 7, 7, 256, 1, 1, 0, True, "pointwise_dma_kernel<16,4,4>;splitk_reduce_kernel"),
+    ("bf16", 3, 64, 3, 3, 64, 1, 1, 0, False, "pointwise_dma_kernel<16,4,4>"),
+    ("bf16", 2, 64, 28, 28, 64, 3, 1, 1, True, "implicit_ws_kernel<64,1,1>;splitk_reduce_kernel"),
+    ("bf16", 3, 32, 8, 8, 32, 3, 1, 1, False, "implicit_ws_kernel<64,1,1>"),
+    ("bf16", 2, 256, 7, 7, 256, 3, 1, 1, True, "implicit_ws_kernel<128,0,1>;splitk_reduce_kernel"),
+    ("bf16", 7, 48, 2, 2, 64, 3, 1, 1, True, "implicit_gemm_kernel<bf16,64,2,9>;splitk_reduce_kernel"),
+    ("bf16", 2, 3, 32, 32, 16, 3, 1, 1, False, "implicit_gemm_kernel<bf16,64,1,9>"),
+    ("bf16", 2, 3, 64, 64, 64, 7, 2, 3, True, "implicit_rows_kernel"),
+    ("f32", 2, 64, 28, 28, 64, 3, 1, 1, True, "implicit_gemm_kernel<f32,64,2,9>;splitk_reduce_kernel"),
+    ("f32", 3, 16, 16, 16, 16, 3, 1, 1, False, "implicit_gemm_kernel<f32,64,2,9>"),
+    ("f32", 5, 64, 2, 3, 96, 1, 1, 0, True, "pointwise_gemm_kernel<f32,128,1,2>"),
+    ("f32", 4, 1024, 7, 7, 256, 1, 1, 0, False, "pointwise_gemm_kernel<f32,128,1,2>;splitk_reduce_kernel"),
+    ("f32", 4, 64, 56, 56, 256, 1, 1, 0, True, "pointwise_gemm_kernel<f32,128,0,2>"),
+    ("f32", 2, 3, 64, 64, 64, 7, 2, 3, False, "implicit_gemm_kernel<f32,64,1,0>"),
+]
+
+
+@pytest.mark.parametrize("case", RESIDUAL, ids=lambda c: "%s-%dx%dx%dx%d-k%d-r%d" % c[:7])
+def test_residual_add_fused_into_each_kernel(case):
+    dtype, n, c, h, w, k, r, stride, pad, relu, kernels = case
+    torch.manual_seed(11)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    net = ConvPlusResidual(c, k, r, stride, pad, relu).to(tdt).eval()
+    x = torch.randn(n, c, h, w).to(tdt)
+    ref = reference(net, x)
+    model = cs.swap_backend(net.to(DEV), {"conv": "implicit_gemm", "proj": "direct"})
+    model.plan(x.shape)
+    d = model.describe()
+    say("case residual-fused", case, d.splitlines()[-3:])
+    conv_line = [line for line in d.splitlines() if " conv v0 " in line and "implicit_gemm" in line][0]
+    assert " + v" in conv_line and (" relu " in conv_line + " ") == relu
+    assert any(line.split()[1] == "add" and " fused " in line + " " for line in d.splitlines())
+    desc = _lib.make_desc(n, c, h, w, k, r, r, stride, pad, dtype=dtype, bias=True)
+    assert "kernels=" in _lib.describe(desc, "implicit_gemm")
+    assert kernels in _lib.describe(desc, "implicit_gemm")
+    with torch.no_grad():
+        y = model(x.to(DEV))
+    torch.cuda.synchronize()
+    assert y.shape == ref.shape
+    err = rel_err(f64(y), ref)
+    assert err <= (1e-4 if dtype == "f32" else 2e-2), "%s: %.3e" % (case, err)
