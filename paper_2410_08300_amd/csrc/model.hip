@@ -45,31 +45,49 @@ __global__ __launch_bounds__(256) void add_kernel(const T* __restrict__ a, const
 }
 
 // One output element per thread; consecutive threads take consecutive q.
-// Max: padding never contributes.  Average: the window sum over the padded
-// input divided by kh*kw.
+// A workgroup covers 256 outputs of one plane (`tiles` workgroups per
+// plane), so the plane is a per-workgroup quantity and the per-thread index
+// arithmetic stays in 32 bits.  Max: padding never contributes.  Average:
+// the window sum over the padded input divided by kh*kw.
 template <typename T, bool MAX>
-__global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ x, T* __restrict__ y, int64_t total, int H,
+__global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ x, T* __restrict__ y, int tiles, int H,
                                                    int W, int P, int Q, int kh, int kw, int sh, int sw, int ph,
                                                    int pw) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (i >= total) return;
-  const int q = static_cast<int>(i % Q);
-  const int p = static_cast<int>((i / Q) % P);
-  const int64_t plane = i / (static_cast<int64_t>(P) * Q);
-  const T* xp = x + plane * H * W;
+  const int plane = blockIdx.x / tiles;
+  const int j = (blockIdx.x - plane * tiles) * 256 + threadIdx.x;
+  if (j >= P * Q) return;
+  const int p = j / Q, q = j - p * Q;
+  const T* xp = x + static_cast<int64_t>(plane) * H * W;
   float acc = MAX ? -INFINITY : 0.f;
+  const int ih0 = p * sh - ph, iw0 = q * sw - pw;
+  if (kh <= 3 && kw <= 3) {  // uniform: all taps' loads issued together, then one wait
+    float v[9];
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      const int ih = ih0 + t / 3, iw = iw0 + t % 3;
+      const bool ok = t / 3 < kh && t % 3 < kw && ih >= 0 && ih < H && iw >= 0 && iw < W;
+      v[t] = elem<T>::load(xp + (ok ? ih * W + iw : 0));
+      v[t] = ok ? v[t] : (MAX ? -INFINITY : 0.f);
+    }
+#pragma unroll
+    for (int t = 0; t < 9; ++t) acc = MAX ? fmaxf(acc, v[t]) : acc + v[t];
+    if (!MAX) acc /= static_cast<float>(kh * kw);
+    elem<T>::store(y + static_cast<int64_t>(plane) * P * Q + j, acc);
+    return;
+  }
   for (int r = 0; r < kh; ++r) {
-    const int ih = p * sh - ph + r;
+    const int ih = ih0 + r;
     if (ih < 0 || ih >= H) continue;
+    const T* row = xp + ih * W;
     for (int s = 0; s < kw; ++s) {
-      const int iw = q * sw - pw + s;
+      const int iw = iw0 + s;
       if (iw < 0 || iw >= W) continue;
-      const float v = elem<T>::load(xp + static_cast<int64_t>(ih) * W + iw);
+      const float v = elem<T>::load(row + iw);
       acc = MAX ? fmaxf(acc, v) : acc + v;
     }
   }
   if (!MAX) acc /= static_cast<float>(kh * kw);
-  elem<T>::store(y + i, acc);
+  elem<T>::store(y + static_cast<int64_t>(plane) * P * Q + j, acc);
 }
 
 // Global average: one wave per plane, lanes stride the plane, then a fixed
@@ -190,16 +208,20 @@ hipError_t launch_elementwise(const Op& op, const void* a, const void* b, void* 
                          reinterpret_cast<const T*>(a), reinterpret_cast<const T*>(b), reinterpret_cast<T*>(y),
                          vout.elems(), op.relu);
       break;
-    case OP_POOL:
+    case OP_POOL: {
+      // Planning keeps planes * tiles and every plane's size below 2^31.
+      const int tiles = (int)blocks_for(vout.d[2] * vout.d[3]);
+      const dim3 grid((unsigned)(vout.d[0] * vout.d[1] * tiles));
       if (op.pool_kind == 0)
-        hipLaunchKernelGGL((pool_kernel<T, true>), dim3(blocks_for(vout.elems())), dim3(256), 0, st,
-                           reinterpret_cast<const T*>(a), reinterpret_cast<T*>(y), vout.elems(), (int)vin.d[2],
-                           (int)vin.d[3], (int)vout.d[2], (int)vout.d[3], op.kh, op.kw, op.sh, op.sw, op.ph, op.pw);
+        hipLaunchKernelGGL((pool_kernel<T, true>), grid, dim3(256), 0, st, reinterpret_cast<const T*>(a),
+                           reinterpret_cast<T*>(y), tiles, (int)vin.d[2], (int)vin.d[3], (int)vout.d[2],
+                           (int)vout.d[3], op.kh, op.kw, op.sh, op.sw, op.ph, op.pw);
       else
-        hipLaunchKernelGGL((pool_kernel<T, false>), dim3(blocks_for(vout.elems())), dim3(256), 0, st,
-                           reinterpret_cast<const T*>(a), reinterpret_cast<T*>(y), vout.elems(), (int)vin.d[2],
-                           (int)vin.d[3], (int)vout.d[2], (int)vout.d[3], op.kh, op.kw, op.sh, op.sw, op.ph, op.pw);
+        hipLaunchKernelGGL((pool_kernel<T, false>), grid, dim3(256), 0, st, reinterpret_cast<const T*>(a),
+                           reinterpret_cast<T*>(y), tiles, (int)vin.d[2], (int)vin.d[3], (int)vout.d[2],
+                           (int)vout.d[3], op.kh, op.kw, op.sh, op.sw, op.ph, op.pw);
       break;
+    }
     case OP_GAP:
       hipLaunchKernelGGL(global_avgpool_kernel<T>, dim3(blocks_for(vin.d[0] * vin.d[1], 4)), dim3(256), 0, st,
                          reinterpret_cast<const T*>(a), reinterpret_cast<T*>(y), vin.d[0] * vin.d[1],
@@ -392,7 +414,7 @@ conv_status_t convsel_model_plan(convsel_model_t* model, int64_t n, int64_t c, i
         break;
       }
       case OP_POOL: {
-        if (a.ndim != 4) return CONV_ERR_INVALID_ARG;
+        if (a.ndim != 4 || a.elems() >= ((int64_t)1 << 31)) return CONV_ERR_INVALID_ARG;  // 32-bit plane offsets
         const int64_t P = (a.d[2] + 2 * op.ph - op.kh) / op.sh + 1;
         const int64_t Q = (a.d[3] + 2 * op.pw - op.kw) / op.sw + 1;
         if (a.d[2] + 2 * op.ph < op.kh || a.d[3] + 2 * op.pw < op.kw || P < 1 || Q < 1) return CONV_ERR_INVALID_ARG;
