@@ -152,3 +152,72 @@ def test_library_exports_model_functions():
     L = _lib.lib()
     for n in names:
         assert hasattr(L, n), n
+
+
+def _lowered(net, shape):
+    m = cs.swap_backend(net, "implicit_gemm")
+    m._native.plan(*shape)
+    return m._native.describe().splitlines()[:-1]
+
+
+def test_residual_fusion_only_where_it_is_exact():
+    """An add goes into a convolution's epilogue only when that is the same
+    computation: the convolution's output is read by nothing else, the
+    convolution has no ReLU of its own, and the other operand already
+    exists when the convolution runs."""
+    class Twice(nn.Module):          # conv output read twice: by the add and by the output add
+        def __init__(self):
+            super().__init__()
+            self.c = nn.Conv2d(8, 8, 3, 1, 1)
+
+        def forward(self, x):
+            y = self.c(x)
+            return (y + x) + y
+
+    class Relu(nn.Module):           # the conv's own ReLU comes before the add
+        def __init__(self):
+            super().__init__()
+            self.c = nn.Conv2d(8, 8, 3, 1, 1)
+
+        def forward(self, x):
+            return torch.relu(self.c(x)) + x
+
+    class Later(nn.Module):          # the other operand is computed after the conv
+        def __init__(self):
+            super().__init__()
+            self.a = nn.Conv2d(8, 8, 3, 1, 1)
+            self.b = nn.Conv2d(8, 8, 1)
+
+        def forward(self, x):
+            y = self.a(x)
+            z = self.b(x)
+            return y + z
+
+    class Self(nn.Module):           # y + y
+        def __init__(self):
+            super().__init__()
+            self.c = nn.Conv2d(8, 8, 3, 1, 1)
+
+        def forward(self, x):
+            y = self.c(x)
+            return y + y
+
+    class Plain(nn.Module):          # fused: conv(x) + x, then ReLU
+        def __init__(self):
+            super().__init__()
+            self.c = nn.Conv2d(8, 8, 3, 1, 1)
+
+        def forward(self, x):
+            return torch.relu(self.c(x) + x)
+
+    shape = (2, 8, 6, 6)
+    for net in (Twice(), Relu(), Self()):
+        d = _lowered(net, shape)
+        assert not any(" fused" in line for line in d), (type(net).__name__, d)
+        assert not any(" + v" in line for line in d if " conv " in line)
+    d = _lowered(Later(), shape)
+    # b runs after a, so a cannot take z as its residual, but b can take a's output
+    conv_b = [line for line in d if line.startswith("1 conv")][0]
+    assert " + v1" in conv_b and any(line.split()[1] == "add" and " fused" in line for line in d)
+    d = _lowered(Plain(), shape)
+    assert d[0].startswith("0 conv v0 -> v1") and " + v0 relu " in d[0] + " " and d[1].endswith("fused offset=-1")
