@@ -153,3 +153,29 @@ def test_residual_add_fused_into_each_kernel(case):
     assert y.shape == ref.shape
     err = rel_err(f64(y), ref)
     assert err <= (1e-4 if dtype == "f32" else 2e-2), "%s: %.3e" % (case, err)
+
+
+def test_resnet50_through_the_executor():
+    """ResNet-50 v1.5 (53 convolutions with folded batch norm, 16 residual
+    adds fused into epilogues, max-pool, global average pool, linear head)
+    in fp32 at batch 2, 64 x 64, each layer on the library's default choice,
+    against the module in fp64 on the CPU: within 1e-3 (fp32 layers are
+    within 1e-4 of their own outputs, 1e-3 for Winograd; normalisation keeps
+    the magnitudes from growing along the chain)."""
+    import bench
+    torch.manual_seed(5)
+    net = randomize_bn(bench.resnet50_module(), 13)
+    x = torch.randn(2, 3, 64, 64)
+    ref = reference(net, x)
+    model = cs.swap_backend(net.to(DEV), "default")
+    model.plan(x.shape)
+    d = model.describe()
+    assert sum(" fused" in line for line in d.splitlines()) == 16
+    say("case resnet50 fp32", len(model.ops), "ops")
+    with torch.no_grad():
+        y = model(x.to(DEV))
+    torch.cuda.synchronize()
+    assert y.shape == ref.shape == (2, 1000)
+    err = rel_err(f64(y), ref)
+    say("resnet50 fp32 rel err %.3e" % err)
+    assert err <= 1e-3
