@@ -30,7 +30,12 @@
  *      arena laid out for filter packages, biases, intermediate values and
  *      the largest convolution workspace.  Intermediate values share arena
  *      space when their lifetimes (producer to last reader) do not overlap.
- *      Host only.
+ *      An add whose operand is the output of an implicit-GEMM convolution
+ *      (read by nothing else, without a ReLU of its own) and whose other
+ *      operand exists before that convolution runs is fused into it: the
+ *      convolution's epilogue adds the other operand and applies the add's
+ *      ReLU, y = relu(round(conv + b) + other), and the add launches
+ *      nothing.  Host only.
  *   3. convsel_model_bind(arena): the caller provides the arena (at least the
  *      planned bytes, 256-byte aligned); the library packs every filter and
  *      copies every bias into it, on `stream`.
