@@ -289,20 +289,6 @@ __device__ __forceinline__ void store_block(const f32x16_t (&acc)[MI][NJ], float
   }
 }
 
-// Epilogue of a wave that holds 32 output channels x 128 pixels as four
-// transposed 32 x 32 blocks (the MFMA computed pixels x channels: block nj,
-// accumulator v of lane l is channel l % 32, pixel nj*32 + 8 (v/4) +
-// 4 (l/32) + v % 4, so a lane holds runs of 4 consecutive pixels of one
-// channel).  Bias, ReLU and the rounding to T happen in registers; the block
-// is staged once in LDS (`stage`: 8 KiB, [channel][128 pixels] in 16-byte
-// units XOR-swizzled by the channel) and leaves as whole 256-byte channel
-// rows, four per store instruction, the pattern that reaches the HBM write
-// rate.  A run of 8 pixels inside one image is one 16-byte store (2-byte
-// alignment is enough on gfx950); a run that crosses an image boundary or
-// passes the last pixel is stored element by element.  Split-K partials
-// (fp32) are staged in two halves of 64 pixels.  Precondition (the callers'
-// plans guarantee it): a run crosses at most one image boundary, i.e.
-// P*Q >= 8 or the tile index space pads planes to a multiple of 8.
 // A run of 8 pixels starting at tile pixel `px` (tile origin col0, channel
 // block row0 of group g): where its first channel row goes and whether it is
 // whole.
@@ -324,6 +310,20 @@ __device__ __forceinline__ Run128t run128t(const EpiArgs& e, int row0, int col0,
   return r;
 }
 
+// Epilogue of a wave that holds 32 output channels x 128 pixels as four
+// transposed 32 x 32 blocks (the MFMA computed pixels x channels: block nj,
+// accumulator v of lane l is channel l % 32, pixel nj*32 + 8 (v/4) +
+// 4 (l/32) + v % 4, so a lane holds runs of 4 consecutive pixels of one
+// channel).  Bias, ReLU and the rounding to T happen in registers; the block
+// is staged once in LDS (`stage`: 8 KiB, [channel][128 pixels] in 16-byte
+// units XOR-swizzled by the channel) and leaves as whole 256-byte channel
+// rows, four per store instruction, the pattern that reaches the HBM write
+// rate.  A run of 8 pixels inside one image is one 16-byte store (2-byte
+// alignment is enough on gfx950); a run that crosses an image boundary or
+// passes the last pixel is stored element by element.  Split-K partials
+// (fp32) are staged in two halves of 64 pixels.  Precondition (the callers'
+// plans guarantee it): a run crosses at most one image boundary, i.e.
+// P*Q >= 8 or the tile index space pads planes to a multiple of 8.
 template <typename T>
 __device__ __forceinline__ void store_block128t(const f32x16_t (&acc)[1][4], float* stage_f, const EpiArgs& e,
                                                 int row0, int col0, int g, int split) {
