@@ -514,7 +514,9 @@ typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 // Sum of the split partials, plus bias, ReLU, rounding to the output type;
-// four consecutive outputs per thread (flat index: outputs stay below 2^31).
+// four consecutive outputs per thread (flat index: outputs stay below 2^31),
+// read and written as one vector when all four exist; the channel of each
+// output is found with one division per thread, then stepped.
 template <typename T>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, const T* __restrict__ bias,
                                                             T* __restrict__ y, int total, int slab, int PQ, int K,
@@ -532,10 +534,42 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
       for (int e = 0; e < n4; ++e) sum[e] += p[e];
     }
   }
+  if (bias) {
+    const int plane = i0 / PQ;
+    int q = i0 - plane * PQ, ch = plane % K;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (e > 0 && ++q == PQ) {
+        q = 0;
+        if (++ch == K) ch = 0;
+      }
+      sum[e] += elem<T>::load(bias + ch);
+    }
+  }
+  typedef typename elem<T>::storage S;
+  if (n4 == 4) {
+    if (res) {  // see EpiArgs::res
+      S r[4];
+      __builtin_memcpy(r, res + i0, sizeof(r));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        T re;
+        __builtin_memcpy(&re, &r[e], sizeof(T));
+        sum[e] = elem<T>::to_f32(elem<T>::from_f32(sum[e])) + elem<T>::to_f32(re);
+      }
+    }
+    S o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const T t = elem<T>::from_f32(relu ? fmaxf(sum[e], 0.f) : sum[e]);
+      __builtin_memcpy(&o[e], &t, sizeof(T));
+    }
+    __builtin_memcpy(y + i0, o, sizeof(o));
+    return;
+  }
   for (int e = 0; e < n4; ++e) {
     const int i = i0 + e;
     float v = sum[e];
-    if (bias) v += elem<T>::load(bias + (i / PQ) % K);
     if (res) v = elem<T>::to_f32(elem<T>::from_f32(v)) + elem<T>::load(res + i);  // see EpiArgs::res
     if (relu) v = fmaxf(v, 0.f);
     elem<T>::store(y + i, v);
