@@ -514,31 +514,42 @@ typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 // Sum of the split partials, plus bias, ReLU, rounding to the output type;
-// four consecutive outputs per thread (flat index: outputs stay below 2^31),
-// read and written as one vector when all four exist; the channel of each
-// output is found with one division per thread, then stepped.
+// kReducePer consecutive outputs per thread (flat index: outputs stay below
+// 2^31), read and written as vectors when all of them exist; the channel of
+// each output is found with one division per thread, then stepped.
+constexpr int kReducePer = 4;
+inline unsigned reduce_blocks(int total) { return (unsigned)((total + 256 * kReducePer - 1) / (256 * kReducePer)); }
+
 template <typename T>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, const T* __restrict__ bias,
                                                             T* __restrict__ y, int total, int slab, int PQ, int K,
                                                             int splits, int relu, const T* __restrict__ res) {
-  const int i0 = (blockIdx.x * 256 + threadIdx.x) * 4;
-  if (i0 >= total) return;
-  const int n4 = total - i0 < 4 ? total - i0 : 4;
-  float sum[4] = {0.f, 0.f, 0.f, 0.f};
+  constexpr int R = kReducePer;
+  static_assert(R % 4 == 0, "whole float4 partial loads");
+  const int64_t i0l = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * R;
+  if (i0l >= total) return;
+  const int i0 = static_cast<int>(i0l);
+  const int nr = total - i0 < R ? total - i0 : R;
+  float sum[R];
+#pragma unroll
+  for (int e = 0; e < R; ++e) sum[e] = 0.f;
   for (int s = 0; s < splits; ++s) {
     const float* p = part + static_cast<int64_t>(s) * slab + i0;
-    if (n4 == 4) {
-      const float4 v = *reinterpret_cast<const float4*>(p);  // slabs and i0 are multiples of 4 floats
-      sum[0] += v.x; sum[1] += v.y; sum[2] += v.z; sum[3] += v.w;
+    if (nr == R) {
+#pragma unroll
+      for (int e = 0; e < R; e += 4) {
+        const float4 v = *reinterpret_cast<const float4*>(p + e);  // slabs and i0 are multiples of 4 floats
+        sum[e] += v.x; sum[e + 1] += v.y; sum[e + 2] += v.z; sum[e + 3] += v.w;
+      }
     } else {
-      for (int e = 0; e < n4; ++e) sum[e] += p[e];
+      for (int e = 0; e < nr; ++e) sum[e] += p[e];
     }
   }
   if (bias) {
     const int plane = i0 / PQ;
     int q = i0 - plane * PQ, ch = plane % K;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
+    for (int e = 0; e < R; ++e) {
       if (e > 0 && ++q == PQ) {
         q = 0;
         if (++ch == K) ch = 0;
@@ -547,27 +558,27 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     }
   }
   typedef typename elem<T>::storage S;
-  if (n4 == 4) {
+  if (nr == R) {
     if (res) {  // see EpiArgs::res
-      S r[4];
+      S r[R];
       __builtin_memcpy(r, res + i0, sizeof(r));
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
+      for (int e = 0; e < R; ++e) {
         T re;
         __builtin_memcpy(&re, &r[e], sizeof(T));
         sum[e] = elem<T>::to_f32(elem<T>::from_f32(sum[e])) + elem<T>::to_f32(re);
       }
     }
-    S o[4];
+    S o[R];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
+    for (int e = 0; e < R; ++e) {
       const T t = elem<T>::from_f32(relu ? fmaxf(sum[e], 0.f) : sum[e]);
       __builtin_memcpy(&o[e], &t, sizeof(T));
     }
     __builtin_memcpy(y + i0, o, sizeof(o));
     return;
   }
-  for (int e = 0; e < n4; ++e) {
+  for (int e = 0; e < nr; ++e) {
     const int i = i0 + e;
     float v = sum[e];
     if (res) v = elem<T>::to_f32(elem<T>::from_f32(v)) + elem<T>::load(res + i);  // see EpiArgs::res

@@ -1023,7 +1023,7 @@ hipError_t launch_one(const IgPlan& pl, const IgArgs& a, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.e.splits == 1) return e;
   const int total = a.N * a.K * a.P * a.Q;
-  hipLaunchKernelGGL(splitk_reduce_kernel<T>, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, stream,
+  hipLaunchKernelGGL(splitk_reduce_kernel<T>, dim3(reduce_blocks(total)), dim3(256), 0, stream,
                      a.e.partial, reinterpret_cast<const T*>(a.e.b), reinterpret_cast<T*>(a.e.y), total, a.e.slab,
                      a.P * a.Q, a.K, a.e.splits, a.e.relu, reinterpret_cast<const T*>(a.e.res));
   return hipGetLastError();
@@ -1185,7 +1185,7 @@ hipError_t pw_dma_launch(const PwPlan& pl, const PwArgs& a, hipStream_t stream) 
   if (e != hipSuccess || a.e.splits == 1) return e;
   // Outputs: images x K x P*Q (a.NPQ counts the padded pixel span).
   const int total = (int)((int64_t)(a.NPQ / a.e.span) * a.e.PQ * a.e.K);
-  hipLaunchKernelGGL(splitk_reduce_kernel<bf16_t>, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, stream,
+  hipLaunchKernelGGL(splitk_reduce_kernel<bf16_t>, dim3(reduce_blocks(total)), dim3(256), 0, stream,
                      a.e.partial, reinterpret_cast<const bf16_t*>(a.e.b), reinterpret_cast<bf16_t*>(a.e.y), total,
                      a.e.slab, a.e.PQ, a.e.K, a.e.splits, a.e.relu, reinterpret_cast<const bf16_t*>(a.e.res));
   return hipGetLastError();
@@ -1198,7 +1198,7 @@ hipError_t pw_launch(const PwPlan& pl, const PwArgs& a, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.e.splits == 1) return e;
   const int total = (int)((int64_t)a.NPQ * a.e.K);
-  hipLaunchKernelGGL(splitk_reduce_kernel<T>, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, stream,
+  hipLaunchKernelGGL(splitk_reduce_kernel<T>, dim3(reduce_blocks(total)), dim3(256), 0, stream,
                      a.e.partial, reinterpret_cast<const T*>(a.e.b), reinterpret_cast<T*>(a.e.y), total, a.e.slab,
                      a.e.PQ, a.e.K, a.e.splits, a.e.relu, reinterpret_cast<const T*>(a.e.res));
   return hipGetLastError();

@@ -422,7 +422,7 @@ hipError_t ws_launch(const WsPlan& pl, const WsArgs& a, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.e.splits == 1) return e;
   const int total = a.N * a.K * a.P * a.Q;
-  hipLaunchKernelGGL(splitk_reduce_kernel<bf16_t>, dim3((unsigned)((total + 1023) / 1024)), dim3(256), 0, stream,
+  hipLaunchKernelGGL(splitk_reduce_kernel<bf16_t>, dim3(reduce_blocks(total)), dim3(256), 0, stream,
                      a.e.partial, reinterpret_cast<const bf16_t*>(a.e.b), reinterpret_cast<bf16_t*>(a.e.y), total,
                      a.e.slab, a.P * a.Q, a.K, a.e.splits, a.e.relu, reinterpret_cast<const bf16_t*>(a.e.res));
   return hipGetLastError();
