@@ -869,34 +869,41 @@ __global__ __launch_bounds__(256) void repack_plane_kernel(const uint16_t* __res
     for (int e = 0; e < 8; ++e) v[e] = pix0 + e < PQ ? v[e] : 0u;
   } else if (sw <= 2 && pix0 + 8 <= PQ && q0 + 8 <= Q && ih0 >= 0 && ih0 < H && iw0 >= 0 &&
              iw0 + 7 * sw < W && static_cast<int64_t>(ih0) * W + iw0 + 16 <= left) {
-    // Eight outputs of one row with every input inside the image: two
-    // 16-byte loads cover the (at most 15) input elements.
-    uint32_t a[8], b[8];
-    load8(static_cast<int64_t>(ih0) * W + iw0, a);
-    load8(static_cast<int64_t>(ih0) * W + iw0 + 8, b);
+    // Eight outputs of one row with every input inside the image: one
+    // 16-byte load (column stride 1) or two (stride 2: the even elements of
+    // 16), both issued before either is unpacked.
+    const uint16_t* row = src + static_cast<int64_t>(ih0) * W + iw0;
     if (sw == 1) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = a[e];
+      load8(row - src, v);
     } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        v[e] = a[2 * e];
-        v[e + 4] = b[2 * e];
-      }
+      uint4 ua, ub;
+      __builtin_memcpy(&ua, row, 16);
+      __builtin_memcpy(&ub, row + 8, 16);
+      v[0] = ua.x & 0xFFFFu; v[1] = ua.y & 0xFFFFu; v[2] = ua.z & 0xFFFFu; v[3] = ua.w & 0xFFFFu;
+      v[4] = ub.x & 0xFFFFu; v[5] = ub.y & 0xFFFFu; v[6] = ub.z & 0xFFFFu; v[7] = ub.w & 0xFFFFu;
     }
   } else {
-    // Element by element, walking the 8 pixels along the output row.
+    // Element by element, walking the 8 pixels along the output row.  All
+    // eight loads are issued before any is used (an element outside the
+    // image reads the plane's first element and is then replaced by zero):
+    // one memory round trip per thread, not eight.
     int p = p0, q = q0;
+    int idx[8];
+    bool ok[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int ih = p * sh - ph, iw = q * sw - pw;
-      const bool ok = pix0 + e < PQ && ih >= 0 && ih < H && iw >= 0 && iw < W;
-      v[e] = ok ? src[ih * W + iw] : 0u;
+      ok[e] = pix0 + e < PQ && ih >= 0 && ih < H && iw >= 0 && iw < W;
+      idx[e] = ok[e] ? ih * W + iw : 0;
       if (++q == Q) {
         q = 0;
         ++p;
       }
     }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = src[idx[e]];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = ok[e] ? v[e] : 0u;
   }
   uint4 o;
   o.x = v[0] | (v[1] << 16);
