@@ -187,12 +187,18 @@ __global__ __launch_bounds__(256) void rows_pack_kernel(const uint16_t* __restri
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= units) return;
   const int k = i / UR, u = i - k * UR;
+  // All eight loads go out before any is used; a zero tap reads w[0] and is
+  // then replaced by zero.
   uint32_t v[8];
+  bool ok[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int s = e - lead;
-    v[e] = k < K && u < CR && s >= 0 && s < S ? w[(static_cast<int64_t>(k) * CR + u) * S + s] : 0u;
+    ok[e] = k < K && u < CR && s >= 0 && s < S;
+    v[e] = w[ok[e] ? (static_cast<int64_t>(k) * CR + u) * S + s : 0];
   }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = ok[e] ? v[e] : 0u;
   u32x4_t o;
 #pragma unroll
   for (int q = 0; q < 4; ++q) o[q] = v[2 * q] | (v[2 * q + 1] << 16);
