@@ -363,7 +363,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
               "(the convolution shards over the batch with no exchange step; see DESIGN.md)", file=sys.stderr)
         sys.exit(2)
 
