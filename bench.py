@@ -364,7 +364,7 @@ def main():
 
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the library has no multi-GPU path "
-              "(the convolution shards over the batch with no exchange step; see DESIGN.md)", file=sys.stderr)
+              "(the convolution shards over the batch with no exchange step)", file=sys.stderr)
         sys.exit(2)
 
     import torch
