@@ -77,59 +77,70 @@ __global__ __launch_bounds__(kThreads) void implicit_rows_kernel(RowArgs a) {
   // (image n, row ih), zero outside the image.  A load whose element lies
   // outside passes an offset past the buffer's end and reads zero.
   const int rows = a.C * a.VR;
+  // Filters: the package tile is the LDS image itself.
+  const int units = BM * a.UR;
+  const uint32_t wbase = static_cast<uint32_t>(blockIdx.y) * units * 16;
+  auto halo_off = [&](int row, int iw) -> uint32_t {  // byte offset of (row, iw), or kOut outside the image
+    const int c = row / a.VR, vv = vr_lo + row - c * a.VR;
+    const int n = vv / a.Hv, ih = vv - n * a.Hv - a.ph;
+    const bool ok = n < a.N && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
+    return ok ? (((static_cast<uint32_t>(n) * a.C + c) * a.H + ih) * a.W + iw) * 2 : kOut;
+  };
   if constexpr (VEC) {
+    // Halo chunks (16 bytes: 8 columns of one row) and filter units go out
+    // in one stream of loads, eight per thread before any is written, so a
+    // workgroup waits for memory once or twice before its first MFMA.
     const int cpr = a.BRS / 8;  // 16-byte chunks per halo row
     const int total = rows * cpr;
-    for (int i0 = tid; i0 < total; i0 += 4 * kThreads) {
-      u32x4_t v[4];
+    const int all = total + units;
+    for (int i0 = tid; i0 < all; i0 += 8 * kThreads) {
+      u32x4_t v[8];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
+      for (int t = 0; t < 8; ++t) {
         const int i = i0 + t * kThreads;
-        const int row = i / cpr, ch = i - row * cpr;
-        const int c = row / a.VR, vv = vr_lo + row - c * a.VR;
-        const int n = vv / a.Hv, ih = vv - n * a.Hv - a.ph, iw = ch * 8 - a.off;
-        const bool ok = i < total && n < a.N && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
-        const uint32_t o = (((static_cast<uint32_t>(n) * a.C + c) * a.H + ih) * a.W + iw) * 2;
-        v[t] = __builtin_amdgcn_raw_buffer_load_b128(xr, ok ? o : kOut, 0, 0);
+        if (i < total) {
+          const int row = i / cpr, ch = i - row * cpr;
+          v[t] = __builtin_amdgcn_raw_buffer_load_b128(xr, halo_off(row, ch * 8 - a.off), 0, 0);
+        } else {
+          const int u = i - total;
+          v[t] = __builtin_amdgcn_raw_buffer_load_b128(wr, u < units ? wbase + u * 16 : kOut, 0, 0);
+        }
       }
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
-        if (i0 + t * kThreads < total) reinterpret_cast<u32x4_t*>(Bs)[i0 + t * kThreads] = v[t];
+      for (int t = 0; t < 8; ++t) {
+        const int i = i0 + t * kThreads;
+        if (i < total)
+          reinterpret_cast<u32x4_t*>(Bs)[i] = v[t];
+        else if (i < all)
+          As[i - total] = v[t];
+      }
     }
   } else {
     for (int col = tid; col < a.BRS; col += kThreads) {
       const int iw = col - a.off;
-      const bool col_ok = iw >= 0 && iw < a.W;
       for (int r0 = 0; r0 < rows; r0 += 8) {
         uint32_t v[8];
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
           const int row = r0 + t;
-          const int c = row / a.VR, vv = vr_lo + row - c * a.VR;
-          const int n = vv / a.Hv, ih = vv - n * a.Hv - a.ph;
-          const bool ok = row < rows && col_ok && n < a.N && ih >= 0 && ih < a.H;
-          const uint32_t o = (((static_cast<uint32_t>(n) * a.C + c) * a.H + ih) * a.W + iw) * 2;
-          v[t] = buf_load_elem(xr, ok ? o : kOut, 0, (bf16_t*)nullptr);
+          v[t] = buf_load_elem(xr, row < rows ? halo_off(row, iw) : kOut, 0, (bf16_t*)nullptr);
         }
 #pragma unroll
         for (int t = 0; t < 8; ++t)
           if (r0 + t < rows) Bs[(r0 + t) * a.BRS + col] = static_cast<uint16_t>(v[t]);
       }
     }
-  }
-  // Filters: the package tile is the LDS image itself.
-  const int units = BM * a.UR;
-  const uint32_t wbase = static_cast<uint32_t>(blockIdx.y) * units * 16;
-  for (int i0 = tid; i0 < units; i0 += 4 * kThreads) {
-    u32x4_t v[4];
+    for (int i0 = tid; i0 < units; i0 += 4 * kThreads) {
+      u32x4_t v[4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int i = i0 + t * kThreads;
-      v[t] = __builtin_amdgcn_raw_buffer_load_b128(wr, i < units ? wbase + i * 16 : kOut, 0, 0);
+      for (int t = 0; t < 4; ++t) {
+        const int i = i0 + t * kThreads;
+        v[t] = __builtin_amdgcn_raw_buffer_load_b128(wr, i < units ? wbase + i * 16 : kOut, 0, 0);
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        if (i0 + t * kThreads < units) As[i0 + t * kThreads] = v[t];
     }
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-      if (i0 + t * kThreads < units) As[i0 + t * kThreads] = v[t];
   }
   for (int u = tid; u < a.CR; u += kThreads) {
     const int c = u / a.R, r = u - c * a.R;
