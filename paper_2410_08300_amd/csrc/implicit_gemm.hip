@@ -639,7 +639,9 @@ __global__ __launch_bounds__((4 + NL) * 64) void pointwise_dma_kernel(PwArgs a) 
   char* lds = reinterpret_cast<char*>(smem);
   vec16* staging = reinterpret_cast<vec16*>(lds + NS * kDmaStageBytes);  // 8 KiB per compute wave
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // The wave index is uniform: reading it into a scalar register keeps the
+  // DMA destinations (and so M0) in scalar arithmetic.
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool loader = wave >= 4;                        // waves 4.. issue the DMA, 0..3 multiply
   const int lw = loader ? wave - 4 : wave;
   const int half = lane >> 5, l32 = lane & 31;
@@ -682,37 +684,51 @@ __global__ __launch_bounds__((4 + NL) * 64) void pointwise_dma_kernel(PwArgs a) 
     constexpr int NPX = UB == 16 ? 1 : 4;
     uint32_t pixoff[NPX];
     int pix_unit = -1;
+    // Per-lane offsets of the current unit, recomputed only when the unit
+    // changes (the chunk's channel offset goes into the scalar offset): A
+    // row k0 + a_row[i], unit a_unit[i] (rows past K fall past the buffer);
+    // B the lane's pixel in channel row b_chan(i), or x_bytes past the last
+    // pixel.  Channels past C are masked only in a layer's last, partial
+    // chunk.
+    uint32_t a_vo[A_INS], b_vo[B_INS];
     auto issue = [&](int u_in, int ch_in, int st) {
       const int u = __builtin_amdgcn_readfirstlane(u_in);
       const int ch = __builtin_amdgcn_readfirstlane(ch_in);
-      const int tile = u / a.e.splits;
-      const int pt = tile / a.ktiles, kt = tile - pt * a.ktiles;
-      const int j0 = pt * BN, k0 = kt * BM, c0 = ch * CC;
+      const int c0 = ch * CC;
       if (u != pix_unit) {
         pix_unit = u;
+        const int tile = u / a.e.splits;
+        const int pt = tile / a.ktiles, kt = tile - pt * a.ktiles;
+        const int j0 = pt * BN, k0 = kt * BM;
 #pragma unroll
         for (int q = 0; q < NPX; ++q) {
           const int j = j0 + b_pix(q);
           const int n = j / a.HW, pix = j - n * a.HW;
           pixoff[q] = j < a.NPQ ? static_cast<uint32_t>((n * a.C * a.HW + pix) * 2) : a.x_bytes;
         }
+#pragma unroll
+        for (int i = 0; i < A_INS; ++i)
+          a_vo[i] = static_cast<uint32_t>(((k0 + a_row[i]) * a.C + a_unit[i] * 8) * 2);
+#pragma unroll
+        for (int i = 0; i < B_INS; ++i) {
+          const uint32_t po = pixoff[UB == 16 ? 0 : (i & 3)];
+          b_vo[i] = po != a.x_bytes ? po + static_cast<uint32_t>(b_chan(i)) * plane : a.x_bytes;
+        }
       }
+      const bool tail = c0 + CC > a.C;  // uniform
       char __attribute__((address_space(3)))* base =
           (char __attribute__((address_space(3)))*)(lds + st * kDmaStageBytes);
       const uint32_t wso = static_cast<uint32_t>(c0 * 2);
 #pragma unroll
       for (int i = 0; i < A_INS; ++i) {
-        const bool ok = c0 + a_unit[i] * 8 < a.C;  // rows past K fall past the buffer
-        const uint32_t vo = ok ? static_cast<uint32_t>(((k0 + a_row[i]) * a.C + a_unit[i] * 8) * 2) : a.w_bytes;
+        const uint32_t vo = (!tail || c0 + a_unit[i] * 8 < a.C) ? a_vo[i] : a.w_bytes;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void_t*)(base + (lw * A_INS + i) * 1024), 16, vo, wso, 0,
                                                  0);
       }
       const uint32_t xso = static_cast<uint32_t>(c0) * plane;
 #pragma unroll
       for (int i = 0; i < B_INS; ++i) {
-        const int c = b_chan(i);
-        const uint32_t po = pixoff[UB == 16 ? 0 : (i & 3)];
-        const uint32_t vo = (c0 + c < a.C && po != a.x_bytes) ? po + static_cast<uint32_t>(c) * plane : a.x_bytes;
+        const uint32_t vo = (!tail || c0 + b_chan(i) < a.C) ? b_vo[i] : a.x_bytes;
         lds_void_t* dst = (lds_void_t*)(base + 16384 + (lw * B_INS + i) * 64 * UB);
         if constexpr (UB == 16)
           __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, dst, 16, vo, xso, 0, 0);
