@@ -160,11 +160,16 @@ def _padding_pair(m):
 
 
 def _static_check(name, m, algo):
-    """Reject, at swap time, picks that cannot run whatever the input shape."""
-    if algo in ("torch", "default", "cached"):
+    """Reject, at swap time, picks that cannot run whatever the input shape.
+    Every choice but "torch" runs the library, whose convolutions pad with
+    zeros only: "default" and "cached" included."""
+    if algo == "torch":
         return
     if m.padding_mode != "zeros":
-        raise ValueError("%s: padding_mode=%r is not supported (zero padding only)" % (name, m.padding_mode))
+        raise ValueError("%s: padding_mode=%r is not supported by the library (zero padding only); "
+                         "select 'torch' for this module" % (name, m.padding_mode))
+    if algo in ("default", "cached"):
+        return
     if algo == "winograd":
         if tuple(m.kernel_size) != (3, 3) or tuple(m.stride) != (1, 1) or tuple(m.dilation) != (1, 1) \
                 or m.groups != 1:
@@ -204,6 +209,10 @@ class Conv2dSwap(nn.Module):
         algo = self.algo
         if algo == "torch":
             return self._torch_conv(x)
+        if self.padding_mode != "zeros":
+            # A table edit can name a library algorithm after the swap.
+            raise ValueError("%s: padding_mode=%r is not supported by the library (zero padding only); "
+                             "select 'torch' for this module" % (self.name, self.padding_mode))
         w = self.weight
         if algo == "cached":
             if self.table.cache is None:

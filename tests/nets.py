@@ -1,24 +1,40 @@
-"""Small inference networks shared by the executor tests (the paper's
-Listing 1 network and a residual network with batch norm, pooling and a
-linear head)."""
+"""Small inference networks shared by the executor and selection tests: a
+plain convolution stack built from a layer specification, and a residual
+network with batch norm, pooling and a linear head."""
 import torch
 from torch import nn
 
+# Two 3x3 convolutions around a 2x2 max-pool, each followed by a ReLU,
+# starting from the toy workload's layer (3 -> 16 channels, pad 1, bias).
+# Entries: ("conv", in, out, kernel, pad), ("relu",), ("maxpool", k),
+# ("flatten",).
+TOY_STACK = (("conv", 3, 16, 3, 1), ("relu",), ("maxpool", 2), ("conv", 16, 32, 3, 1), ("relu",),
+             ("flatten",))
 
-class ConvNet(nn.Module):
-    """The toy network of the paper's Listing 1."""
 
-    def __init__(self):
-        super().__init__()
-        self.conv1 = nn.Conv2d(3, 16, 3, padding=1)
-        self.maxpool = nn.MaxPool2d(2, 2)
-        self.conv2 = nn.Conv2d(16, 32, 3, padding=1)
+class ConvStack(nn.Sequential):
+    """A sequential network from a layer specification (see TOY_STACK);
+    its Conv2d modules are named "0", "3", ... by position."""
 
-    def forward(self, x):
-        x = torch.relu(self.conv1(x))
-        x = self.maxpool(x)
-        x = torch.relu(self.conv2(x))
-        return torch.flatten(x, 1)
+    def __init__(self, spec=TOY_STACK):
+        layers = []
+        for item in spec:
+            kind = item[0]
+            if kind == "conv":
+                _, ci, co, k, pad = item
+                layers.append(nn.Conv2d(ci, co, k, padding=pad))
+            elif kind == "relu":
+                layers.append(nn.ReLU())
+            elif kind == "maxpool":
+                layers.append(nn.MaxPool2d(item[1], item[1]))
+            elif kind == "flatten":
+                layers.append(nn.Flatten())
+            else:
+                raise ValueError("unknown layer kind %r" % (kind,))
+        super().__init__(*layers)
+
+    def conv_names(self):
+        return [n for n, m in self.named_children() if isinstance(m, nn.Conv2d)]
 
 
 class Block(nn.Module):

@@ -12,12 +12,12 @@ from torch import nn
 import oracle
 import paper_2410_08300_amd as cs
 from paper_2410_08300_amd import _lib, backend
-from nets import ConvNet, ResNetSmall, randomize_bn
+from nets import ConvStack, ResNetSmall, randomize_bn
 
 
 def test_listing1_lowering_and_plan():
-    m = cs.swap_backend(ConvNet(), ["direct", "smm"])
-    assert m.ops == [("conv", "conv1"), ("maxpool", "maxpool"), ("conv", "conv2"), ("flatten", "flatten")]
+    m = cs.swap_backend(ConvStack(), ["direct", "smm"])
+    assert m.ops == [("conv", "0"), ("maxpool", "2"), ("conv", "3"), ("flatten", "_5")]
     nbytes = m._native.plan(2, 3, 32, 32)
     assert m._native.output_shape() == (2, 32 * 16 * 16)
     d = m._native.describe()
@@ -119,10 +119,10 @@ def test_unsupported_nodes_and_errors():
     with pytest.raises(NotImplementedError):
         cs.swap_backend(nn.Sequential(nn.Conv2d(3, 4, 3), nn.ReLU(), nn.BatchNorm2d(4)))   # BN not after a conv
     with pytest.raises(ValueError):
-        cs.swap_backend(ConvNet(), ["direct"])                                            # list length
+        cs.swap_backend(ConvStack(), ["direct"])                                            # list length
     with pytest.raises(ValueError):
-        cs.swap_backend(ConvNet(), "torch")
-    m = cs.swap_backend(ConvNet())
+        cs.swap_backend(ConvStack(), "torch")
+    m = cs.swap_backend(ConvStack())
     with pytest.raises(_lib.Conv2dError):
         m._native.plan(2, 4, 32, 32)                  # 4 input channels, conv1 expects 3
     with pytest.raises(_lib.Conv2dError):

@@ -1,5 +1,7 @@
-"""GPU checks of the model executor (swap_backend): whole networks against
-the same modules evaluated in float64 on the CPU.
+"""GPU checks of the model executor (swap_backend): whole networks and each
+of the executor's own kernels against a float64 host reference built from
+the oracle's convolution and plain numpy definitions of batch norm, ReLU,
+pooling, adds and linear layers (tests/ref_net.py).
 
 Tolerances (max |y - ref| / max |ref| over the network output): fp32
 networks 1e-3 -- every convolution is within 1e-4 of its own output (1e-3
@@ -10,7 +12,9 @@ that do not amplify relative error, stays within their sum; bf16 networks
 reference keeps every intermediate in float64, so the rounding adds up over
 the chain (twice the single-layer bf16 bar).  A single convolution with a
 fused residual add is held to the single-layer bars: 1e-4 (fp32) and 2e-2
-(bf16: the convolution's output and the sum are each rounded once)."""
+(bf16: the convolution's output and the sum are each rounded once).  The
+pooling, ReLU and add kernels compute maxima, sums of at most 49 terms and
+single adds: 1e-6 in fp32, exact maxima and ReLU."""
 import numpy as np
 import pytest
 import torch
@@ -18,7 +22,8 @@ import torch
 import paper_2410_08300_amd as cs
 from gpu_util import rel_err, f64, say
 from paper_2410_08300_amd import _lib
-from nets import ConvNet, ConvPlusResidual, ResNetSmall, randomize_bn
+import ref_net
+from nets import ConvStack, ConvPlusResidual, ResNetSmall, randomize_bn
 
 pytestmark = pytest.mark.gpu
 
@@ -29,18 +34,15 @@ DEV = torch.device("cuda:0")
 
 
 def reference(net, x):
-    """The module in float64 on the CPU (the network's own definition)."""
-    import copy
-    ref = copy.deepcopy(net).to("cpu").double().eval()
-    with torch.no_grad():
-        return ref(x.double().cpu()).numpy()
+    """The network evaluated in float64 by the oracle and numpy."""
+    return ref_net.reference(net, x)
 
 
 @pytest.mark.parametrize("sel", ["default", ("direct", "smm"), ("kn2row", "implicit_precomp_gemm"),
                                  ("winograd", "im2col_gemm"), ("implicit_gemm", "implicit_gemm")])
 def test_listing1_network(sel):
     torch.manual_seed(0)
-    net = ConvNet().eval()
+    net = ConvStack().eval()
     x = torch.randn(2, 3, 32, 32)
     ref = reference(net, x)
     model = cs.swap_backend(net.to(DEV), list(sel) if isinstance(sel, tuple) else sel)
@@ -179,3 +181,96 @@ def test_resnet50_through_the_executor():
     err = rel_err(f64(y), ref)
     say("resnet50 fp32 rel err %.3e" % err)
     assert err <= 1e-3
+
+
+def _identity_conv(c, dtype):
+    """A 1 x 1 convolution whose output equals its input exactly (unit
+    filters, zero bias): gives a parameterised network whose next operation
+    runs on the executor's own kernel."""
+    conv = torch.nn.Conv2d(c, c, 1)
+    with torch.no_grad():
+        conv.weight.copy_(torch.eye(c).reshape(c, c, 1, 1))
+        conv.bias.zero_()
+    return conv.to(dtype)
+
+
+# (kind, kernel, stride, pad, N, C, H, W): windows of 2x2 to 7x7, strides
+# 1-3, padding up to half the window, odd planes.
+POOLS = [
+    ("max", 2, 2, 0, 2, 5, 13, 11), ("max", 3, 2, 1, 3, 4, 15, 15), ("max", 3, 1, 1, 2, 3, 9, 7),
+    ("max", 5, 2, 2, 1, 6, 17, 12), ("max", 3, 3, 0, 2, 4, 10, 14), ("max", 7, 1, 3, 1, 2, 8, 9),
+    ("avg", 2, 2, 0, 2, 5, 13, 11), ("avg", 3, 2, 1, 3, 4, 15, 15), ("avg", 3, 1, 1, 2, 3, 9, 7),
+    ("avg", 5, 2, 2, 1, 6, 17, 12), ("avg", 3, 3, 0, 2, 4, 10, 14), ("avg", 7, 1, 3, 1, 2, 8, 9),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("case", POOLS, ids=lambda c: "%s%d-s%d-p%d-%dx%dx%dx%d" % c)
+def test_pool_kernel(case, dtype):
+    kind, k, st, pad, n, c, h, w = case
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    pool = torch.nn.MaxPool2d(k, st, pad) if kind == "max" else torch.nn.AvgPool2d(k, st, pad)
+    net = torch.nn.Sequential(_identity_conv(c, tdt), pool).eval()
+    g = torch.Generator().manual_seed(POOLS.index(case))
+    x = torch.randn(n, c, h, w, generator=g).to(tdt)
+    ref = reference(net, x)
+    model = cs.swap_backend(net.to(DEV), "direct")
+    say("case pool", case, dtype)
+    with torch.no_grad():
+        y = model(x.to(DEV))
+    torch.cuda.synchronize()
+    assert tuple(y.shape) == ref.shape
+    got = f64(y)
+    if kind == "max":
+        assert np.array_equal(got, ref)       # a maximum is one of the inputs
+    else:
+        # fp32 sum of at most 49 inputs / bf16: the average rounded once
+        assert rel_err(got, ref) <= (1e-6 if dtype == "f32" else 2 ** -8)
+
+
+@pytest.mark.parametrize("hw", [(1, 1), (7, 7), (5, 3), (13, 17), (2, 9)])
+def test_global_avgpool_kernel(hw):
+    h, w = hw
+    net = torch.nn.Sequential(_identity_conv(6, torch.float32), torch.nn.AdaptiveAvgPool2d(1)).eval()
+    x = torch.randn(3, 6, h, w, generator=torch.Generator().manual_seed(h * 31 + w))
+    ref = reference(net, x)
+    model = cs.swap_backend(net.to(DEV), "direct")
+    say("case global_avgpool", hw)
+    with torch.no_grad():
+        y = model(x.to(DEV))
+    torch.cuda.synchronize()
+    assert tuple(y.shape) == ref.shape == (3, 6, 1, 1)
+    assert rel_err(f64(y), ref) <= 1e-6
+
+
+class _PoolAddRelu(torch.nn.Module):
+    """Two pools of one convolution output, added, then a ReLU: neither add
+    operand is a convolution output and the ReLU follows the add's second
+    reader, so the add and the ReLU run on their own kernels."""
+
+    def __init__(self, c):
+        super().__init__()
+        self.conv = _identity_conv(c, torch.float32)
+        self.p1 = torch.nn.MaxPool2d(3, 1, 1)
+        self.p2 = torch.nn.AvgPool2d(3, 1, 1)
+
+    def forward(self, x):
+        y = self.conv(x)
+        s = self.p1(y) + self.p2(y)
+        return torch.relu(self.p1(s)) + s
+
+
+def test_add_and_relu_kernels():
+    net = _PoolAddRelu(5).eval()
+    x = torch.randn(2, 5, 11, 9, generator=torch.Generator().manual_seed(4))
+    ref = reference(net, x)
+    model = cs.swap_backend(net.to(DEV), "direct")
+    kinds = [k for k, _ in model.ops]
+    assert kinds.count("add") == 2 and kinds.count("relu") == 1
+    model.plan(x.shape)
+    assert not any(" fused" in line for line in model.describe().splitlines())
+    say("case add+relu kernels")
+    with torch.no_grad():
+        y = model(x.to(DEV))
+    torch.cuda.synchronize()
+    assert rel_err(f64(y), ref) <= 1e-6

@@ -11,22 +11,7 @@ from torch import nn
 import oracle
 import paper_2410_08300_amd as cs
 from paper_2410_08300_amd import selection
-
-
-class ConvNet(nn.Module):
-    """The toy network of the paper's Listing 1 (two 3x3 convolutions)."""
-
-    def __init__(self):
-        super().__init__()
-        self.conv1 = nn.Conv2d(3, 16, 3, padding=1)
-        self.maxpool = nn.MaxPool2d(2, 2)
-        self.conv2 = nn.Conv2d(16, 32, 3, padding=1)
-
-    def forward(self, x):
-        x = torch.relu(self.conv1(x))
-        x = self.maxpool(x)
-        x = torch.relu(self.conv2(x))
-        return torch.flatten(x, 1)
+from nets import ConvStack
 
 
 class Deep(nn.Module):
@@ -56,11 +41,11 @@ def fake_backend(monkeypatch):
 
 def test_single_name_list_and_callable(fake_backend):
     torch.manual_seed(0)
-    m = ConvNet()
+    m = ConvStack()
     x = torch.randn(2, 3, 16, 16)
     ref = m(x)
     t = cs.swap_conv2d(m, "direct")
-    assert list(t.items()) == [("conv1", "direct"), ("conv2", "direct")]
+    assert list(t.items()) == [("0", "direct"), ("3", "direct")]
     assert torch.allclose(m(x), ref, atol=1e-5)
     t = cs.swap_conv2d(m, ["implicit_gemm", "gemm"])
     assert list(t.values()) == ["implicit_gemm", "im2col_gemm"]
@@ -72,10 +57,10 @@ def test_single_name_list_and_callable(fake_backend):
 
 
 def test_table_edit_changes_algorithm_without_reswapping(fake_backend):
-    m = ConvNet()
+    m = ConvStack()
     t = cs.swap_conv2d(m, "direct")
     x = torch.randn(1, 3, 8, 8)
-    t.set("conv2", "winograd")
+    t.set("3", "winograd")
     fake_backend.clear()
     m(x)
     assert fake_backend == ["direct", "winograd"]
@@ -106,9 +91,9 @@ def test_dict_selector_and_reswap():
 
 def test_selector_errors():
     with pytest.raises(ValueError):
-        cs.swap_conv2d(ConvNet(), ["direct"])                 # list length mismatch
+        cs.swap_conv2d(ConvStack(), ["direct"])                 # list length mismatch
     with pytest.raises(ValueError):
-        cs.swap_conv2d(ConvNet(), "fft")                      # unknown name
+        cs.swap_conv2d(ConvStack(), "fft")                      # unknown name
     with pytest.raises(ValueError):
         cs.swap_conv2d(Deep(), "winograd")                    # 5x5 stem cannot use F(2x2,3x3)
     with pytest.raises(ValueError):
@@ -133,7 +118,7 @@ def test_algo_cache_measures_each_shape_once_and_persists(fake_backend, monkeypa
 
     monkeypatch.setattr(selection, "select_fastest", fake_select)
     torch.manual_seed(3)
-    m = ConvNet()
+    m = ConvStack()
     x = torch.randn(2, 3, 16, 16)
     ref = m(x)
     cache = cs.AlgoCache(device="test")
@@ -150,10 +135,10 @@ def test_algo_cache_measures_each_shape_once_and_persists(fake_backend, monkeypa
     cache.save(str(path))
     back = cs.AlgoCache.load(str(path))
     assert back.entries == cache.entries and back.device == "test"
-    key = cs.AlgoCache.key_for(x, m.conv1.weight, m.conv1.bias, (1, 1), (1, 1), (1, 1), 1)
+    key = cs.AlgoCache.key_for(x, m[0].weight, m[0].bias, (1, 1), (1, 1), (1, 1), 1)
     assert back.lookup(key) == "smm"
     # a loaded cache answers without timing
-    m2 = ConvNet()
+    m2 = ConvStack()
     cs.swap_conv2d(m2, back)
     timed.clear()
     m2(x)
@@ -176,8 +161,32 @@ def test_algo_cache_keys_and_errors():
     with pytest.raises(ValueError):
         cs.AlgoCache.from_json('{"version": 99, "entries": {}}')
     t = cs.AlgoTable()
-    t.set("conv1", "cached")
-    m = ConvNet()
-    cs.swap_conv2d(m, {"conv1": "cached"})
+    t.set("0", "cached")
+    m = ConvStack()
+    cs.swap_conv2d(m, {"0": "cached"})
     with pytest.raises(ValueError):
         m(torch.randn(1, 3, 8, 8))                                  # "cached" without a cache
+
+
+def test_non_zero_padding_modes_never_reach_the_library(fake_backend):
+    """The library pads with zeros only: every selector form that would run
+    a reflect / replicate / circular module on the library is refused at swap
+    time, and a later table edit to a library algorithm is refused at call
+    time; "torch" keeps such a module working."""
+    for mode in ("reflect", "replicate", "circular"):
+        def net():
+            return nn.Sequential(nn.Conv2d(3, 4, 3, padding=1, padding_mode=mode), nn.Conv2d(4, 4, 1))
+        for sel in ("default", "direct", ["default", "direct"], {"1": "direct"}, lambda c: "default",
+                    cs.AlgoCache()):
+            with pytest.raises(ValueError, match="padding_mode"):
+                cs.swap_conv2d(net(), sel)
+        m = net()
+        x = torch.randn(1, 3, 6, 6)
+        ref = m(x)
+        t = cs.swap_conv2d(m, {"0": "torch", "1": "direct"})
+        fake_backend.clear()
+        assert torch.allclose(m(x), ref, atol=1e-5) and fake_backend == ["direct"]
+        for algo in ("direct", "default", "cached"):
+            t.set("0", algo)
+            with pytest.raises(ValueError, match="padding_mode"):
+                m(x)
