@@ -1,0 +1,805 @@
+// Implicit GEMM (paper, Sec. V-B item (b)) for bf16 3x3 layers with stride 1
+// or 2, dilation 1, one group and C a multiple of the channel chunk.
+//
+// The contraction is Y[pixel][k] = sum over (tap, c) of X~[pixel + tap][c] *
+// W[k][c][tap]: output pixels (flattened n, p, q) as the MFMA's A rows,
+// output channels as its B columns, reduced 16 channels of one tap per
+// v_mfma_f32_32x32x16_bf16.  A workgroup owns a tile of TP consecutive
+// pixels x TK channels and walks the input channels in chunks of CH.  Per
+// chunk, LDS holds
+//
+//   * the halo: every input row the tile's pixels read, pixel-major (the CH
+//     channels of one input pixel are contiguous, 16-byte units XOR-swizzled
+//     so that 16 consecutive pixels hit distinct banks), with the zero
+//     padding columns in place.  Any tap of any pixel is then one 16-byte LDS
+//     read of 8 channels, which is exactly one lane's MFMA operand.  For
+//     stride 2 each row is split into its even and odd columns, so that the
+//     pixels of one tap are again consecutive slots;
+//   * the filters of the tile: [tap][TK][CH], swizzled the same way.
+//
+// Loader waves (the last kLoaders waves) fill these from the tensors as
+// given: NCHW input rows with 16-byte loads (8 pixels of one channel; 8
+// channels per lane), transposed in registers into 8 pixel vectors; KCRS
+// filters with nine 16-byte loads per (filter, 8 channels) -- the 72
+// consecutive values of 8 channels x 9 taps -- regrouped in registers into
+// nine tap vectors.  No packing kernel runs before the convolution.  Two LDS
+// stages alternate; while the compute waves multiply chunk i, the loaders
+// write chunk i+1 and have chunk i+2's loads in flight.
+//
+// Compute waves form a WP x WK grid; each holds MB x NB blocks of 32 x 32
+// accumulators (32 MB pixels x 32 NB channels), so that each operand read
+// from LDS feeds NB (pixel fragments) or MB (filter fragments) MFMAs.  The
+// epilogue adds bias (and the model executor's residual), applies ReLU,
+// rounds and stores each lane's runs of four consecutive pixels of one
+// channel as 8-byte stores, or stores fp32 partials for a split reduction.
+#include <stdio.h>
+
+#include <algorithm>
+#include <atomic>
+#include <string>
+#include <type_traits>
+
+#include "common.hpp"
+#include "igemm_common.hpp"
+#include "kernels.hpp"
+
+namespace convsel {
+
+namespace {
+
+using namespace igemm;
+
+constexpr int kLoaders = 4;   // loader waves per workgroup
+constexpr int kK3Taps = 9;
+constexpr int kHSMax = 2;     // halo items per loader lane and chunk (at most)
+
+struct K3Args {
+  const void* x;       // first image of this launch
+  const void* w;       // filters, K x C x 3 x 3
+  uint32_t x_bytes, w_bytes;
+  int N, C, H, W, K, P, Q;
+  int sh, ph, pw;      // stride (both axes), padding
+  int Hp;              // virtual rows per image: (P - 1) * sh + 3
+  int NPQ;
+  int ptiles, ktiles;
+  int nch, chunks_per_split;
+  int VR;              // halo rows staged per chunk
+  int RS, PS;          // LDS slots per halo row; stride 2: slots per column-parity plane
+  int NG;              // column windows per input row
+  int halo_items;      // VR * NG * (CH / 8)
+  int halo_bytes;      // one stage's halo, rounded to 256 bytes
+  int stage_bytes;     // halo + filter tile
+  EpiArgs e;
+};
+
+// Bank swizzle of the 16-byte unit u of slot `pos` (a pixel or a filter row
+// of UP units): 16 consecutive slots' units land in 16 distinct 16-byte bank
+// groups.
+template <int UP>
+__device__ __forceinline__ int k3_swz(int pos) {
+  return (pos / (16 / UP)) & (UP - 1);
+}
+
+// Epilogue of one compute wave: NB blocks of 32 channels (channel block nb
+// starts at kb0 + 32 nb) x 32 MB pixels (tile pixels col0 ..), in the MFMA
+// layout (block (mb, nb), accumulator v of lane l: channel l % 32, pixel
+// 32 mb + 8 (v / 4) + 4 (l / 32) + v % 4).  Channel block by channel block,
+// the values are rounded (bf16, after bias and ReLU) or kept (fp32 partials
+// of a split reduction), staged in this wave's LDS region as
+// [channel][pixels] rows of 16-byte units XOR-swizzled by the channel, read
+// back as 8-pixel runs and stored with one 16-byte store per run (two for
+// fp32) -- every store instruction then covers whole contiguous rows of
+// 64 to 512 bytes instead of 32 separate 16-byte pieces.  A run that crosses
+// an image boundary or passes the last pixel is stored element by element
+// (runs cross at most one boundary: P*Q >= 8).
+template <int MB, int NB>
+__device__ __forceinline__ void k3_epilogue(const f32x16_t (&acc)[MB][NB], char* stage, const EpiArgs& e, int kb0,
+                                            int col0, int split) {
+  const int lane = threadIdx.x & 63;
+  const int l32 = lane & 31, h = lane >> 5;
+  const int PQ = e.PQ;
+  const int64_t next_img = static_cast<int64_t>(e.K - 1) * PQ;
+  if (e.splits <= 1) {
+    constexpr int U = MB * 4;          // 16-byte units per staged channel row (8 pixels each)
+    constexpr int RPI = 64 / U;        // rows covered by one pass of the wave
+    constexpr int PASSES = 32 / RPI;
+    const uint16_t* bias = reinterpret_cast<const uint16_t*>(e.b);
+    uint16_t* y = reinterpret_cast<uint16_t*>(e.y);
+    const int rrow = lane / U, u = lane % U;
+    const Run128t r = run128t(e, kb0, col0, 0, u * 8);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int kb = kb0 + 32 * nb;
+      const float bv = (bias && kb + l32 < e.K) ? bf16_to_f32(bias[kb + l32]) : 0.f;
+      const bool relu_now = e.relu && !e.res;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          float v4[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            v4[t] = acc[mb][nb][4 * g + t] + bv;
+            if (relu_now) v4[t] = fmaxf(v4[t], 0.f);
+          }
+          uint2 w;
+          w.x = f32x2_to_bf16x2(v4[0], v4[1]);
+          w.y = f32x2_to_bf16x2(v4[2], v4[3]);
+          const int px0 = mb * 32 + 8 * g + 4 * h;
+          *reinterpret_cast<uint2*>(stage + l32 * (U * 16) + (((px0 >> 3) ^ (l32 & (U - 1))) << 4) +
+                                    ((px0 >> 2) & 1) * 8) = w;
+        }
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's staging writes are done
+      __builtin_amdgcn_wave_barrier();
+      uint4 d[PASSES];
+#pragma unroll
+      for (int it = 0; it < PASSES; ++it) {
+        const int row = rrow + RPI * it;
+        d[it] = *reinterpret_cast<const uint4*>(stage + row * (U * 16) + ((u ^ (row & (U - 1))) << 4));
+      }
+      const int64_t ob = r.o + static_cast<int64_t>(kb - kb0) * PQ;
+      if (e.res) {
+        // Residual add (and the ReLU after it): all rows' residual runs are
+        // requested before any is used.
+        uint4 rr[PASSES];
+        const uint16_t* rp = reinterpret_cast<const uint16_t*>(e.res);
+        if (r.full) {
+#pragma unroll
+          for (int it = 0; it < PASSES; ++it) {
+            const int row = rrow + RPI * it;
+            rr[it] = make_uint4(0u, 0u, 0u, 0u);
+            if (kb + row < e.K) __builtin_memcpy(&rr[it], rp + ob + static_cast<int64_t>(row) * PQ, 16);
+          }
+        }
+#pragma unroll
+        for (int it = 0; it < PASSES; ++it) {
+          const int row = rrow + RPI * it;
+          if (kb + row >= e.K || r.nvalid <= 0) continue;
+          const int64_t o = ob + static_cast<int64_t>(row) * PQ;
+          const uint32_t w[4] = {d[it].x, d[it].y, d[it].z, d[it].w};
+          float v[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) v[t] = __uint_as_float((w[t >> 1] >> (16 * (t & 1))) << 16);
+          if (r.full) {
+            const uint32_t q[4] = {rr[it].x, rr[it].y, rr[it].z, rr[it].w};
+#pragma unroll
+            for (int t = 0; t < 8; ++t) v[t] += __uint_as_float((q[t >> 1] >> (16 * (t & 1))) << 16);
+          } else {
+            add_residual_run<bf16_t>(v, e, o, false, r.nvalid, r.wrap, PQ, next_img);
+          }
+          if (e.relu)
+#pragma unroll
+            for (int t = 0; t < 8; ++t) v[t] = fmaxf(v[t], 0.f);
+          d[it].x = f32x2_to_bf16x2(v[0], v[1]);
+          d[it].y = f32x2_to_bf16x2(v[2], v[3]);
+          d[it].z = f32x2_to_bf16x2(v[4], v[5]);
+          d[it].w = f32x2_to_bf16x2(v[6], v[7]);
+        }
+      }
+#pragma unroll
+      for (int it = 0; it < PASSES; ++it) {
+        const int row = rrow + RPI * it;
+        if (kb + row >= e.K || r.nvalid <= 0) continue;
+        const int64_t o = ob + static_cast<int64_t>(row) * PQ;
+        if (r.full) {
+          __builtin_memcpy(y + o, &d[it], 16);
+        } else {
+          const uint32_t wd[4] = {d[it].x, d[it].y, d[it].z, d[it].w};
+#pragma unroll
+          for (int t = 0; t < 8; ++t)
+            if (t < r.nvalid)
+              y[o + t + (t >= r.wrap ? next_img : 0)] = static_cast<uint16_t>(wd[t >> 1] >> (16 * (t & 1)));
+        }
+      }
+      __builtin_amdgcn_wave_barrier();  // the next block reuses the staging rows
+    }
+    return;
+  }
+  // fp32 partial sums: rows of 32 MB floats (8 MB units), one 8-pixel run
+  // (two units) per lane and pass.
+  constexpr int U = MB * 8;
+  constexpr int LPR = MB * 4;        // lanes per row
+  constexpr int RPI = 64 / LPR;
+  constexpr int PASSES = 32 / RPI;
+  float* part = e.partial + static_cast<int64_t>(split) * e.slab;
+  const int rrow = lane / LPR, c = lane % LPR;
+  const Run128t r = run128t(e, kb0, col0, 0, c * 8);
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int kb = kb0 + 32 * nb;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int px0 = mb * 32 + 8 * g + 4 * h;
+        const float4 v = make_float4(acc[mb][nb][4 * g], acc[mb][nb][4 * g + 1], acc[mb][nb][4 * g + 2],
+                                     acc[mb][nb][4 * g + 3]);
+        *reinterpret_cast<float4*>(stage + l32 * (U * 16) + (((px0 >> 2) ^ (l32 & (U - 1))) << 4)) = v;
+      }
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_wave_barrier();
+    float4 lo[PASSES], hi[PASSES];
+#pragma unroll
+    for (int it = 0; it < PASSES; ++it) {
+      const int row = rrow + RPI * it;
+      lo[it] = *reinterpret_cast<const float4*>(stage + row * (U * 16) + (((2 * c) ^ (row & (U - 1))) << 4));
+      hi[it] = *reinterpret_cast<const float4*>(stage + row * (U * 16) + (((2 * c + 1) ^ (row & (U - 1))) << 4));
+    }
+    const int64_t ob = r.o + static_cast<int64_t>(kb - kb0) * PQ;
+#pragma unroll
+    for (int it = 0; it < PASSES; ++it) {
+      const int row = rrow + RPI * it;
+      if (kb + row >= e.K || r.nvalid <= 0) continue;
+      const int64_t o = ob + static_cast<int64_t>(row) * PQ;
+      if (r.full) {
+        __builtin_memcpy(part + o, &lo[it], 16);
+        __builtin_memcpy(part + o + 4, &hi[it], 16);
+      } else {
+        const float vals[8] = {lo[it].x, lo[it].y, lo[it].z, lo[it].w, hi[it].x, hi[it].y, hi[it].z, hi[it].w};
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+          if (t < r.nvalid) part[o + t + (t >= r.wrap ? next_img : 0)] = vals[t];
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+template <int CH, int WP, int WK, int MB, int NB, bool S2, int UPX, int HS>
+__global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Args a) {
+  constexpr int NC = WP * WK;                 // compute waves
+  constexpr int TP = WP * MB * 32, TK = WK * NB * 32;
+  constexpr int UP = CH / 8;                  // 16-byte units per pixel / filter row
+  constexpr int KS = CH / 16;                 // MFMA steps per tap and chunk
+  static_assert(CH == 16 || CH == 32, "channel chunk");
+  static_assert(UPX == 8 || UPX == 4, "column window");
+  extern __shared__ __align__(16) vec16 smem[];
+  char* lds = reinterpret_cast<char*>(smem);
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // Work units (pixel tile, channel tile, split) are dealt to the eight XCDs
+  // in contiguous ranges, channel tile outermost: workgroup b runs on XCD
+  // b % 8, so each XCD reads a contiguous range of pixel tiles and (for
+  // many channel tiles) only its own slice of the filters, which its L2
+  // then holds for all of its workgroups.
+  const int units = a.ptiles * a.ktiles * a.e.splits;
+  const int per_xcd = (units + 7) >> 3;
+  const int unit = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (unit >= units || (blockIdx.x >> 3) >= per_xcd) return;  // uniform over the workgroup
+  const int split = unit % a.e.splits;
+  const int tile = unit / a.e.splits;
+  const int ktile = tile / a.ptiles, ptile = tile - ktile * a.ptiles;
+  const int j0 = ptile * TP, k0 = ktile * TK;
+  const int ch_begin = split * a.chunks_per_split;
+  const int nchunks = min(a.nch, ch_begin + a.chunks_per_split) - ch_begin;
+  const int npairs = (nchunks + 1) >> 1;  // barrier steps run in pairs
+  const int PQ = a.P * a.Q;
+  auto vrow = [&](int j) {
+    const int n = j / PQ, pq = j - n * PQ;
+    return n * a.Hp + (pq / a.Q) * a.sh;
+  };
+  const int v_lo = vrow(j0);
+
+  if (wave >= NC) {
+    // ---------------- loader waves ----------------
+    const int lt = tid - NC * 64;
+    const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
+    const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
+    const uint32_t plane = static_cast<uint32_t>(a.H * a.W * 2);
+    // Halo items: (channel group g, halo row vr, column window gc).  The
+    // per-lane offset is that of channel 8g; the chunk's channels go into
+    // the scalar offset.  Rows outside the image read zeros.
+    uint32_t hvo[HS];
+    int hrow[HS];    // LDS slot of the item's halo row, -1: no item
+    int hcol[HS];    // padded column of the window's first pixel
+    int hg[HS];
+#pragma unroll
+    for (int t = 0; t < HS; ++t) {
+      const int it = lt + t * 256;
+      hvo[t] = a.x_bytes;
+      hrow[t] = -1;
+      hcol[t] = 0;
+      hg[t] = 0;
+      if (it < a.halo_items) {
+        // Rows fastest: consecutive lanes write slots a halo row apart,
+        // not UPX slots apart (which would put them all in one bank group).
+        const int per_g = a.VR * a.NG;
+        const int g = it / per_g, rem = it - g * per_g;
+        const int gc = rem / a.VR, vr = rem - gc * a.VR;
+        const int ws = min(gc * UPX, a.W - UPX);
+        const int v = v_lo + vr;
+        const int n = v / a.Hp, h = v - n * a.Hp - a.ph;
+        if (n < a.N && h >= 0 && h < a.H)
+          hvo[t] = static_cast<uint32_t>(((n * a.C + 8 * g) * a.H + h) * a.W + ws) * 2;
+        hg[t] = g;
+        hrow[t] = vr * a.RS;
+        hcol[t] = ws + a.pw;
+      }
+    }
+    // Filter items: (filter row kl, channel group g); rows past K read zeros.
+    const int kl = lt / UP, fg = lt - (lt / UP) * UP;
+    const bool f_on = kl < TK;
+    const uint32_t fvo = (f_on && k0 + kl < a.K)
+                             ? static_cast<uint32_t>(((k0 + kl) * a.C + 8 * fg) * kK3Taps) * 2
+                             : a.w_bytes;
+    constexpr int HD = UPX / 2;  // dwords per channel of a window
+    // Every chunk issues the same HS * 8 + 9 loads per lane (unused halo
+    // slots read zeros past the buffer), so the compiler's own count of the
+    // loads in flight matches the explicit waits below.
+    constexpr int PER = HS * 8 + kK3Taps;
+    static_assert(2 * PER <= 63, "vmcnt range");
+    // Two register sets, by chunk parity: chunk i+2's loads stay in flight
+    // while chunk i+1 is written to LDS.
+    uint32_t hd[2][HS][8][HD];
+    u32x4_t fd[2][kK3Taps];
+
+    auto issue = [&](int ch, auto set_c) {
+      constexpr int SET = decltype(set_c)::value;
+      const int c0 = (ch_begin + ch) * CH;
+#pragma unroll
+      for (int t = 0; t < HS; ++t) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint32_t so = static_cast<uint32_t>(c0 + e) * plane;
+          if constexpr (UPX == 8) {
+            const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(xr, hvo[t], so, 0);
+            hd[SET][t][e][0] = v[0]; hd[SET][t][e][1] = v[1]; hd[SET][t][e][2] = v[2]; hd[SET][t][e][3] = v[3];
+          } else {
+            const auto v = __builtin_amdgcn_raw_buffer_load_b64(xr, hvo[t], so, 0);
+            hd[SET][t][e][0] = v[0]; hd[SET][t][e][1] = v[1];
+          }
+        }
+      }
+      const uint32_t fso = static_cast<uint32_t>(c0 * kK3Taps * 2);
+#pragma unroll
+      for (int q = 0; q < kK3Taps; ++q)
+        fd[SET][q] = __builtin_amdgcn_raw_buffer_load_b128(wr, fvo, fso + 16 * q, 0);
+    };
+    auto write = [&](int st, auto set_c) {
+      constexpr int SET = decltype(set_c)::value;
+      char* Hs = lds + st * a.stage_bytes;
+      char* Fs = Hs + a.halo_bytes;
+#pragma unroll
+      for (int t = 0; t < HS; ++t) {
+        if (hrow[t] >= 0) {
+#pragma unroll
+          for (int px = 0; px < UPX; ++px) {
+            // pixel px of the window: channels 8g .. 8g+7 as one 16-byte unit
+            u32x4_t o;
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+              const uint32_t d0 = hd[SET][t][2 * m][px >> 1], d1 = hd[SET][t][2 * m + 1][px >> 1];
+              o[m] = (px & 1) ? ((d0 >> 16) | (d1 & 0xFFFF0000u)) : ((d0 & 0xFFFFu) | (d1 << 16));
+            }
+            const int pc = hcol[t] + px;
+            const int slot = S2 ? hrow[t] + (pc & 1) * a.PS + (pc >> 1) : hrow[t] + pc;
+            const int unit_ = hg[t] ^ k3_swz<UP>(slot);
+            *reinterpret_cast<u32x4_t*>(Hs + slot * (CH * 2) + unit_ * 16) = o;
+          }
+        }
+      }
+      if (f_on) {
+        // element i = c * 9 + tap of the 72 loaded values (c = 0..7)
+        auto el = [&](int i) -> uint32_t { return (fd[SET][i >> 3][(i >> 1) & 3] >> (16 * (i & 1))) & 0xFFFFu; };
+        const int unit_ = fg ^ k3_swz<UP>(kl);
+#pragma unroll
+        for (int tap = 0; tap < kK3Taps; ++tap) {
+          u32x4_t o;
+#pragma unroll
+          for (int m = 0; m < 4; ++m) o[m] = el(2 * m * kK3Taps + tap) | (el((2 * m + 1) * kK3Taps + tap) << 16);
+          *reinterpret_cast<u32x4_t*>(Fs + (tap * TK + kl) * (CH * 2) + unit_ * 16) = o;
+        }
+      }
+    };
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    // Chunks past the last re-read the last one (never written to LDS), so
+    // the issue sequence does not depend on the chunk count.
+    auto chunk_of = [&](int ch) { return ch < nchunks ? ch : nchunks - 1; };
+
+    // The first two chunks' loads go out before the workgroup clears the
+    // halo padding, so the clearing and the wave launches overlap them.
+    issue(0, S0{});
+    issue(chunk_of(1), S1{});
+    for (int i = lt; i < a.halo_bytes / 16; i += 256) {
+      reinterpret_cast<u32x4_t*>(lds)[i] = u32x4_t{0u, 0u, 0u, 0u};
+      reinterpret_cast<u32x4_t*>(lds + a.stage_bytes)[i] = u32x4_t{0u, 0u, 0u, 0u};
+    }
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_s_barrier();  // the padding is clear
+    asm volatile("" ::: "memory");
+    CONVSEL_WAIT_VMCNT(PER);  // chunk 0 (chunk 1's loads may stay in flight)
+    write(0, S0{});
+    issue(chunk_of(2), S0{});
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this lane's LDS writes are done
+    // Chunk i+1 comes from register set (i+1) & 1, and chunk i+3's loads
+    // refill that set; chunk i+2's (the PER loads issued after chunk i+1's)
+    // stay in flight.  Steps run in pairs (an odd chunk count gets an empty
+    // last step, matched by the compute waves) and every step issues its
+    // loads, so the loop carries the same loads in flight on every path.
+    auto step = [&](int i, auto set_c) {  // set_c: (i + 1) & 1
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_barrier();  // A(i): chunk i visible to the compute waves
+      asm volatile("" ::: "memory");
+      CONVSEL_WAIT_VMCNT(PER);
+      if (i + 1 < nchunks) write((i + 1) & 1, set_c);  // its stage was freed at B(i-1)
+      issue(chunk_of(i + 3), set_c);
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_barrier();  // B(i): the compute waves are done with stage i & 1
+      asm volatile("" ::: "memory");
+    };
+    for (int i = 0; i < npairs * 2; i += 2) {
+      step(i, S1{});
+      step(i + 1, S0{});
+    }
+    CONVSEL_WAIT_VMCNT(0);  // the re-reads past the last chunk
+    return;
+  }
+
+  // ---------------- compute waves ----------------
+  __builtin_amdgcn_s_barrier();  // the loaders have cleared the halo padding
+  const int wp = wave % WP, wk = wave / WP;
+  const int half = lane >> 5, l32 = lane & 31;
+  const int jl = min(j0 + TP, a.NPQ) - 1;
+  // Slot of each pixel fragment row (clamped to the tile's last pixel).
+  int apos[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const int j = min(j0 + (wp * MB + mb) * 32 + l32, jl);
+    const int pq = j - (j / PQ) * PQ;
+    const int q = pq - (pq / a.Q) * a.Q;
+    apos[mb] = (vrow(j) - v_lo) * a.RS + q;
+  }
+  // Tap offsets in slots: row r, column s (stride 2: parity plane s & 1, s >> 1 further).
+  auto tapoff = [&](int t) {
+    const int r = t / 3, s = t - (t / 3) * 3;
+    return S2 ? r * a.RS + (s & 1) * a.PS + (s >> 1) : r * a.RS + s;
+  };
+  // Filter fragment offsets within a tap (bytes): row kr, unit 2u + half.
+  int boff[NB][KS];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int kr = (wk * NB + nb) * 32 + l32;
+#pragma unroll
+    for (int u = 0; u < KS; ++u) boff[nb][u] = kr * (CH * 2) + (((2 * u + half) ^ k3_swz<UP>(kr)) * 16);
+  }
+
+  f32x16_t acc[MB][NB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = zero16();
+
+  // A chunk is 9 KS steps (tap t, 16-channel slice u), each MB pixel and NB
+  // filter fragment reads and MB x NB MFMAs.  The reads run D steps ahead of
+  // the MFMAs (at most 15 LDS reads in flight per wave), and a wave with a
+  // single 32 x 32 block alternates two accumulators by step parity, so that
+  // neither an LDS round trip nor a dependent MFMA sits between two MFMAs.
+  constexpr int NSTEP = kK3Taps * KS;
+  constexpr int RD = MB + NB;                 // reads per step
+  constexpr int D0 = 15 / RD - 1;
+  constexpr int D = D0 < 1 ? 1 : (D0 > NSTEP - 1 ? NSTEP - 1 : D0);
+  constexpr int NACC = MB * NB == 1 ? 2 : 1;
+  f32x16_t acc2[1];  // the second accumulator (NACC == 2)
+  acc2[0] = zero16();
+  for (int i = 0; i < nchunks; ++i) {
+    lds_sync();  // A(i)
+    const char* Hs = lds + (i & 1) * a.stage_bytes;
+    const char* Fs = Hs + a.halo_bytes;
+    bf16x8_t fa[D + 1][MB], fb[D + 1][NB];
+    auto read = [&](auto s_c) {
+      constexpr int S = decltype(s_c)::value;
+      constexpr int t = S / KS, u = S % KS, slot = S % (D + 1);
+      const int to = tapoff(t);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const int pos = apos[mb] + to;
+        fa[slot][mb] =
+            *reinterpret_cast<const bf16x8_t*>(Hs + pos * (CH * 2) + (((2 * u + half) ^ k3_swz<UP>(pos)) * 16));
+      }
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        fb[slot][nb] = *reinterpret_cast<const bf16x8_t*>(Fs + t * (TK * CH * 2) + boff[nb][u]);
+    };
+    static_for<D>([&](auto s_c) { read(s_c); });
+    static_for<NSTEP>([&](auto s_c) {
+      constexpr int S = decltype(s_c)::value;
+      if constexpr (S + D < NSTEP) read(std::integral_constant<int, S + D>{});
+      // Keep the program order: the scheduler would otherwise sink each read
+      // next to its MFMA.
+      __builtin_amdgcn_sched_barrier(0);
+      constexpr int slot = S % (D + 1);
+      if constexpr (NACC == 2 && (S & 1)) {
+        acc2[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][0], fb[slot][0], acc2[0], 0, 0, 0);
+      } else {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][mb], fb[slot][nb], acc[mb][nb], 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    lds_sync();  // B(i)
+  }
+  if constexpr (NACC == 2) acc[0][0] += acc2[0];
+  if (nchunks & 1) {  // the loaders' empty last step of an odd chunk count
+    lds_sync();
+    lds_sync();
+  }
+
+  // ---------------- epilogue ----------------
+  // After B of the last chunk no wave reads the stages again: each compute
+  // wave stages its output in its own region at the start of LDS.
+  char* stage = lds + wave * (MB * 32 * 32 * 4);
+  k3_epilogue<MB, NB>(acc, stage, a.e, k0 + wk * NB * 32, j0 + wp * MB * 32, split);
+}
+
+// ---------------------------------------------------------------------------
+// Host side: tile configurations and planning.
+// ---------------------------------------------------------------------------
+struct K3Config {
+  int CH, WP, WK, MB, NB;
+  int tp() const { return WP * MB * 32; }
+  int tk() const { return WK * NB * 32; }
+  int nc() const { return WP * WK; }
+};
+
+// The instantiated tile shapes (pixels x channels per workgroup, wave tile):
+// 512 x 64 (waves 128 x 64), 128 x 128 (64 x 64), 128 x 64 (64 x 32),
+// 64 x 64 (32 x 32).
+constexpr K3Config kK3Configs[] = {
+    {16, 4, 1, 4, 2},
+    {16, 2, 2, 2, 2},
+    {32, 2, 2, 2, 1},
+    {32, 2, 2, 1, 1},
+};
+constexpr int kNumK3Configs = sizeof(kK3Configs) / sizeof(kK3Configs[0]);
+
+struct K3Plan {
+  int cfg;
+  bool s2;
+  int upx;
+  int64_t images_per_launch;
+  size_t part_bytes, lds;
+  K3Args a;
+};
+
+// Largest halo span (virtual rows) of any TP-pixel tile of N images.
+int k3_halo_rows(const Shape& s, int64_t N, int Hp, int TP) {
+  const int64_t PQ = s.P * s.Q, NPQ = N * PQ;
+  const int64_t tiles = (NPQ + TP - 1) / TP;
+  auto vrow = [&](int64_t j) {
+    const int64_t n = j / PQ, pq = j % PQ;
+    return n * Hp + (pq / s.Q) * s.sh;
+  };
+  // A tile's span depends only on where it starts within an image, which
+  // repeats every PQ / gcd(TP, PQ) tiles.
+  int64_t a = TP, b = PQ;
+  while (b) {
+    const int64_t t = a % b;
+    a = b;
+    b = t;
+  }
+  const int64_t period = PQ / a;
+  int64_t best = 0;
+  for (int64_t t = 0; t < tiles && t <= period; ++t) {
+    const int64_t j1 = ((t + 1) * TP < NPQ ? (t + 1) * TP : NPQ) - 1;
+    best = std::max(best, vrow(j1) - vrow(t * TP) + 3);
+  }
+  best = std::max(best, vrow(NPQ - 1) - vrow((tiles - 1) * TP) + 3);
+  return (int)best;
+}
+
+bool k3_shape_ok(const Shape& s) {
+  if (s.dtype != DT_BF16 || s.G != 1 || s.R != 3 || s.S != 3) return false;
+  if (s.sh != s.sw || (s.sh != 1 && s.sh != 2) || s.dh != 1 || s.dw != 1) return false;
+  if (s.C % 16 != 0 || s.W < 4 || s.P * s.Q < 8) return false;
+  if (s.ph > 2 || s.pw > 2) return false;
+  return true;
+}
+
+bool make_k3_plan_cfg(const Shape& s, int cfg, K3Plan& pl, int64_t N1) {
+  const K3Config c = kK3Configs[cfg];
+  if (s.C % c.CH != 0) return false;
+  pl.cfg = cfg;
+  pl.s2 = s.sh == 2;
+  pl.upx = s.W >= 8 ? 8 : 4;
+  pl.images_per_launch = N1;
+  K3Args& a = pl.a;
+  a.N = (int)N1; a.C = (int)s.C; a.H = (int)s.H; a.W = (int)s.W; a.K = (int)s.K;
+  a.P = (int)s.P; a.Q = (int)s.Q;
+  a.sh = s.sh; a.ph = s.ph; a.pw = s.pw;
+  a.Hp = (int)((s.P - 1) * s.sh + 3);
+  a.NPQ = (int)(N1 * s.P * s.Q);
+  a.ptiles = (a.NPQ + c.tp() - 1) / c.tp();
+  a.ktiles = (int)((s.K + c.tk() - 1) / c.tk());
+  a.nch = (int)(s.C / c.CH);
+  a.VR = k3_halo_rows(s, N1, a.Hp, c.tp());
+  // Padded columns read: q * sh + tap column < (Q - 1) * sh + 3; written: [pw, W + pw).
+  const int cols = (int)std::max<int64_t>((s.Q - 1) * s.sh + 3, s.W + s.pw);
+  if (pl.s2) {
+    a.PS = (cols + 1) / 2;
+    a.RS = 2 * a.PS;
+  } else {
+    a.PS = 0;
+    a.RS = cols;
+  }
+  a.NG = (int)((s.W + pl.upx - 1) / pl.upx);
+  a.halo_items = a.VR * a.NG * (c.CH / 8);
+  if (a.halo_items > kHSMax * 256) return false;
+  a.halo_bytes = (int)(((size_t)a.VR * a.RS * c.CH * 2 + 255) / 256 * 256);
+  const size_t filt = (size_t)kK3Taps * c.tk() * c.CH * 2;
+  a.stage_bytes = (int)(a.halo_bytes + filt);
+  pl.lds = (size_t)2 * a.stage_bytes;
+  // The epilogue stages each compute wave's fp32 or bf16 rows in LDS.
+  const size_t staging = (size_t)c.nc() * c.MB * 32 * 32 * 4;
+  if (pl.lds < staging) pl.lds = staging;
+  if (pl.lds > kLdsLimit) return false;
+  const int64_t tiles = (int64_t)a.ptiles * a.ktiles;
+  split_chunks(tiles, a.nch, &a.e.splits, &a.chunks_per_split);
+  a.e.K = (int)s.K; a.e.Kg = (int)s.K; a.e.relu = s.relu ? 1 : 0; a.e.PQ = (int)(s.P * s.Q);
+  a.e.span = a.e.PQ;
+  a.e.NPQ = a.NPQ;
+  a.e.slab = (int)((N1 * s.K * s.P * s.Q + 3) & ~(int64_t)3);
+  pl.part_bytes = a.e.splits > 1 ? (size_t)a.e.splits * a.e.slab * sizeof(float) : 0;
+  return true;
+}
+
+// Estimated time of a plan in units of one 32x32x16 MFMA per SIMD: rounds of
+// workgroups over the CUs times the MFMAs per compute wave of one workgroup,
+// divided by the wave tile's operand reuse efficiency, plus a pass over the
+// partial sums when the channels are split.
+double k3_cost(const K3Plan& pl) {
+  const K3Config c = kK3Configs[pl.cfg];
+  const K3Args& a = pl.a;
+  const int64_t wgs = (int64_t)a.ptiles * a.ktiles * a.e.splits;
+  const double rounds = (double)((wgs + kCUs - 1) / kCUs);
+  const double mfma = (double)a.chunks_per_split * kK3Taps * (c.CH / 16) * c.MB * c.NB * (c.nc() / 4.0);
+  const double reuse = (double)(c.MB * c.NB) / (c.MB + c.NB);  // MFMAs per fragment read
+  const double eff = reuse >= 1.3 ? 1.0 : reuse >= 1.0 ? 0.9 : 0.75;
+  const double fill = 3.0 * kK3Taps * (c.CH / 16) * c.MB * c.NB;  // the first chunk's latency
+  double t = rounds * (mfma / eff + fill);
+  if (a.e.splits > 1) t += (double)a.e.splits * a.NPQ * a.K / (kCUs * 64.0 * 8.0);
+  return t;
+}
+
+bool make_k3_plan(const Shape& s, K3Plan& pl, int64_t N1 = -1) {
+  if (!k3_shape_ok(s)) return false;
+  const int64_t img_bytes = s.C * s.H * s.W * 2;
+  if (img_bytes > kMaxLaunchBytes) return false;
+  if (N1 < 0) {
+    N1 = kMaxLaunchBytes / img_bytes;
+    if (N1 > s.N) N1 = s.N;
+    if (N1 < 1) N1 = 1;
+  }
+  if ((int64_t)s.K * s.C * 9 * 2 >= ((int64_t)1 << 31)) return false;
+  bool found = false;
+  double best = 0;
+  for (int cfg = 0; cfg < kNumK3Configs; ++cfg) {
+    K3Plan cand;
+    if (!make_k3_plan_cfg(s, cfg, cand, N1)) continue;
+    const double t = k3_cost(cand);
+    if (!found || t < best) {
+      best = t;
+      pl = cand;
+      found = true;
+    }
+  }
+  return found;
+}
+
+template <int CH, int WP, int WK, int MB, int NB, bool S2, int UPX, int HS>
+hipError_t k3_launch(const K3Plan& pl, const K3Args& a, hipStream_t stream) {
+  const auto kern = conv3x3_kernel<CH, WP, WK, MB, NB, S2, UPX, HS>;
+  static std::atomic<int> lds_limit{64 * 1024};
+  if ((int)pl.lds > lds_limit.load()) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsLimit);
+    if (e != hipSuccess) return e;
+    lds_limit.store((int)kLdsLimit);
+  }
+  const int units = a.ptiles * a.ktiles * a.e.splits;
+  const dim3 grid((unsigned)(8 * ((units + 7) / 8)));
+  hipLaunchKernelGGL(kern, grid, dim3((WP * WK + kLoaders) * 64), pl.lds, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.e.splits == 1) return e;
+  const int total = a.N * a.K * a.P * a.Q;
+  hipLaunchKernelGGL(splitk_reduce_kernel<bf16_t>, dim3(reduce_blocks(total)), dim3(256), 0, stream,
+                     a.e.partial, reinterpret_cast<const bf16_t*>(a.e.b), reinterpret_cast<bf16_t*>(a.e.y), total,
+                     a.e.slab, a.P * a.Q, a.K, a.e.splits, a.e.relu, reinterpret_cast<const bf16_t*>(a.e.res));
+  return hipGetLastError();
+}
+
+template <int CH, int WP, int WK, int MB, int NB, bool S2, int UPX>
+hipError_t k3_dispatch_hs(const K3Plan& pl, const K3Args& a, hipStream_t st) {
+  return a.halo_items > 256 ? k3_launch<CH, WP, WK, MB, NB, S2, UPX, 2>(pl, a, st)
+                            : k3_launch<CH, WP, WK, MB, NB, S2, UPX, 1>(pl, a, st);
+}
+
+template <int CH, int WP, int WK, int MB, int NB>
+hipError_t k3_dispatch_cfg(const K3Plan& pl, const K3Args& a, hipStream_t st) {
+  if (pl.s2)
+    return pl.upx == 8 ? k3_dispatch_hs<CH, WP, WK, MB, NB, true, 8>(pl, a, st)
+                       : k3_dispatch_hs<CH, WP, WK, MB, NB, true, 4>(pl, a, st);
+  return pl.upx == 8 ? k3_dispatch_hs<CH, WP, WK, MB, NB, false, 8>(pl, a, st)
+                     : k3_dispatch_hs<CH, WP, WK, MB, NB, false, 4>(pl, a, st);
+}
+
+hipError_t k3_dispatch(const K3Plan& pl, const K3Args& a, hipStream_t st) {
+  switch (pl.cfg) {
+    case 0: return k3_dispatch_cfg<16, 4, 1, 4, 2>(pl, a, st);
+    case 1: return k3_dispatch_cfg<16, 2, 2, 2, 2>(pl, a, st);
+    case 2: return k3_dispatch_cfg<32, 2, 2, 2, 1>(pl, a, st);
+    case 3: return k3_dispatch_cfg<32, 2, 2, 1, 1>(pl, a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+bool k3_applies(const Shape& s) {
+  K3Plan pl;
+  return make_k3_plan(s, pl);
+}
+
+size_t k3_split_bytes(const Shape& s) {
+  K3Plan pl;
+  if (!make_k3_plan(s, pl)) return 0;
+  size_t m = pl.part_bytes;
+  const int64_t rest = s.N % pl.images_per_launch;
+  if (rest) {
+    K3Plan last;
+    if (make_k3_plan(s, last, rest) && last.part_bytes > m) m = last.part_bytes;
+  }
+  return m;
+}
+
+hipError_t k3_main(const Shape& s, const void* x, const void* w, const void* b, void* y, void* part_ws,
+                   hipStream_t stream, const void* res) {
+  K3Plan pl;
+  if (!make_k3_plan(s, pl)) return hipErrorInvalidValue;
+  const int64_t img_elems = s.C * s.H * s.W, out_elems = s.K * s.P * s.Q;
+  for (int64_t n0 = 0; n0 < s.N; n0 += pl.images_per_launch) {
+    const int64_t cnt = s.N - n0 < pl.images_per_launch ? s.N - n0 : pl.images_per_launch;
+    K3Plan cur = pl;
+    if (cnt != pl.images_per_launch && !make_k3_plan(s, cur, cnt)) return hipErrorInvalidValue;
+    if (cur.a.e.splits > 1 && !part_ws) return hipErrorInvalidValue;
+    K3Args a = cur.a;
+    a.x = reinterpret_cast<const uint16_t*>(x) + n0 * img_elems;
+    a.x_bytes = (uint32_t)(cnt * img_elems * 2);
+    a.w = w;
+    a.w_bytes = (uint32_t)(s.K * s.C * 9 * 2);
+    a.e.y = reinterpret_cast<uint16_t*>(y) + n0 * out_elems;
+    a.e.res = res ? reinterpret_cast<const uint16_t*>(res) + n0 * out_elems : nullptr;
+    a.e.b = b;
+    a.e.partial = reinterpret_cast<float*>(part_ws);
+    a.e.vec = 1;
+    const hipError_t e = k3_dispatch(cur, a, stream);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+std::string k3_describe(const Shape& s) {
+  K3Plan pl;
+  if (!make_k3_plan(s, pl)) return "implicit_gemm (3x3 halo/filter tiles): not applicable";
+  const K3Config c = kK3Configs[pl.cfg];
+  char buf[512];
+  snprintf(buf, sizeof(buf),
+           "implicit_gemm kernels=conv3x3_kernel<%d,%d,%d,%d,%d,%d,%d,%d>%s tile=%dx%d grid=%dx%d chunk=%d "
+           "halo_rows=%d halo_items=%d lds=%zu images_per_launch=%lld (loader waves: halo rows transposed to "
+           "pixel-major LDS, KCRS filters regrouped to tap-major LDS; compute waves: MFMA %dx%d per wave)",
+           c.CH, c.WP, c.WK, c.MB, c.NB, pl.s2 ? 1 : 0, pl.upx, pl.a.halo_items > 256 ? 2 : 1,
+           pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "",
+           c.tp(), c.tk(), pl.a.ptiles * pl.a.ktiles, pl.a.e.splits, c.CH, pl.a.VR, pl.a.halo_items, pl.lds,
+           (long long)pl.images_per_launch, 32 * c.MB, 32 * c.NB);
+  return buf;
+}
+
+}  // namespace convsel

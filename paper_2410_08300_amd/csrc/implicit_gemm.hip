@@ -1366,7 +1366,7 @@ std::string describe_typed(const Shape& s) {
 }  // namespace
 
 bool implicit_gemm_fits(const Shape& s) {
-  if (use_pointwise(s) || rows_applies(s) || ws_applies(s)) return true;
+  if (use_pointwise(s) || rows_applies(s) || k3_applies(s) || ws_applies(s)) return true;
   IgPlan pl;
   if (s.dtype == DT_F32) return make_plan<float>(s, pl);
   return make_plan<bf16_t>(s, pl);
@@ -1375,6 +1375,7 @@ bool implicit_gemm_fits(const Shape& s) {
 size_t implicit_gemm_packed_bytes(const Shape& s) {
   if (use_pointwise(s)) return (size_t)(s.K * s.C * s.esize());  // a plain copy of the filters
   if (rows_applies(s)) return rows_packed_bytes(s);
+  if (k3_applies(s)) return (size_t)(s.K * s.C * 9 * 2);  // a plain copy of the filters
   if (ws_applies(s)) return ws_packed_bytes(s);
   IgPlan pl;
   const bool ok = s.dtype == DT_F32 ? make_plan<float>(s, pl) : make_plan<bf16_t>(s, pl);
@@ -1383,6 +1384,7 @@ size_t implicit_gemm_packed_bytes(const Shape& s) {
 
 size_t implicit_gemm_split_bytes(const Shape& s) {
   if (rows_applies(s)) return 0;
+  if (k3_applies(s)) return k3_split_bytes(s);
   if (ws_applies(s)) return ws_split_bytes(s);
   if (use_pointwise(s)) return s.dtype == DT_F32 ? pw_split_bytes<float>(s) : pw_split_bytes<bf16_t>(s);
   return s.dtype == DT_F32 ? split_bytes_typed<float>(s) : split_bytes_typed<bf16_t>(s);
@@ -1394,14 +1396,15 @@ size_t implicit_gemm_workspace(const Shape& s) {
 
 hipError_t launch_implicit_pack(const Shape& s, const void* w, void* wp, hipStream_t stream) {
   if (rows_applies(s)) return rows_pack(s, w, wp, stream);
+  if (k3_applies(s) || use_pointwise(s)) return launch_copy(w, wp, implicit_gemm_packed_bytes(s), stream);
   if (ws_applies(s)) return ws_pack(s, w, wp, stream);
-  if (use_pointwise(s)) return launch_copy(w, wp, implicit_gemm_packed_bytes(s), stream);
   return s.dtype == DT_F32 ? pack_typed<float>(s, w, wp, stream) : pack_typed<bf16_t>(s, w, wp, stream);
 }
 
 hipError_t launch_implicit_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* part,
                                 hipStream_t stream, const void* res) {
   if (rows_applies(s)) return rows_main(s, x, wp, b, y, stream, res);
+  if (k3_applies(s)) return k3_main(s, x, wp, b, y, part, stream, res);
   if (ws_applies(s)) return ws_main(s, x, wp, b, y, part, stream, res);
   if (use_pointwise(s))
     return s.dtype == DT_F32 ? pw_main_typed<float>(s, x, wp, b, y, part, res, stream)
@@ -1416,7 +1419,8 @@ hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, co
   // A 1x1 layer reads its filters as given when they are 16-byte aligned;
   // otherwise (and for every other layer) the package is built in the
   // workspace first.
-  if (use_pointwise(s) && reinterpret_cast<uintptr_t>(w) % 16 == 0) return launch_implicit_main(s, x, w, b, y, part, stream);
+  if ((use_pointwise(s) || k3_applies(s)) && reinterpret_cast<uintptr_t>(w) % 16 == 0)
+    return launch_implicit_main(s, x, w, b, y, part, stream);
   if (!ws) return hipErrorInvalidValue;
   hipError_t e = launch_implicit_pack(s, w, ws, stream);
   if (e != hipSuccess) return e;
@@ -1425,6 +1429,7 @@ hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, co
 
 std::string implicit_gemm_describe(const Shape& s) {
   if (rows_applies(s)) return rows_describe(s);
+  if (k3_applies(s)) return k3_describe(s);
   if (ws_applies(s)) return ws_describe(s);
   if (use_pointwise(s)) return s.dtype == DT_F32 ? pw_describe<float>(s) : pw_describe<bf16_t>(s);
   return s.dtype == DT_F32 ? describe_typed<float>(s) : describe_typed<bf16_t>(s);

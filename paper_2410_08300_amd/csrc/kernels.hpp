@@ -61,6 +61,15 @@ hipError_t rows_main(const Shape& s, const void* x, const void* wp, const void* 
                      const void* res = nullptr);
 std::string rows_describe(const Shape& s);
 
+// Implicit GEMM for bf16 3x3 layers, stride 1 or 2, dilation 1, one group,
+// C a multiple of 16, W >= 4: filters read as given (KCRS, 16-byte aligned),
+// split-K partials (k3_split_bytes) the only workspace.
+bool k3_applies(const Shape& s);
+size_t k3_split_bytes(const Shape& s);
+hipError_t k3_main(const Shape& s, const void* x, const void* w, const void* b, void* y, void* part_ws,
+                   hipStream_t stream, const void* res = nullptr);
+std::string k3_describe(const Shape& s);
+
 // Implicit GEMM with loader and compute waves (bf16, one group, nine taps,
 // C > 8): its own filter package ([16-channel chunk][K padded][19 units]),
 // plus split-K partials.

@@ -114,21 +114,34 @@ def test_workspace_sizes():
     per_img = 112 * 112 * 512 * 9 * 2
     assert _lib.workspace_bytes(big, "im2col_gemm") == (1 << 30) // per_img * per_img
     assert _lib.workspace_bytes(_lib.make_desc(0, 4, 8, 8, 4, 3, 3), "im2col_gemm") == 0
-    # implicit GEMM, bf16 3x3: the loader/compute-wave kernel's package is
-    # [16-channel chunk][K padded to the tile][19 units of 8 channels] (9
-    # taps x 2 channel groups + a zero unit), plus fp32 split partial sums
-    # for small grids.
-    # 64 -> 64 channels, 56x56, batch 32: 784 tiles of 64 x 128, no split.
+    # implicit GEMM, bf16 3x3 (stride 1 or 2, C a multiple of 16): the filters
+    # are read as given (the per-call workspace only holds a copy for
+    # unaligned filter pointers), plus fp32 split partial sums for small
+    # grids.
+    # 64 -> 64 channels, 56x56, batch 32: 196 tiles of 512 x 64, no split.
     large = _lib.make_desc(32, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, "bf16")
-    assert _lib.workspace_bytes(large, "implicit_gemm") == 4 * 64 * 19 * 16
-    assert "implicit_ws_kernel<64,1,1>" in _lib.describe(large, "implicit_gemm")
-    # 512 -> 512 channels, 7x7, batch 32: 13 x 4 tiles of 128 x 128 leave
-    # most of 256 CUs idle, so the 32 chunks are split four ways; the odd
-    # plane width takes the pixel-by-pixel halo loads.
+    assert _lib.workspace_bytes(large, "implicit_gemm") == 64 * 64 * 9 * 2
+    assert _lib.prepacked_workspace_bytes(large, "implicit_gemm") == 0
+    assert "conv3x3_kernel<16,4,1,4,2,0,8,1> tile=512x64 grid=196x1" in _lib.describe(large, "implicit_gemm")
+    # 256 -> 256 channels, 14x14, batch 32: 49 x 2 tiles of 128 x 128 split
+    # two ways over the 16 channel chunks.
+    mid = _lib.make_desc(32, 256, 14, 14, 256, 3, 3, 1, 1, 1, 1, "bf16")
+    part = 2 * 32 * 256 * 196 * 4
+    assert _lib.prepacked_workspace_bytes(mid, "implicit_gemm") == part
+    assert "conv3x3_kernel<16,2,2,2,2,0,8,1>;splitk_reduce_kernel tile=128x128 grid=98x2" in \
+        _lib.describe(mid, "implicit_gemm")
+    # Stride 2 splits rows into column-parity planes; 7-wide rows load in
+    # 4-pixel windows.
+    s2 = _lib.make_desc(32, 512, 14, 14, 512, 3, 3, 2, 1, 1, 1, "bf16")
+    assert "conv3x3_kernel<32,2,2,1,1,1,8,1>" in _lib.describe(s2, "implicit_gemm")
     small = _lib.make_desc(32, 512, 7, 7, 512, 3, 3, 1, 1, 1, 1, "bf16")
-    packed = 32 * 512 * 19 * 16
-    assert _lib.workspace_bytes(small, "implicit_gemm") == packed + 4 * 32 * 512 * 49 * 4
-    assert "implicit_ws_kernel<128,0,1>;splitk_reduce_kernel" in _lib.describe(small, "implicit_gemm")
+    assert "conv3x3_kernel<32,2,2,1,1,0,4,1>" in _lib.describe(small, "implicit_gemm")
+    # Other bf16 3x3 layers (channels not a multiple of 16, dilation, planes
+    # below 8 pixels) keep the loader/compute-wave kernel and its package
+    # [16-channel chunk][K padded to the tile][19 units of 8 channels].
+    odd = _lib.make_desc(2, 24, 9, 9, 40, 3, 3, 1, 1, 1, 1, "bf16")
+    assert _lib.workspace_bytes(odd, "implicit_gemm") == 2 * 64 * 19 * 16
+    assert "implicit_ws_kernel<64,0,1>" in _lib.describe(odd, "implicit_gemm")
     # fp32 3x3 keeps the general kernel: [chunk][K padded][tap][units].
     f32 = _lib.make_desc(32, 64, 56, 56, 64, 3, 3, 1, 1, 1, 1, "f32")
     assert _lib.workspace_bytes(f32, "implicit_gemm") == 8 * 64 * 18 * 16
