@@ -148,6 +148,21 @@ conv_algo_t conv2d_default_algo(const conv2d_desc_t* desc);
 conv_status_t conv2d(const void* x, const void* w, const void* b, void* y, const conv2d_desc_t* desc,
                      conv_algo_t algo, void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): conv2d()
+ * without the workspace arguments.  Its workspace is a library-owned static
+ * device array of conv2d_static_scratch_capacity() bytes (32 MiB), one per
+ * GPU, held until the process ends; the call itself allocates nothing and
+ * runs the same kernels as conv2d(), so the results are identical.
+ * Returns WORKSPACE (before any HIP call) when conv2d_workspace_bytes() of
+ * the layer and algo exceeds the capacity; otherwise as conv2d().  Every
+ * call on one GPU shares that GPU's array: calls that may run at the same
+ * time on one GPU (different streams, host threads) race and must be
+ * serialised by the caller; nothing in the array needs to start at zero. */
+conv_status_t conv2d_static_scratch(const void* x, const void* w, const void* b, void* y, const conv2d_desc_t* desc,
+                                    conv_algo_t algo, void* stream);
+size_t conv2d_static_scratch_capacity(void);
+
 /* Filter packages.  Implicit GEMM and Winograd first rearrange the filters
  * (implicit GEMM: into its tile layout, zero-padded; implicit precomputed-
  * index GEMM: zero-padded filters plus its index tables; KN2ROW: the

@@ -25,7 +25,7 @@ EXPORTED = ("conv2d_output_shape", "conv2d_check", "conv2d_workspace_bytes", "co
             "conv2d", "conv2d_packed_filter_bytes", "conv2d_pack_filters", "conv2d_prepacked_workspace_bytes",
             "conv2d_prepacked", "conv2d_describe", "conv2d_im2col", "conv2d_winograd_filter_transform",
             "conv2d_winograd_input_transform", "conv2d_status_string", "conv2d_algo_name",
-            "conv2d_algo_from_name")
+            "conv2d_algo_from_name", "conv2d_static_scratch", "conv2d_static_scratch_capacity")
 
 
 EXPORTED_MODEL = ("convsel_model_create", "convsel_model_destroy", "convsel_model_conv", "convsel_model_linear",
@@ -79,6 +79,10 @@ def lib():
         L.conv2d_default_algo.restype = i32
         L.conv2d.argtypes = [vp, vp, vp, vp, dp, i32, vp, ctypes.c_size_t, vp]
         L.conv2d.restype = i32
+        L.conv2d_static_scratch.argtypes = [vp, vp, vp, vp, dp, i32, vp]
+        L.conv2d_static_scratch.restype = i32
+        L.conv2d_static_scratch_capacity.argtypes = []
+        L.conv2d_static_scratch_capacity.restype = ctypes.c_size_t
         L.conv2d_packed_filter_bytes.argtypes = [dp, i32, ctypes.POINTER(ctypes.c_size_t)]
         L.conv2d_packed_filter_bytes.restype = i32
         L.conv2d_pack_filters.argtypes = [vp, vp, dp, i32, vp]
@@ -221,6 +225,16 @@ def conv2d_raw(x_ptr, w_ptr, b_ptr, y_ptr, desc, algo, ws_ptr, ws_bytes, stream)
     """conv2d() on raw device addresses (ints); returns the status."""
     return lib().conv2d(x_ptr, w_ptr, b_ptr, y_ptr, ctypes.byref(desc),
                         algo_id(algo) if isinstance(algo, str) else int(algo), ws_ptr, ws_bytes, stream)
+
+
+def conv2d_static_scratch_raw(x_ptr, w_ptr, b_ptr, y_ptr, desc, algo, stream):
+    """conv2d_static_scratch() on raw device addresses (ints); returns the status."""
+    return lib().conv2d_static_scratch(x_ptr, w_ptr, b_ptr, y_ptr, ctypes.byref(desc),
+                                       algo_id(algo) if isinstance(algo, str) else int(algo), stream)
+
+
+def static_scratch_capacity():
+    return int(lib().conv2d_static_scratch_capacity())
 
 
 def im2col_raw(x_ptr, col_ptr, desc, stream):

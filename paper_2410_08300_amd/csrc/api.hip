@@ -212,6 +212,35 @@ conv_status_t ensure_device() {
   return g_dev_state[dev] == 1 ? CONV_OK : CONV_ERR_DEVICE;
 }
 
+// Scratch of conv2d_static_scratch(): the workspace of callers that cannot
+// allocate.  A device global, so every GPU the library runs on holds its own
+// copy (from module load until the process ends).  Host code must not use
+// the array's name as an address: the per-device address comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+void* g_scratch_ptr[64];
+
+// This device's scratch address, or nullptr if it cannot be found (the
+// caller's device is already checked by ensure_device()).
+void* scratch_for_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_dev_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
 conv_status_t from_hip(hipError_t e) {
   if (e == hipSuccess) return CONV_OK;
   (void)hipGetLastError();
@@ -422,6 +451,27 @@ conv_status_t conv2d(const void* x, const void* w, const void* b, void* y, const
   if (st != CONV_OK || s.N == 0) return st;
   return run(s, algo, x, w, nullptr, b, y, workspace, (hipStream_t)stream);
 }
+
+conv_status_t conv2d_static_scratch(const void* x, const void* w, const void* b, void* y, const conv2d_desc_t* desc,
+                                    conv_algo_t algo, void* stream) {
+  Shape s;
+  conv_status_t st = validate(desc, &s);
+  if (st != CONV_OK) return st;
+  if (algo == CONV_ALGO_DEFAULT) algo = default_rule(s);
+  st = support(s, algo);
+  if (st != CONV_OK) return st;
+  if (workspace_for(s, algo) > kScratchBytes) return CONV_ERR_WORKSPACE;
+  if (s.N == 0) return CONV_OK;
+  st = ensure_device();
+  if (st != CONV_OK) return st;
+  void* ws = scratch_for_current_device();
+  if (!ws) return CONV_ERR_DEVICE;
+  st = prepare_call(desc, &algo, &s, x, w, b, y, ws, kScratchBytes, false);
+  if (st != CONV_OK) return st;
+  return run(s, algo, x, w, nullptr, b, y, ws, (hipStream_t)stream);
+}
+
+size_t conv2d_static_scratch_capacity(void) { return kScratchBytes; }
 
 conv_status_t conv2d_packed_filter_bytes(const conv2d_desc_t* desc, conv_algo_t algo, size_t* bytes) {
   Shape s;

@@ -309,3 +309,17 @@ def test_default_choice_walks_the_fitted_tree():
             assert _lib.default_algo(d) == F.predict(nodes, ranks, sh, supported), sh
             checked += 1
     assert checked > 200
+
+
+def test_static_scratch_rejects_layers_beyond_its_capacity_before_any_device_call():
+    """conv2d_static_scratch: a layer whose workspace exceeds the library's
+    static scratch is refused with WORKSPACE on the host; N = 0 is a no-op."""
+    cap = _lib.static_scratch_capacity()
+    assert cap == 32 << 20
+    big = _lib.make_desc(128, 256, 112, 112, 512, 1, 1, 1, 0, 1, 1, "bf16")
+    assert _lib.workspace_bytes(big, "implicit_gemm") > cap or _lib.workspace_bytes(big, "im2col_gemm") > cap
+    algo = "implicit_gemm" if _lib.workspace_bytes(big, "implicit_gemm") > cap else "im2col_gemm"
+    fake = 1 << 20  # never dereferenced: the size check comes first
+    assert _lib.conv2d_static_scratch_raw(fake, fake * 2, None, fake * 3, big, algo, None) == _lib.CONV_ERR_WORKSPACE
+    empty = _lib.make_desc(0, 4, 8, 8, 4, 3, 3, 1, 1)
+    assert _lib.conv2d_static_scratch_raw(None, None, None, None, empty, "direct", None) == _lib.CONV_OK
