@@ -651,21 +651,21 @@ bool make_k3_plan_cfg(const Shape& s, int cfg, K3Plan& pl, int64_t N1) {
   return true;
 }
 
-// Estimated time of a plan in units of one 32x32x16 MFMA per SIMD: rounds of
-// workgroups over the CUs times the MFMAs per compute wave of one workgroup,
-// divided by the wave tile's operand reuse efficiency, plus a pass over the
-// partial sums when the channels are split.
+// Estimated time of a plan, in microseconds: rounds of workgroups over the
+// CUs times the MFMAs of one compute wave (32 cycles each at about 2.1 GHz)
+// divided by the tile's measured efficiency (the loaders, not the MFMAs,
+// bound these kernels: smaller tiles reload the filters for fewer pixels),
+// plus the first chunk's latency, plus, when the channels are split, the
+// fp32 partial sums written and read back and the reduction's launch.
 double k3_cost(const K3Plan& pl) {
+  static constexpr double kEff[kNumK3Configs] = {0.45, 0.40, 0.30, 0.20};
   const K3Config c = kK3Configs[pl.cfg];
   const K3Args& a = pl.a;
   const int64_t wgs = (int64_t)a.ptiles * a.ktiles * a.e.splits;
   const double rounds = (double)((wgs + kCUs - 1) / kCUs);
-  const double mfma = (double)a.chunks_per_split * kK3Taps * (c.CH / 16) * c.MB * c.NB * (c.nc() / 4.0);
-  const double reuse = (double)(c.MB * c.NB) / (c.MB + c.NB);  // MFMAs per fragment read
-  const double eff = reuse >= 1.3 ? 1.0 : reuse >= 1.0 ? 0.9 : 0.75;
-  const double fill = 3.0 * kK3Taps * (c.CH / 16) * c.MB * c.NB;  // the first chunk's latency
-  double t = rounds * (mfma / eff + fill);
-  if (a.e.splits > 1) t += (double)a.e.splits * a.NPQ * a.K / (kCUs * 64.0 * 8.0);
+  const double mfma = (double)a.chunks_per_split * kK3Taps * (c.CH / 16) * c.MB * c.NB;
+  double t = rounds * mfma * (32.0 / 2100.0) / kEff[pl.cfg] + 3.0;
+  if (a.e.splits > 1) t += 3.0 + (double)a.e.splits * a.NPQ * a.K * 8.0 / 3.0e6;
   return t;
 }
 

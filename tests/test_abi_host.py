@@ -123,19 +123,22 @@ def test_workspace_sizes():
     assert _lib.workspace_bytes(large, "implicit_gemm") == 64 * 64 * 9 * 2
     assert _lib.prepacked_workspace_bytes(large, "implicit_gemm") == 0
     assert "conv3x3_kernel<16,4,1,4,2,0,8,1> tile=512x64 grid=196x1" in _lib.describe(large, "implicit_gemm")
-    # 256 -> 256 channels, 14x14, batch 32: 49 x 2 tiles of 128 x 128 split
-    # two ways over the 16 channel chunks.
+    # 256 -> 256 channels, 14x14, batch 32: 49 x 4 tiles of 128 x 64, no
+    # split (a split's fp32 partial sums cost more than the smaller tile).
     mid = _lib.make_desc(32, 256, 14, 14, 256, 3, 3, 1, 1, 1, 1, "bf16")
-    part = 2 * 32 * 256 * 196 * 4
-    assert _lib.prepacked_workspace_bytes(mid, "implicit_gemm") == part
-    assert "conv3x3_kernel<16,2,2,2,2,0,8,1>;splitk_reduce_kernel tile=128x128 grid=98x2" in \
-        _lib.describe(mid, "implicit_gemm")
+    assert _lib.prepacked_workspace_bytes(mid, "implicit_gemm") == 0
+    assert "conv3x3_kernel<32,2,2,2,1,0,8,1> tile=128x64 grid=196x1" in _lib.describe(mid, "implicit_gemm")
+    # 512 -> 512 channels, 7x7: 13 x 8 tiles of 128 x 64 split two ways.
+    s7 = _lib.make_desc(32, 512, 7, 7, 512, 3, 3, 1, 1, 1, 1, "bf16")
+    assert _lib.prepacked_workspace_bytes(s7, "implicit_gemm") == 2 * 32 * 512 * 49 * 4
+    assert "conv3x3_kernel<32,2,2,2,1,0,4,1>;splitk_reduce_kernel tile=128x64 grid=104x2" in \
+        _lib.describe(s7, "implicit_gemm")
     # Stride 2 splits rows into column-parity planes; 7-wide rows load in
     # 4-pixel windows.
-    s2 = _lib.make_desc(32, 512, 14, 14, 512, 3, 3, 2, 1, 1, 1, "bf16")
-    assert "conv3x3_kernel<32,2,2,1,1,1,8,1>" in _lib.describe(s2, "implicit_gemm")
-    small = _lib.make_desc(32, 512, 7, 7, 512, 3, 3, 1, 1, 1, 1, "bf16")
-    assert "conv3x3_kernel<32,2,2,1,1,0,4,1>" in _lib.describe(small, "implicit_gemm")
+    s2 = _lib.make_desc(32, 128, 56, 56, 128, 3, 3, 2, 1, 1, 1, "bf16")
+    assert "conv3x3_kernel<16,2,2,2,2,1,8,1> tile=128x128 grid=196x1" in _lib.describe(s2, "implicit_gemm")
+    small = _lib.make_desc(32, 64, 7, 7, 128, 3, 3, 1, 1, 1, 1, "bf16")
+    assert "conv3x3_kernel<32,2,2,1,1,0,4,1> tile=64x64" in _lib.describe(small, "implicit_gemm")
     # Other bf16 3x3 layers (channels not a multiple of 16, dilation, planes
     # below 8 pixels) keep the loader/compute-wave kernel and its package
     # [16-channel chunk][K padded to the tile][19 units of 8 channels].
