@@ -245,7 +245,7 @@ __device__ __forceinline__ void k3_epilogue(const f32x16_t (&acc)[MB][NB], char*
   }
 }
 
-template <int CH, int WP, int WK, int MB, int NB, bool S2, int UPX, int HS>
+template <int CH, int WP, int WK, int MB, int NB, bool S2, int UPX, int HS, bool PK>
 __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Args a) {
   constexpr int NC = WP * WK;                 // compute waves
   constexpr int TP = WP * MB * 32, TK = WK * NB * 32;
@@ -287,6 +287,9 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
     const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
     const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
     const uint32_t plane = static_cast<uint32_t>(a.H * a.W * 2);
+    // With a filter package (PK) loader waves 0-1 load the halo and waves 2-3
+    // copy the filter tiles by DMA; otherwise all four do both.
+    constexpr int HL = PK ? 128 : 256;  // halo lanes
     // Halo items: (channel group g, halo row vr, column window gc).  The
     // per-lane offset is that of channel 8g; the chunk's channels go into
     // the scalar offset.  Rows outside the image read zeros.
@@ -296,12 +299,12 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
     int hg[HS];
 #pragma unroll
     for (int t = 0; t < HS; ++t) {
-      const int it = lt + t * 256;
+      const int it = lt + t * HL;
       hvo[t] = a.x_bytes;
       hrow[t] = -1;
       hcol[t] = 0;
       hg[t] = 0;
-      if (it < a.halo_items) {
+      if (lt < HL && it < a.halo_items) {
         // Rows fastest: consecutive lanes write slots a halo row apart,
         // not UPX slots apart (which would put them all in one bank group).
         const int per_g = a.VR * a.NG;
@@ -317,13 +320,150 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
         hcol[t] = ws + a.pw;
       }
     }
+    constexpr int HD = UPX / 2;  // dwords per channel of a window
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    // Chunks past the last re-read the last one (never written to LDS), so
+    // the issue sequence does not depend on the chunk count.
+    auto chunk_of = [&](int ch) { return ch < nchunks ? ch : nchunks - 1; };
+    if constexpr (PK) {
+      constexpr int NST = 3;
+      if (lt >= HL) {
+        // ---- filter DMA waves: chunk i's tile lands in stage i % 3 ----
+        // The package holds each (chunk, channel tile) filter tile as
+        // [tap][TK][CH], FU 16-byte units; DMA instruction j of wave dw
+        // fills LDS units (dw FI + j) 64 + lane, and a lane fetches the
+        // package unit that the bank swizzle puts there.
+        constexpr int FU = kK3Taps * TK * CH / 8;
+        constexpr int FI = FU / 128;
+        static_assert(FU % 128 == 0 && FI <= 31, "DMA split");
+        const int dw = wave - NC - 2;
+        uint32_t dvo[FI];
+#pragma unroll
+        for (int j = 0; j < FI; ++j) {
+          const int u = (dw * FI + j) * 64 + lane;
+          const int row = u / UP, phys = u - (u / UP) * UP;
+          dvo[j] = static_cast<uint32_t>(row * UP + (phys ^ k3_swz<UP>(row % TK))) * 16;
+        }
+        auto dma = [&](int ch, int st) {
+          const uint32_t so = static_cast<uint32_t>(((ch_begin + ch) * a.ktiles + ktile) * FU) * 16;
+          char __attribute__((address_space(3)))* Fs =
+              (char __attribute__((address_space(3)))*)(lds + st * a.stage_bytes + a.halo_bytes);
+#pragma unroll
+          for (int j = 0; j < FI; ++j) {
+            // (The offset goes through a scalar: with the array element as the
+            // operand, hipcc's host pass silently drops the kernel's stub.)
+            const uint32_t vo = dvo[j];
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void_t*)(Fs + (dw * FI + j) * 1024), 16, vo, so, 0, 0);
+          }
+        };
+        dma(0, 0);
+        if (nchunks > 1) dma(1, 1);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();  // the padding is clear
+        int st2 = 2;                   // stage of chunk i + 2
+        for (int i = 0; i < npairs * 2; ++i) {
+          if (i < nchunks) {
+            // chunk i's tile must have landed; chunk i+1's may stay in flight
+            if (i + 1 < nchunks) CONVSEL_WAIT_VMCNT(FI); else CONVSEL_WAIT_VMCNT(0);
+          }
+          asm volatile("" ::: "memory");
+          __builtin_amdgcn_s_barrier();  // A(i)
+          asm volatile("" ::: "memory");
+          if (i + 2 < nchunks) dma(i + 2, st2);  // its stage held chunk i-1, freed at B(i-1)
+          st2 = st2 == NST - 1 ? 0 : st2 + 1;
+          asm volatile("" ::: "memory");
+          __builtin_amdgcn_s_barrier();  // B(i)
+          asm volatile("" ::: "memory");
+        }
+        return;
+      }
+      // ---- halo waves: register path, two sets, three stages ----
+      uint32_t hd[2][HS][8][HD];
+      auto issue_h = [&](int ch, auto set_c) {
+        constexpr int SET = decltype(set_c)::value;
+        const int c0 = (ch_begin + ch) * CH;
+#pragma unroll
+        for (int t = 0; t < HS; ++t) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const uint32_t so = static_cast<uint32_t>(c0 + e) * plane;
+            if constexpr (UPX == 8) {
+              const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(xr, hvo[t], so, 0);
+              hd[SET][t][e][0] = v[0]; hd[SET][t][e][1] = v[1]; hd[SET][t][e][2] = v[2]; hd[SET][t][e][3] = v[3];
+            } else {
+              const auto v = __builtin_amdgcn_raw_buffer_load_b64(xr, hvo[t], so, 0);
+              hd[SET][t][e][0] = v[0]; hd[SET][t][e][1] = v[1];
+            }
+          }
+        }
+      };
+      auto write_h = [&](int st, auto set_c) {
+        constexpr int SET = decltype(set_c)::value;
+        char* Hs = lds + st * a.stage_bytes;
+#pragma unroll
+        for (int t = 0; t < HS; ++t) {
+          if (hrow[t] >= 0) {
+#pragma unroll
+            for (int px = 0; px < UPX; ++px) {
+              u32x4_t o;
+#pragma unroll
+              for (int m = 0; m < 4; ++m) {
+                const uint32_t d0 = hd[SET][t][2 * m][px >> 1], d1 = hd[SET][t][2 * m + 1][px >> 1];
+                o[m] = (px & 1) ? ((d0 >> 16) | (d1 & 0xFFFF0000u)) : ((d0 & 0xFFFFu) | (d1 << 16));
+              }
+              const int pc = hcol[t] + px;
+              const int slot = S2 ? hrow[t] + (pc & 1) * a.PS + (pc >> 1) : hrow[t] + pc;
+              const int unit_ = hg[t] ^ k3_swz<UP>(slot);
+              *reinterpret_cast<u32x4_t*>(Hs + slot * (CH * 2) + unit_ * 16) = o;
+            }
+          }
+        }
+      };
+      constexpr int PH = HS * 8;
+      issue_h(0, S0{});
+      issue_h(chunk_of(1), S1{});
+      for (int i = lt; i < a.halo_bytes / 16; i += HL) {
+#pragma unroll
+        for (int st = 0; st < NST; ++st) reinterpret_cast<u32x4_t*>(lds + st * a.stage_bytes)[i] = u32x4_t{0u, 0u, 0u, 0u};
+      }
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      __builtin_amdgcn_s_barrier();  // the padding is clear
+      asm volatile("" ::: "memory");
+      CONVSEL_WAIT_VMCNT(PH);  // chunk 0 (chunk 1's loads may stay in flight)
+      write_h(0, S0{});
+      issue_h(chunk_of(2), S0{});
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      int st1 = 1;  // stage of chunk i + 1
+      auto hstep = [&](int i, auto set_c) {  // set_c: (i + 1) & 1
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();  // A(i)
+        asm volatile("" ::: "memory");
+        CONVSEL_WAIT_VMCNT(PH);
+        if (i + 1 < nchunks) write_h(st1, set_c);  // its stage held chunk i-2, freed at B(i-2)
+        issue_h(chunk_of(i + 3), set_c);
+        st1 = st1 == NST - 1 ? 0 : st1 + 1;
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();  // B(i)
+        asm volatile("" ::: "memory");
+      };
+      for (int i = 0; i < npairs * 2; i += 2) {
+        hstep(i, S1{});
+        hstep(i + 1, S0{});
+      }
+      CONVSEL_WAIT_VMCNT(0);
+      return;
+    }
     // Filter items: (filter row kl, channel group g); rows past K read zeros.
     const int kl = lt / UP, fg = lt - (lt / UP) * UP;
     const bool f_on = kl < TK;
     const uint32_t fvo = (f_on && k0 + kl < a.K)
                              ? static_cast<uint32_t>(((k0 + kl) * a.C + 8 * fg) * kK3Taps) * 2
                              : a.w_bytes;
-    constexpr int HD = UPX / 2;  // dwords per channel of a window
     // Every chunk issues the same HS * 8 + 9 loads per lane (unused halo
     // slots read zeros past the buffer), so the compiler's own count of the
     // loads in flight matches the explicit waits below.
@@ -392,12 +532,6 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
         }
       }
     };
-    using S0 = std::integral_constant<int, 0>;
-    using S1 = std::integral_constant<int, 1>;
-    // Chunks past the last re-read the last one (never written to LDS), so
-    // the issue sequence does not depend on the chunk count.
-    auto chunk_of = [&](int ch) { return ch < nchunks ? ch : nchunks - 1; };
-
     // The first two chunks' loads go out before the workgroup clears the
     // halo padding, so the clearing and the wave launches overlap them.
     issue(0, S0{});
@@ -487,9 +621,11 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
   constexpr int NACC = MB * NB == 1 ? 2 : 1;
   f32x16_t acc2[1];  // the second accumulator (NACC == 2)
   acc2[0] = zero16();
+  int cst = 0;  // stage of chunk i
   for (int i = 0; i < nchunks; ++i) {
     lds_sync();  // A(i)
-    const char* Hs = lds + (i & 1) * a.stage_bytes;
+    const char* Hs = lds + cst * a.stage_bytes;
+    cst = cst == (PK ? 2 : 1) ? 0 : cst + 1;
     const char* Fs = Hs + a.halo_bytes;
     bf16x8_t fa[D + 1][MB], fb[D + 1][NB];
     auto read = [&](auto s_c) {
@@ -563,6 +699,7 @@ constexpr int kNumK3Configs = sizeof(kK3Configs) / sizeof(kK3Configs[0]);
 
 struct K3Plan {
   int cfg;
+  bool pk;   // filters from the tile-ordered package by DMA (three LDS stages)
   bool s2;
   int upx;
   int64_t images_per_launch;
@@ -604,10 +741,11 @@ bool k3_shape_ok(const Shape& s) {
   return true;
 }
 
-bool make_k3_plan_cfg(const Shape& s, int cfg, K3Plan& pl, int64_t N1) {
+bool make_k3_plan_cfg(const Shape& s, int cfg, K3Plan& pl, int64_t N1, bool pk = false) {
   const K3Config c = kK3Configs[cfg];
   if (s.C % c.CH != 0) return false;
   pl.cfg = cfg;
+  pl.pk = pk;
   pl.s2 = s.sh == 2;
   pl.upx = s.W >= 8 ? 8 : 4;
   pl.images_per_launch = N1;
@@ -632,11 +770,11 @@ bool make_k3_plan_cfg(const Shape& s, int cfg, K3Plan& pl, int64_t N1) {
   }
   a.NG = (int)((s.W + pl.upx - 1) / pl.upx);
   a.halo_items = a.VR * a.NG * (c.CH / 8);
-  if (a.halo_items > kHSMax * 256) return false;
+  if (a.halo_items > kHSMax * (pk ? 128 : 256)) return false;
   a.halo_bytes = (int)(((size_t)a.VR * a.RS * c.CH * 2 + 255) / 256 * 256);
   const size_t filt = (size_t)kK3Taps * c.tk() * c.CH * 2;
   a.stage_bytes = (int)(a.halo_bytes + filt);
-  pl.lds = (size_t)2 * a.stage_bytes;
+  pl.lds = (size_t)(pk ? 3 : 2) * a.stage_bytes;
   // The epilogue stages each compute wave's fp32 or bf16 rows in LDS.
   const size_t staging = (size_t)c.nc() * c.MB * 32 * 32 * 4;
   if (pl.lds < staging) pl.lds = staging;
@@ -669,7 +807,7 @@ double k3_cost(const K3Plan& pl) {
   return t;
 }
 
-bool make_k3_plan(const Shape& s, K3Plan& pl, int64_t N1 = -1) {
+bool make_k3_plan(const Shape& s, K3Plan& pl, int64_t N1 = -1, bool prepacked = false) {
   if (!k3_shape_ok(s)) return false;
   const int64_t img_bytes = s.C * s.H * s.W * 2;
   if (img_bytes > kMaxLaunchBytes) return false;
@@ -691,12 +829,76 @@ bool make_k3_plan(const Shape& s, K3Plan& pl, int64_t N1 = -1) {
       found = true;
     }
   }
-  return found;
+  if (!found) return false;
+  // Prepacked filters (built once, outside the call) go in by DMA from the
+  // package wherever its three stages fit, in every launch of the layer
+  // (the package's layout follows the tile shape); not for the 512-pixel
+  // tile, where the register path measured as fast.  A per-call package
+  // would cost its own launch, which measured more than the DMA saves, so
+  // conv2d() regroups the filters in the kernel.
+  K3Plan with_pk, rest;
+  const int64_t r = s.N % N1;
+  if (prepacked && pl.cfg != 0 && make_k3_plan_cfg(s, pl.cfg, with_pk, N1, true) &&
+      (r == 0 || make_k3_plan_cfg(s, pl.cfg, rest, r, true)))
+    pl = with_pk;
+  return true;
 }
 
-template <int CH, int WP, int WK, int MB, int NB, bool S2, int UPX, int HS>
+// Plan of a launch of `cnt` images with the tile shape and filter path of
+// the layer's plan.
+bool k3_plan_for_launch(const Shape& s, const K3Plan& pl, int64_t cnt, K3Plan& cur) {
+  if (cnt == pl.images_per_launch) {
+    cur = pl;
+    return true;
+  }
+  return make_k3_plan_cfg(s, pl.cfg, cur, cnt, pl.pk);
+}
+
+// Filter package: for chunk cg (CH channels) and channel tile kt, the LDS
+// image of the tile's filters, [tap][TK][CH], zero past K.  One thread per
+// (chunk, filter row, 8-channel group) reads the group's 8 x 9 values (72
+// consecutive bf16 of the KCRS filter) and writes its nine tap units.
+constexpr int kK3PackThreads = 128;
+__global__ __launch_bounds__(kK3PackThreads) void k3_pack_kernel(const uint16_t* __restrict__ w,
+                                                                 u32x4_t* __restrict__ pk, int K, int C, int Kpad,
+                                                                 int TK, int CH, int items, int vec) {
+  const int item = blockIdx.x * kK3PackThreads + threadIdx.x;
+  if (item >= items) return;
+  const int UP = CH / 8;
+  const int g = item % UP, rest = item / UP;
+  const int k = rest % Kpad, cg = rest / Kpad;
+  uint32_t v[72];  // element i = c * 9 + tap, c = 0..7
+  if (k < K && vec) {
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(w + (static_cast<int64_t>(k) * C + cg * CH + 8 * g) * 9);
+#pragma unroll
+    for (int q = 0; q < 9; ++q) {
+      const u32x4_t d = src[q];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[8 * q + 2 * e] = d[e] & 0xFFFFu;
+        v[8 * q + 2 * e + 1] = d[e] >> 16;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 72; ++i)
+      v[i] = k < K ? w[(static_cast<int64_t>(k) * C + cg * CH + 8 * g + i / 9) * 9 + i % 9] : 0u;
+  }
+  const int ktiles = Kpad / TK;
+  const int64_t FU = (int64_t)9 * TK * UP;
+  u32x4_t* dst = pk + (static_cast<int64_t>(cg) * ktiles + k / TK) * FU + (k % TK) * UP + g;
+#pragma unroll
+  for (int tap = 0; tap < 9; ++tap) {
+    u32x4_t o;
+#pragma unroll
+    for (int m = 0; m < 4; ++m) o[m] = v[(2 * m) * 9 + tap] | (v[(2 * m + 1) * 9 + tap] << 16);
+    dst[static_cast<int64_t>(tap) * TK * UP] = o;
+  }
+}
+
+template <int CH, int WP, int WK, int MB, int NB, bool S2, int UPX, int HS, bool PK>
 hipError_t k3_launch(const K3Plan& pl, const K3Args& a, hipStream_t stream) {
-  const auto kern = conv3x3_kernel<CH, WP, WK, MB, NB, S2, UPX, HS>;
+  const auto kern = conv3x3_kernel<CH, WP, WK, MB, NB, S2, UPX, HS, PK>;
   static std::atomic<int> lds_limit{64 * 1024};
   if ((int)pl.lds > lds_limit.load()) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -718,8 +920,11 @@ hipError_t k3_launch(const K3Plan& pl, const K3Args& a, hipStream_t stream) {
 
 template <int CH, int WP, int WK, int MB, int NB, bool S2, int UPX>
 hipError_t k3_dispatch_hs(const K3Plan& pl, const K3Args& a, hipStream_t st) {
-  return a.halo_items > 256 ? k3_launch<CH, WP, WK, MB, NB, S2, UPX, 2>(pl, a, st)
-                            : k3_launch<CH, WP, WK, MB, NB, S2, UPX, 1>(pl, a, st);
+  if (pl.pk)
+    return a.halo_items > 128 ? k3_launch<CH, WP, WK, MB, NB, S2, UPX, 2, true>(pl, a, st)
+                              : k3_launch<CH, WP, WK, MB, NB, S2, UPX, 1, true>(pl, a, st);
+  return a.halo_items > 256 ? k3_launch<CH, WP, WK, MB, NB, S2, UPX, 2, false>(pl, a, st)
+                            : k3_launch<CH, WP, WK, MB, NB, S2, UPX, 1, false>(pl, a, st);
 }
 
 template <int CH, int WP, int WK, int MB, int NB>
@@ -755,26 +960,51 @@ size_t k3_split_bytes(const Shape& s) {
   const int64_t rest = s.N % pl.images_per_launch;
   if (rest) {
     K3Plan last;
-    if (make_k3_plan(s, last, rest) && last.part_bytes > m) m = last.part_bytes;
+    if (k3_plan_for_launch(s, pl, rest, last) && last.part_bytes > m) m = last.part_bytes;
   }
   return m;
 }
 
-hipError_t k3_main(const Shape& s, const void* x, const void* w, const void* b, void* y, void* part_ws,
-                   hipStream_t stream, const void* res) {
+bool k3_uses_package(const Shape& s) {
   K3Plan pl;
-  if (!make_k3_plan(s, pl)) return hipErrorInvalidValue;
+  return make_k3_plan(s, pl, -1, true) && pl.pk;
+}
+
+size_t k3_package_bytes(const Shape& s) {
+  K3Plan pl;
+  if (!make_k3_plan(s, pl, -1, true) || !pl.pk) return 0;
+  return (size_t)pl.a.ktiles * kK3Configs[pl.cfg].tk() * s.C * 9 * 2;
+}
+
+hipError_t k3_pack(const Shape& s, const void* w, void* pk, hipStream_t stream) {
+  K3Plan pl;
+  if (!make_k3_plan(s, pl, -1, true) || !pl.pk) return hipErrorInvalidValue;
+  const K3Config c = kK3Configs[pl.cfg];
+  const int Kpad = pl.a.ktiles * c.tk();
+  const int items = (int)(s.C / c.CH) * Kpad * (c.CH / 8);
+  const int vec = reinterpret_cast<uintptr_t>(w) % 16 == 0;
+  hipLaunchKernelGGL(k3_pack_kernel, dim3((unsigned)((items + kK3PackThreads - 1) / kK3PackThreads)),
+                     dim3(kK3PackThreads), 0, stream, reinterpret_cast<const uint16_t*>(w),
+                     reinterpret_cast<u32x4_t*>(pk), (int)s.K, (int)s.C, Kpad, c.tk(), c.CH, items, vec);
+  return hipGetLastError();
+}
+
+hipError_t k3_main(const Shape& s, const void* x, const void* w, const void* b, void* y, void* part_ws,
+                   hipStream_t stream, const void* res, bool prepacked) {
+  K3Plan pl;
+  if (!make_k3_plan(s, pl, -1, prepacked)) return hipErrorInvalidValue;
   const int64_t img_elems = s.C * s.H * s.W, out_elems = s.K * s.P * s.Q;
   for (int64_t n0 = 0; n0 < s.N; n0 += pl.images_per_launch) {
     const int64_t cnt = s.N - n0 < pl.images_per_launch ? s.N - n0 : pl.images_per_launch;
-    K3Plan cur = pl;
-    if (cnt != pl.images_per_launch && !make_k3_plan(s, cur, cnt)) return hipErrorInvalidValue;
+    K3Plan cur;
+    if (!k3_plan_for_launch(s, pl, cnt, cur)) return hipErrorInvalidValue;
     if (cur.a.e.splits > 1 && !part_ws) return hipErrorInvalidValue;
     K3Args a = cur.a;
     a.x = reinterpret_cast<const uint16_t*>(x) + n0 * img_elems;
     a.x_bytes = (uint32_t)(cnt * img_elems * 2);
-    a.w = w;
-    a.w_bytes = (uint32_t)(s.K * s.C * 9 * 2);
+    a.w = w;  // the package when pl.pk, else the KCRS filters
+    a.w_bytes = pl.pk ? (uint32_t)((size_t)pl.a.ktiles * kK3Configs[pl.cfg].tk() * s.C * 9 * 2)
+                      : (uint32_t)(s.K * s.C * 9 * 2);
     a.e.y = reinterpret_cast<uint16_t*>(y) + n0 * out_elems;
     a.e.res = res ? reinterpret_cast<const uint16_t*>(res) + n0 * out_elems : nullptr;
     a.e.b = b;
@@ -786,19 +1016,23 @@ hipError_t k3_main(const Shape& s, const void* x, const void* w, const void* b, 
   return hipSuccess;
 }
 
-std::string k3_describe(const Shape& s) {
+std::string k3_describe(const Shape& s, bool prepacked) {
   K3Plan pl;
-  if (!make_k3_plan(s, pl)) return "implicit_gemm (3x3 halo/filter tiles): not applicable";
+  if (!make_k3_plan(s, pl, -1, prepacked)) return "implicit_gemm (3x3 halo/filter tiles): not applicable";
   const K3Config c = kK3Configs[pl.cfg];
   char buf[512];
   snprintf(buf, sizeof(buf),
-           "implicit_gemm kernels=conv3x3_kernel<%d,%d,%d,%d,%d,%d,%d,%d>%s tile=%dx%d grid=%dx%d chunk=%d "
+           "implicit_gemm kernels=%sconv3x3_kernel<%d,%d,%d,%d,%d,%d,%d,%d,%d>%s tile=%dx%d grid=%dx%d chunk=%d "
            "halo_rows=%d halo_items=%d lds=%zu images_per_launch=%lld (loader waves: halo rows transposed to "
-           "pixel-major LDS, KCRS filters regrouped to tap-major LDS; compute waves: MFMA %dx%d per wave)",
-           c.CH, c.WP, c.WK, c.MB, c.NB, pl.s2 ? 1 : 0, pl.upx, pl.a.halo_items > 256 ? 2 : 1,
+           "pixel-major LDS, %s; compute waves: MFMA %dx%d per wave)",
+           pl.pk ? "k3_pack_kernel;" : "", c.CH, c.WP, c.WK, c.MB, c.NB, pl.s2 ? 1 : 0, pl.upx,
+           pl.a.halo_items > (pl.pk ? 128 : 256) ? 2 : 1, pl.pk ? 1 : 0,
            pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "",
            c.tp(), c.tk(), pl.a.ptiles * pl.a.ktiles, pl.a.e.splits, c.CH, pl.a.VR, pl.a.halo_items, pl.lds,
-           (long long)pl.images_per_launch, 32 * c.MB, 32 * c.NB);
+           (long long)pl.images_per_launch,
+           pl.pk ? "filter tiles copied by DMA from the package, three LDS stages"
+                 : "KCRS filters regrouped to tap-major LDS, two LDS stages",
+           32 * c.MB, 32 * c.NB);
   return buf;
 }
 

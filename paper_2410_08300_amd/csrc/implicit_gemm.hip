@@ -1375,7 +1375,7 @@ bool implicit_gemm_fits(const Shape& s) {
 size_t implicit_gemm_packed_bytes(const Shape& s) {
   if (use_pointwise(s)) return (size_t)(s.K * s.C * s.esize());  // a plain copy of the filters
   if (rows_applies(s)) return rows_packed_bytes(s);
-  if (k3_applies(s)) return (size_t)(s.K * s.C * 9 * 2);  // a plain copy of the filters
+  if (k3_applies(s)) return k3_uses_package(s) ? k3_package_bytes(s) : (size_t)(s.K * s.C * 9 * 2);
   if (ws_applies(s)) return ws_packed_bytes(s);
   IgPlan pl;
   const bool ok = s.dtype == DT_F32 ? make_plan<float>(s, pl) : make_plan<bf16_t>(s, pl);
@@ -1396,6 +1396,7 @@ size_t implicit_gemm_workspace(const Shape& s) {
 
 hipError_t launch_implicit_pack(const Shape& s, const void* w, void* wp, hipStream_t stream) {
   if (rows_applies(s)) return rows_pack(s, w, wp, stream);
+  if (k3_applies(s) && k3_uses_package(s)) return k3_pack(s, w, wp, stream);
   if (k3_applies(s) || use_pointwise(s)) return launch_copy(w, wp, implicit_gemm_packed_bytes(s), stream);
   if (ws_applies(s)) return ws_pack(s, w, wp, stream);
   return s.dtype == DT_F32 ? pack_typed<float>(s, w, wp, stream) : pack_typed<bf16_t>(s, w, wp, stream);
@@ -1404,7 +1405,7 @@ hipError_t launch_implicit_pack(const Shape& s, const void* w, void* wp, hipStre
 hipError_t launch_implicit_main(const Shape& s, const void* x, const void* wp, const void* b, void* y, void* part,
                                 hipStream_t stream, const void* res) {
   if (rows_applies(s)) return rows_main(s, x, wp, b, y, stream, res);
-  if (k3_applies(s)) return k3_main(s, x, wp, b, y, part, stream, res);
+  if (k3_applies(s)) return k3_main(s, x, wp, b, y, part, stream, res, true);
   if (ws_applies(s)) return ws_main(s, x, wp, b, y, part, stream, res);
   if (use_pointwise(s))
     return s.dtype == DT_F32 ? pw_main_typed<float>(s, x, wp, b, y, part, res, stream)
@@ -1419,8 +1420,19 @@ hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, co
   // A 1x1 layer reads its filters as given when they are 16-byte aligned;
   // otherwise (and for every other layer) the package is built in the
   // workspace first.
-  if ((use_pointwise(s) || k3_applies(s)) && reinterpret_cast<uintptr_t>(w) % 16 == 0)
-    return launch_implicit_main(s, x, w, b, y, part, stream);
+  if (use_pointwise(s) && reinterpret_cast<uintptr_t>(w) % 16 == 0) return launch_implicit_main(s, x, w, b, y, part, stream);
+  if (k3_applies(s)) {
+    // The filters as given (a copy in the workspace when they are not
+    // 16-byte aligned), regrouped inside the kernel.
+    const void* wk = w;
+    if (reinterpret_cast<uintptr_t>(w) % 16 != 0) {
+      if (!ws) return hipErrorInvalidValue;
+      hipError_t e = launch_copy(w, ws, (size_t)(s.K * s.C * 9 * 2), stream);
+      if (e != hipSuccess) return e;
+      wk = ws;
+    }
+    return k3_main(s, x, wk, b, y, part, stream, nullptr, false);
+  }
   if (!ws) return hipErrorInvalidValue;
   hipError_t e = launch_implicit_pack(s, w, ws, stream);
   if (e != hipSuccess) return e;
@@ -1429,7 +1441,15 @@ hipError_t launch_implicit_gemm(const Shape& s, const void* x, const void* w, co
 
 std::string implicit_gemm_describe(const Shape& s) {
   if (rows_applies(s)) return rows_describe(s);
-  if (k3_applies(s)) return k3_describe(s);
+  if (k3_applies(s)) {
+    std::string d = k3_describe(s);
+    if (k3_uses_package(s)) {
+      const std::string p = k3_describe(s, true);
+      const size_t a = p.find("conv3x3_kernel"), b = p.find(' ', a);
+      d += " prepacked_kernel=" + p.substr(a, b - a);
+    }
+    return d;
+  }
   if (ws_applies(s)) return ws_describe(s);
   if (use_pointwise(s)) return s.dtype == DT_F32 ? pw_describe<float>(s) : pw_describe<bf16_t>(s);
   return s.dtype == DT_F32 ? describe_typed<float>(s) : describe_typed<bf16_t>(s);

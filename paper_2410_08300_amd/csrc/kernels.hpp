@@ -62,13 +62,19 @@ hipError_t rows_main(const Shape& s, const void* x, const void* wp, const void* 
 std::string rows_describe(const Shape& s);
 
 // Implicit GEMM for bf16 3x3 layers, stride 1 or 2, dilation 1, one group,
-// C a multiple of 16, W >= 4: filters read as given (KCRS, 16-byte aligned),
-// split-K partials (k3_split_bytes) the only workspace.
+// C a multiple of 16, W >= 4, P*Q >= 8; workspace: the filter package (when
+// used) and split-K partials (k3_split_bytes).
 bool k3_applies(const Shape& s);
+// Whether prepacked calls copy the filter tiles by DMA from a package
+// (k3_package_bytes, built by k3_pack from the KCRS filters); otherwise, and
+// in every per-call conv2d(), the kernel reads the KCRS filters as given.
+bool k3_uses_package(const Shape& s);
+size_t k3_package_bytes(const Shape& s);
+hipError_t k3_pack(const Shape& s, const void* w, void* pk, hipStream_t stream);
 size_t k3_split_bytes(const Shape& s);
 hipError_t k3_main(const Shape& s, const void* x, const void* w, const void* b, void* y, void* part_ws,
-                   hipStream_t stream, const void* res = nullptr);
-std::string k3_describe(const Shape& s);
+                   hipStream_t stream, const void* res = nullptr, bool prepacked = false);
+std::string k3_describe(const Shape& s, bool prepacked = false);
 
 // Implicit GEMM with loader and compute waves (bf16, one group, nine taps,
 // C > 8): its own filter package ([16-channel chunk][K padded][19 units]),
