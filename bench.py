@@ -120,6 +120,8 @@ KERNEL_SOURCES = {
     "repack_plane_kernel": ("implicit_gemm.hip", "igemm_common.hpp"),
     "splitk_reduce_kernel": ("igemm_common.hpp",),
     "implicit_rows_kernel": ("implicit_rows.hip", "igemm_common.hpp"),
+    "conv3x3_kernel": ("conv3x3.hip", "igemm_common.hpp"),
+    "implicit_ws_kernel": ("implicit_ws.hip", "igemm_common.hpp"),
     "gemm_nt_kernel": ("gemm.hip",),
     "direct_": ("direct.hip",),
     "wino_": ("winograd.hip", "gemm.hip"),

@@ -17,14 +17,23 @@
 //     pixels of one tap are again consecutive slots;
 //   * the filters of the tile: [tap][TK][CH], swizzled the same way.
 //
-// Loader waves (the last kLoaders waves) fill these from the tensors as
-// given: NCHW input rows with 16-byte loads (8 pixels of one channel; 8
-// channels per lane), transposed in registers into 8 pixel vectors; KCRS
-// filters with nine 16-byte loads per (filter, 8 channels) -- the 72
-// consecutive values of 8 channels x 9 taps -- regrouped in registers into
-// nine tap vectors.  No packing kernel runs before the convolution.  Two LDS
-// stages alternate; while the compute waves multiply chunk i, the loaders
-// write chunk i+1 and have chunk i+2's loads in flight.
+// Loader waves (the last kLoaders waves) fill these.  The halo always comes
+// from the NCHW input as given: 16-byte loads (8 pixels of one channel; 8
+// channels per lane), transposed in registers into 8 pixel vectors.  The
+// filters come one of two ways:
+//
+//   * per call (PK = false), from the KCRS tensor as given: nine 16-byte
+//     loads per (filter, 8 channels) -- the 72 consecutive values of 8
+//     channels x 9 taps -- regrouped in registers into nine tap vectors.  No
+//     packing kernel runs before the convolution.  All four loader waves do
+//     both jobs; two LDS stages alternate, and while the compute waves
+//     multiply chunk i the loaders write chunk i+1 and have chunk i+2's
+//     loads in flight;
+//   * prepacked (PK = true), from a package that k3_pack builds once per
+//     filter tensor, each (chunk, channel tile) filter tile stored in its
+//     LDS order: two loader waves copy it by LDS DMA with no register
+//     traffic while the other two transpose the halo, over three LDS stages
+//     (the DMA of chunk i+2 goes out while chunk i is multiplied).
 //
 // Compute waves form a WP x WK grid; each holds MB x NB blocks of 32 x 32
 // accumulators (32 MB pixels x 32 NB channels), so that each operand read
@@ -59,8 +68,9 @@ struct K3Args {
   uint32_t x_bytes, w_bytes;
   int N, C, H, W, K, P, Q;
   int sh, ph, pw;      // stride (both axes), padding
-  int Hp;              // virtual rows per image: (P - 1) * sh + 3
-  int NPQ;
+  int Hp;              // virtual rows per image (at least (P - 1) * sh + 3)
+  int E, PE;           // enumerated columns per output row (E >= Q), pixels per image (P * E)
+  int NPQ;             // enumerated pixels of the launch: N * P * E
   int ptiles, ktiles;
   int nch, chunks_per_split;
   int VR;              // halo rows staged per chunk
@@ -92,9 +102,47 @@ __device__ __forceinline__ int k3_swz(int pos) {
 // 64 to 512 bytes instead of 32 separate 16-byte pieces.  A run that crosses
 // an image boundary or passes the last pixel is stored element by element
 // (runs cross at most one boundary: P*Q >= 8).
+// Stores the first n (1..7) bf16 values of an 8-value run: 8, 4 and 2-byte
+// pieces.
+__device__ __forceinline__ void k3_store_head(uint16_t* p, uint32_t d0, uint32_t d1, uint32_t d2, uint32_t d3,
+                                              int n) {
+  const bool b4 = n >= 4;
+  if (b4) {
+    const uint2 v = make_uint2(d0, d1);
+    __builtin_memcpy(p, &v, 8);
+  }
+  const int t2 = b4 ? 4 : 0;
+  const uint32_t w2 = b4 ? d2 : d0;
+  const bool b2 = n - t2 >= 2;
+  if (b2) __builtin_memcpy(p + t2, &w2, 4);
+  const int t1 = t2 + (b2 ? 2 : 0);
+  const uint32_t w1 = t1 == 0 ? d0 : t1 == 2 ? d1 : t1 == 4 ? d2 : d3;
+  if (n - t1 >= 1) p[t1] = static_cast<uint16_t>(w1);
+}
+
+// Output run of the 8 enumerated pixels col0 + px .. +7 (channel row0).
+// With E == Q the enumeration is the output order itself (runs may cross
+// rows and one image boundary); with E > Q (E a multiple of 8) a run lies in
+// one output row, and its pixels at columns >= Q are padding, not stored.
+struct K3Map {
+  int E, PE, Q, NPQ;
+};
+__device__ __forceinline__ Run128t k3_run(const EpiArgs& e, const K3Map& m, int row0, int col0, int px) {
+  if (m.E == m.Q) return run128t(e, row0, col0, 0, px);
+  Run128t r;
+  const int j = col0 + px;
+  const int n = j / m.PE, rem = j - n * m.PE;
+  const int p = rem / m.E, q = rem - p * m.E;
+  r.nvalid = (j < m.NPQ && q < m.Q) ? min(8, m.Q - q) : 0;
+  r.wrap = 8;
+  r.full = r.nvalid == 8;
+  r.o = (static_cast<int64_t>(n) * e.K + row0) * e.PQ + p * m.Q + q;
+  return r;
+}
+
 template <int MB, int NB>
-__device__ __forceinline__ void k3_epilogue(const f32x16_t (&acc)[MB][NB], char* stage, const EpiArgs& e, int kb0,
-                                            int col0, int split) {
+__device__ __forceinline__ void k3_epilogue(const f32x16_t (&acc)[MB][NB], char* stage, const EpiArgs& e,
+                                            const K3Map& m, int kb0, int col0, int split) {
   const int lane = threadIdx.x & 63;
   const int l32 = lane & 31, h = lane >> 5;
   const int PQ = e.PQ;
@@ -106,7 +154,7 @@ __device__ __forceinline__ void k3_epilogue(const f32x16_t (&acc)[MB][NB], char*
     const uint16_t* bias = reinterpret_cast<const uint16_t*>(e.b);
     uint16_t* y = reinterpret_cast<uint16_t*>(e.y);
     const int rrow = lane / U, u = lane % U;
-    const Run128t r = run128t(e, kb0, col0, 0, u * 8);
+    const Run128t r = k3_run(e, m, kb0, col0, u * 8);
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const int kb = kb0 + 32 * nb;
@@ -183,6 +231,8 @@ __device__ __forceinline__ void k3_epilogue(const f32x16_t (&acc)[MB][NB], char*
         const int64_t o = ob + static_cast<int64_t>(row) * PQ;
         if (r.full) {
           __builtin_memcpy(y + o, &d[it], 16);
+        } else if (r.wrap >= 8) {
+          k3_store_head(y + o, d[it].x, d[it].y, d[it].z, d[it].w, r.nvalid);
         } else {
           const uint32_t wd[4] = {d[it].x, d[it].y, d[it].z, d[it].w};
 #pragma unroll
@@ -203,7 +253,7 @@ __device__ __forceinline__ void k3_epilogue(const f32x16_t (&acc)[MB][NB], char*
   constexpr int PASSES = 32 / RPI;
   float* part = e.partial + static_cast<int64_t>(split) * e.slab;
   const int rrow = lane / LPR, c = lane % LPR;
-  const Run128t r = run128t(e, kb0, col0, 0, c * 8);
+  const Run128t r = k3_run(e, m, kb0, col0, c * 8);
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     const int kb = kb0 + 32 * nb;
@@ -234,6 +284,20 @@ __device__ __forceinline__ void k3_epilogue(const f32x16_t (&acc)[MB][NB], char*
       if (r.full) {
         __builtin_memcpy(part + o, &lo[it], 16);
         __builtin_memcpy(part + o + 4, &hi[it], 16);
+      } else if (r.wrap >= 8) {
+        // the first nvalid floats: 4 (16 bytes), then 2, then 1
+        const int nv = r.nvalid;
+        const bool b4 = nv >= 4;
+        if (b4) __builtin_memcpy(part + o, &lo[it], 16);
+        const float qx = b4 ? hi[it].x : lo[it].x, qy = b4 ? hi[it].y : lo[it].y;
+        const float qz = b4 ? hi[it].z : lo[it].z;
+        const int t2 = b4 ? 4 : 0;
+        const bool b2 = nv - t2 >= 2;
+        if (b2) {
+          const float2 q2 = make_float2(qx, qy);
+          __builtin_memcpy(part + o + t2, &q2, 8);
+        }
+        if (nv - t2 - (b2 ? 2 : 0) >= 1) part[o + t2 + (b2 ? 2 : 0)] = b2 ? qz : qx;
       } else {
         const float vals[8] = {lo[it].x, lo[it].y, lo[it].z, lo[it].w, hi[it].x, hi[it].y, hi[it].z, hi[it].w};
 #pragma unroll
@@ -274,10 +338,9 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
   const int ch_begin = split * a.chunks_per_split;
   const int nchunks = min(a.nch, ch_begin + a.chunks_per_split) - ch_begin;
   const int npairs = (nchunks + 1) >> 1;  // barrier steps run in pairs
-  const int PQ = a.P * a.Q;
   auto vrow = [&](int j) {
-    const int n = j / PQ, pq = j - n * PQ;
-    return n * a.Hp + (pq / a.Q) * a.sh;
+    const int n = j / a.PE, pq = j - n * a.PE;
+    return n * a.Hp + (pq / a.E) * a.sh;
   };
   const int v_lo = vrow(j0);
 
@@ -305,11 +368,13 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
       hcol[t] = 0;
       hg[t] = 0;
       if (lt < HL && it < a.halo_items) {
-        // Rows fastest: consecutive lanes write slots a halo row apart,
-        // not UPX slots apart (which would put them all in one bank group).
-        const int per_g = a.VR * a.NG;
-        const int g = it / per_g, rem = it - g * per_g;
-        const int gc = rem / a.VR, vr = rem - gc * a.VR;
+        // Channel groups fastest, then column windows, then rows: the UP
+        // lanes of one window write distinct units of the same slots, and
+        // windows and rows spread the rest over the banks (the bank groups
+        // of 16 consecutive slots are taken by the compute waves' reads, so
+        // the writes' pattern can only be chosen by the item order).
+        const int g = it % UP, rest = it / UP;
+        const int vr = rest / a.NG, gc = rest - vr * a.NG;
         const int ws = min(gc * UPX, a.W - UPX);
         const int v = v_lo + vr;
         const int n = v / a.Hp, h = v - n * a.Hp - a.ph;
@@ -585,8 +650,8 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
     const int j = min(j0 + (wp * MB + mb) * 32 + l32, jl);
-    const int pq = j - (j / PQ) * PQ;
-    const int q = pq - (pq / a.Q) * a.Q;
+    const int pq = j - (j / a.PE) * a.PE;
+    const int q = pq - (pq / a.E) * a.E;
     apos[mb] = (vrow(j) - v_lo) * a.RS + q;
   }
   // Tap offsets in slots: row r, column s (stride 2: parity plane s & 1, s >> 1 further).
@@ -673,7 +738,8 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
   // After B of the last chunk no wave reads the stages again: each compute
   // wave stages its output in its own region at the start of LDS.
   char* stage = lds + wave * (MB * 32 * 32 * 4);
-  k3_epilogue<MB, NB>(acc, stage, a.e, k0 + wk * NB * 32, j0 + wp * MB * 32, split);
+  const K3Map m{a.E, a.PE, a.Q, a.NPQ};
+  k3_epilogue<MB, NB>(acc, stage, a.e, m, k0 + wk * NB * 32, j0 + wp * MB * 32, split);
 }
 
 // ---------------------------------------------------------------------------
@@ -700,6 +766,8 @@ constexpr int kNumK3Configs = sizeof(kK3Configs) / sizeof(kK3Configs[0]);
 struct K3Plan {
   int cfg;
   bool pk;   // filters from the tile-ordered package by DMA (three LDS stages)
+  bool aligned;  // pixel layout with bank-aligned rows (E >= Q), else E = Q
+  int nsplit;    // ways the channel reduction is split
   bool s2;
   int upx;
   int64_t images_per_launch;
@@ -707,13 +775,14 @@ struct K3Plan {
   K3Args a;
 };
 
-// Largest halo span (virtual rows) of any TP-pixel tile of N images.
-int k3_halo_rows(const Shape& s, int64_t N, int Hp, int TP) {
-  const int64_t PQ = s.P * s.Q, NPQ = N * PQ;
+// Largest halo span (virtual rows) of any TP-pixel tile of N images
+// (pixels enumerated with E columns per output row).
+int k3_halo_rows(const Shape& s, int64_t N, int Hp, int TP, int E) {
+  const int64_t PQ = s.P * E, NPQ = N * PQ;
   const int64_t tiles = (NPQ + TP - 1) / TP;
   auto vrow = [&](int64_t j) {
     const int64_t n = j / PQ, pq = j % PQ;
-    return n * Hp + (pq / s.Q) * s.sh;
+    return n * Hp + (pq / E) * s.sh;
   };
   // A tile's span depends only on where it starts within an image, which
   // repeats every PQ / gcd(TP, PQ) tiles.
@@ -741,11 +810,44 @@ bool k3_shape_ok(const Shape& s) {
   return true;
 }
 
-bool make_k3_plan_cfg(const Shape& s, int cfg, K3Plan& pl, int64_t N1, bool pk = false) {
+// Pixel layouts.  The compute waves read the halo in 16-lane groups of 16
+// consecutive tile pixels; the reads are free of bank conflicts when those
+// pixels' slots are 16 consecutive slots (mod 16).  Along an output row they
+// are; across a row end the slot jumps by sh * RS - Q, across an image by
+// Hp * RS - P * Q.  The aligned layout pads each output row to E columns (a
+// multiple of 8; the padding pixels are computed and not stored) and picks
+// RS and Hp so that both jumps are 0 mod 16.  At stride 1 consecutive halo
+// rows share their padding columns (the right padding of row v is the left
+// padding of row v + 1: both are zeros), which keeps RS small.  The plain
+// layout (E = Q) is used where the aligned one does not fit.
+void k3_layout(const Shape& s, bool aligned, int& E, int& RS, int& PS, int& Hp) {
+  // Padded columns read: q * sh + tap column < (Q - 1) * sh + 3; written: [pw, W + pw).
+  const int cols = (int)std::max<int64_t>((s.Q - 1) * s.sh + 3, s.W + s.pw);
+  const int hmin = (int)((s.P - 1) * s.sh + 3);
+  PS = s.sh == 2 ? (cols + 1) / 2 : 0;
+  if (!aligned) {
+    E = (int)s.Q;
+    RS = s.sh == 2 ? 2 * PS : cols;
+    Hp = hmin;
+    return;
+  }
+  E = (int)((s.Q + 7) / 8 * 8);
+  RS = s.sh == 2 ? 2 * PS : (int)std::max<int64_t>(s.W + s.pw, (s.Q - 1) + 3 - s.pw);
+  while (((s.sh * RS - E) % 16 + 16) % 16 != 0) ++RS;
+  Hp = hmin;
+  for (int h = hmin; h < hmin + 16; ++h)
+    if (((h * RS - (int)s.P * E) % 16 + 16) % 16 == 0) {
+      Hp = h;
+      break;
+    }
+}
+
+bool make_k3_plan_cfg(const Shape& s, int cfg, K3Plan& pl, int64_t N1, bool pk, bool aligned, int nsplit) {
   const K3Config c = kK3Configs[cfg];
   if (s.C % c.CH != 0) return false;
   pl.cfg = cfg;
   pl.pk = pk;
+  pl.aligned = aligned;
   pl.s2 = s.sh == 2;
   pl.upx = s.W >= 8 ? 8 : 4;
   pl.images_per_launch = N1;
@@ -753,25 +855,20 @@ bool make_k3_plan_cfg(const Shape& s, int cfg, K3Plan& pl, int64_t N1, bool pk =
   a.N = (int)N1; a.C = (int)s.C; a.H = (int)s.H; a.W = (int)s.W; a.K = (int)s.K;
   a.P = (int)s.P; a.Q = (int)s.Q;
   a.sh = s.sh; a.ph = s.ph; a.pw = s.pw;
-  a.Hp = (int)((s.P - 1) * s.sh + 3);
-  a.NPQ = (int)(N1 * s.P * s.Q);
+  k3_layout(s, aligned, a.E, a.RS, a.PS, a.Hp);
+  a.PE = (int)(s.P * a.E);
+  if (N1 * a.PE >= ((int64_t)1 << 31)) return false;
+  a.NPQ = (int)(N1 * a.PE);
   a.ptiles = (a.NPQ + c.tp() - 1) / c.tp();
   a.ktiles = (int)((s.K + c.tk() - 1) / c.tk());
   a.nch = (int)(s.C / c.CH);
-  a.VR = k3_halo_rows(s, N1, a.Hp, c.tp());
-  // Padded columns read: q * sh + tap column < (Q - 1) * sh + 3; written: [pw, W + pw).
-  const int cols = (int)std::max<int64_t>((s.Q - 1) * s.sh + 3, s.W + s.pw);
-  if (pl.s2) {
-    a.PS = (cols + 1) / 2;
-    a.RS = 2 * a.PS;
-  } else {
-    a.PS = 0;
-    a.RS = cols;
-  }
+  a.VR = k3_halo_rows(s, N1, a.Hp, c.tp(), a.E);
   a.NG = (int)((s.W + pl.upx - 1) / pl.upx);
   a.halo_items = a.VR * a.NG * (c.CH / 8);
   if (a.halo_items > kHSMax * (pk ? 128 : 256)) return false;
-  a.halo_bytes = (int)(((size_t)a.VR * a.RS * c.CH * 2 + 255) / 256 * 256);
+  // 16 spare zero slots after the last row: taps of the last row's final
+  // pixels (and of padding pixels) read past it.
+  a.halo_bytes = (int)((((size_t)a.VR * a.RS + 16) * c.CH * 2 + 255) / 256 * 256);
   const size_t filt = (size_t)kK3Taps * c.tk() * c.CH * 2;
   a.stage_bytes = (int)(a.halo_bytes + filt);
   pl.lds = (size_t)(pk ? 3 : 2) * a.stage_bytes;
@@ -779,8 +876,13 @@ bool make_k3_plan_cfg(const Shape& s, int cfg, K3Plan& pl, int64_t N1, bool pk =
   const size_t staging = (size_t)c.nc() * c.MB * 32 * 32 * 4;
   if (pl.lds < staging) pl.lds = staging;
   if (pl.lds > kLdsLimit) return false;
-  const int64_t tiles = (int64_t)a.ptiles * a.ktiles;
-  split_chunks(tiles, a.nch, &a.e.splits, &a.chunks_per_split);
+  // The channel chunks are split nsplit ways (fewer when the chunks do not
+  // go round).
+  if (nsplit < 1 || nsplit > a.nch) return false;
+  a.chunks_per_split = (a.nch + nsplit - 1) / nsplit;
+  a.e.splits = (a.nch + a.chunks_per_split - 1) / a.chunks_per_split;
+  if (a.e.splits != nsplit) return false;
+  pl.nsplit = nsplit;
   a.e.K = (int)s.K; a.e.Kg = (int)s.K; a.e.relu = s.relu ? 1 : 0; a.e.PQ = (int)(s.P * s.Q);
   a.e.span = a.e.PQ;
   a.e.NPQ = a.NPQ;
@@ -789,21 +891,42 @@ bool make_k3_plan_cfg(const Shape& s, int cfg, K3Plan& pl, int64_t N1, bool pk =
   return true;
 }
 
-// Estimated time of a plan, in microseconds: rounds of workgroups over the
-// CUs times the MFMAs of one compute wave (32 cycles each at about 2.1 GHz)
-// divided by the tile's measured efficiency (the loaders, not the MFMAs,
-// bound these kernels: smaller tiles reload the filters for fewer pixels),
-// plus the first chunk's latency, plus, when the channels are split, the
-// fp32 partial sums written and read back and the reduction's launch.
-double k3_cost(const K3Plan& pl) {
-  static constexpr double kEff[kNumK3Configs] = {0.45, 0.40, 0.30, 0.20};
+// Estimated time of a plan, in microseconds:
+//
+//   a + rounds * chunks * max(b[tile] * MFMAs per chunk, c * halo items per
+//   loader lane * CH / 16 + d * filter bytes regrouped per chunk / 1024)
+//     + g * rounds + (split: e + f * splits * N*K*P*Q * 8 bytes / 1e6)
+//
+// rounds = workgroups over the 256 CUs, chunks per workgroup, MFMAs of one
+// compute wave.  A chunk is bound either by the compute waves (their MFMAs
+// and operand reads, per tile shape) or by the loader waves (halo rows
+// transposed per lane, filters regrouped); a and g are the launch and the
+// per-round pipeline fill and drain; split partial sums cost their fp32
+// round trip and the reduction kernel.  The constants are least-squares fits
+// (relative error) to measured times of the bf16 3x3 layers of ResNet-50 at
+// batch 32 over every tile shape and split of 1, 2 and 4; one set for the
+// per-call kernel (filters regrouped by the loaders), one for the package
+// kernel (filters by DMA).  Median error about 6% (per call) and 12%
+// (package).
+struct K3CostParams {
+  double a, b[kNumK3Configs], c, d, e, f, g;
+};
+constexpr K3CostParams kK3CostCall = {7.18, {0.0180, 0.0252, 0.0307, 0.0534}, 0.500, 0.0, 2.99, 0.168, 4.85};
+constexpr K3CostParams kK3CostPack = {4.90, {0.0180, 0.0278, 0.0175, 0.0094}, 0.315, 0.0, 0.90, 0.204, 4.39};
+
+double k3_cost(const K3Plan& pl, const Shape& s) {
+  const K3CostParams& m = pl.pk ? kK3CostPack : kK3CostCall;
   const K3Config c = kK3Configs[pl.cfg];
   const K3Args& a = pl.a;
   const int64_t wgs = (int64_t)a.ptiles * a.ktiles * a.e.splits;
   const double rounds = (double)((wgs + kCUs - 1) / kCUs);
-  const double mfma = (double)a.chunks_per_split * kK3Taps * (c.CH / 16) * c.MB * c.NB;
-  double t = rounds * mfma * (32.0 / 2100.0) / kEff[pl.cfg] + 3.0;
-  if (a.e.splits > 1) t += 3.0 + (double)a.e.splits * a.NPQ * a.K * 8.0 / 3.0e6;
+  const double mfma = (double)kK3Taps * (c.CH / 16) * c.MB * c.NB;
+  const int HL = pl.pk ? 128 : 256;
+  const double hs = (double)((a.halo_items + HL - 1) / HL);
+  const double filt = pl.pk ? 0.0 : (double)c.tk() * c.CH / 1024.0;
+  const double chunk = std::max(m.b[pl.cfg] * mfma, m.c * hs * c.CH / 16.0 + m.d * filt);
+  double t = m.a + rounds * a.chunks_per_split * chunk + m.g * rounds;
+  if (a.e.splits > 1) t += m.e + m.f * a.e.splits * (double)(a.N * s.P * s.Q) * s.K * 8.0 / 1e6;
   return t;
 }
 
@@ -817,30 +940,51 @@ bool make_k3_plan(const Shape& s, K3Plan& pl, int64_t N1 = -1, bool prepacked = 
     if (N1 < 1) N1 = 1;
   }
   if ((int64_t)s.K * s.C * 9 * 2 >= ((int64_t)1 << 31)) return false;
+  // Every tile shape and split of 1, 2, 4 or 8, in the aligned layout where
+  // it fits (else the plain one), scored by the per-call estimate plus the
+  // package kernel's estimate (or the per-call one again where the package
+  // kernel does not fit): both calls of a layer run the same tiles and split,
+  // so their results are the same bits, and the choice serves both.  The
+  // remainder launch (N not a multiple of the images per launch) must fit the
+  // same choice.
+  const int64_t r = s.N % N1;
+  auto build = [&](int cfg, bool pk, bool al, int S, K3Plan& out) {
+    K3Plan rest;
+    return make_k3_plan_cfg(s, cfg, out, N1, pk, al, S) && (r == 0 || make_k3_plan_cfg(s, cfg, rest, r, pk, al, S));
+  };
   bool found = false;
   double best = 0;
+  K3Plan best_call, best_pack;
+  bool best_has_pack = false;
   for (int cfg = 0; cfg < kNumK3Configs; ++cfg) {
-    K3Plan cand;
-    if (!make_k3_plan_cfg(s, cfg, cand, N1)) continue;
-    const double t = k3_cost(cand);
-    if (!found || t < best) {
-      best = t;
-      pl = cand;
-      found = true;
+    for (int S = 1; S <= 8; S *= 2) {
+      K3Plan call;
+      bool al = true;
+      if (!build(cfg, false, true, S, call)) {
+        al = false;
+        if (!build(cfg, false, false, S, call)) continue;
+      }
+      // The package kernel: not for the 512-pixel tile, where the register
+      // path measured as fast.
+      K3Plan pack;
+      const bool has_pack = cfg != 0 && build(cfg, true, al, S, pack);
+      const double t = k3_cost(call, s) + (has_pack ? k3_cost(pack, s) : k3_cost(call, s));
+      if (!found || t < best) {
+        best = t;
+        best_call = call;
+        best_pack = pack;
+        best_has_pack = has_pack;
+        found = true;
+      }
     }
   }
   if (!found) return false;
   // Prepacked filters (built once, outside the call) go in by DMA from the
-  // package wherever its three stages fit, in every launch of the layer
-  // (the package's layout follows the tile shape); not for the 512-pixel
-  // tile, where the register path measured as fast.  A per-call package
-  // would cost its own launch, which measured more than the DMA saves, so
-  // conv2d() regroups the filters in the kernel.
-  K3Plan with_pk, rest;
-  const int64_t r = s.N % N1;
-  if (prepacked && pl.cfg != 0 && make_k3_plan_cfg(s, pl.cfg, with_pk, N1, true) &&
-      (r == 0 || make_k3_plan_cfg(s, pl.cfg, rest, r, true)))
-    pl = with_pk;
+  // package in every launch of the layer (the package's layout follows the
+  // tile shape).  A per-call package would cost its own launch, which
+  // measured more than the DMA saves, so conv2d() regroups the filters in
+  // the kernel.
+  pl = prepacked && best_has_pack ? best_pack : best_call;
   return true;
 }
 
@@ -851,7 +995,7 @@ bool k3_plan_for_launch(const Shape& s, const K3Plan& pl, int64_t cnt, K3Plan& c
     cur = pl;
     return true;
   }
-  return make_k3_plan_cfg(s, pl.cfg, cur, cnt, pl.pk);
+  return make_k3_plan_cfg(s, pl.cfg, cur, cnt, pl.pk, pl.aligned, pl.nsplit);
 }
 
 // Filter package: for chunk cg (CH channels) and channel tile kt, the LDS
@@ -1023,12 +1167,13 @@ std::string k3_describe(const Shape& s, bool prepacked) {
   char buf[512];
   snprintf(buf, sizeof(buf),
            "implicit_gemm kernels=%sconv3x3_kernel<%d,%d,%d,%d,%d,%d,%d,%d,%d>%s tile=%dx%d grid=%dx%d chunk=%d "
-           "halo_rows=%d halo_items=%d lds=%zu images_per_launch=%lld (loader waves: halo rows transposed to "
-           "pixel-major LDS, %s; compute waves: MFMA %dx%d per wave)",
+           "halo_rows=%d halo_items=%d row_slots=%d cols=%d lds=%zu images_per_launch=%lld (loader waves: halo "
+           "rows transposed to pixel-major LDS, %s; compute waves: MFMA %dx%d per wave)",
            pl.pk ? "k3_pack_kernel;" : "", c.CH, c.WP, c.WK, c.MB, c.NB, pl.s2 ? 1 : 0, pl.upx,
            pl.a.halo_items > (pl.pk ? 128 : 256) ? 2 : 1, pl.pk ? 1 : 0,
            pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "",
-           c.tp(), c.tk(), pl.a.ptiles * pl.a.ktiles, pl.a.e.splits, c.CH, pl.a.VR, pl.a.halo_items, pl.lds,
+           c.tp(), c.tk(), pl.a.ptiles * pl.a.ktiles, pl.a.e.splits, c.CH, pl.a.VR, pl.a.halo_items, pl.a.RS,
+           pl.a.E, pl.lds,
            (long long)pl.images_per_launch,
            pl.pk ? "filter tiles copied by DMA from the package, three LDS stages"
                  : "KCRS filters regrouped to tap-major LDS, two LDS stages",

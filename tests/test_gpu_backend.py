@@ -125,6 +125,8 @@ RESIDUAL = [
     ("bf16", 32, 64, 56, 56, 64, 3, 1, 1, True, "conv3x3_kernel<16,4,1,4,2,0,8,1,0>"),
     ("bf16", 32, 128, 56, 56, 128, 3, 2, 1, True, "conv3x3_kernel<16,2,2,2,2,1,8,1,0>"),
     ("bf16", 2, 128, 112, 112, 64, 3, 1, 1, False, "conv3x3_kernel<32,2,2,2,1,0,8,1,0>"),
+    ("bf16", 2, 256, 28, 28, 256, 3, 2, 1, True, "conv3x3_kernel<32,2,2,1,1,1,8,1,0>;splitk_reduce_kernel"),
+    ("bf16", 4, 256, 14, 14, 256, 3, 1, 1, False, "conv3x3_kernel<32,2,2,1,1,0,8,1,1>;splitk_reduce_kernel"),
     ("bf16", 7, 48, 2, 2, 64, 3, 1, 1, True, "implicit_gemm_kernel<bf16,64,2,9>;splitk_reduce_kernel"),
     ("bf16", 2, 3, 32, 32, 16, 3, 1, 1, False, "implicit_gemm_kernel<bf16,64,1,9>"),
     ("bf16", 2, 3, 64, 64, 64, 7, 2, 3, True, "implicit_rows_kernel"),

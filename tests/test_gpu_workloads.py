@@ -10,7 +10,8 @@
   planes of 8 of its images (the first, the last and six seeded ones),
   which the GPU computes within the full-batch launch;
 * reruns of the full-batch implicit GEMM calls are bit-identical (the split-K
-  reduction sums the partials in a fixed order)."""
+  reduction sums the partials in a fixed order), and so are the same calls
+  with a filter package built beforehand."""
 import numpy as np
 import pytest
 import torch
@@ -98,7 +99,14 @@ def test_full_batch_full_outputs(wl, li):
         if algo == "implicit_gemm":
             y2 = cs.conv2d(x, w, b, L.stride, L.pad, L.dilation, L.groups, algo=algo, relu=L.relu)
             assert torch.equal(y, y2), "%s %s: rerun differs" % (wl, L.name)
-            del y2
+            # The prepacked call (another filter path in some kernels, the
+            # same reduction order) gives the same bits.
+            pk = cs.pack_filters(w, tuple(x.shape), L.stride, L.pad, L.dilation, L.groups, algo,
+                                 bias=b is not None, relu=L.relu)
+            y2 = cs.conv2d_prepacked(x, pk, tuple(w.shape), b, L.stride, L.pad, L.dilation, L.groups,
+                                     algo=algo, relu=L.relu)
+            assert torch.equal(y, y2), "%s %s: prepacked call differs" % (wl, L.name)
+            del y2, pk
         del y, ys
     del x, w, b, xs, ref_dev
     torch.cuda.empty_cache()
