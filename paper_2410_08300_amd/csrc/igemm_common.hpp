@@ -29,6 +29,7 @@ struct EpiArgs {
   int splits;          // workgroups sharing one output tile along the channels
   int slab;            // floats per split of `partial` (N*K*P*Q rounded up to 4)
   int vec;             // store piece in elements (8, 4, 2 or 1; see store_tile)
+  uint32_t y_bytes = 0;  // bytes of y in this launch when below 2^31 (buffer stores), else 0
   // Residual added after the bias and before the ReLU (same layout and type
   // as y; NULL: none).  With bf16 the convolution's value is rounded to bf16
   // first, so y = round(relu(round(conv + b) + res)) -- the rounding steps
@@ -326,7 +327,7 @@ __device__ __forceinline__ Run128t run128t(const EpiArgs& e, int row0, int col0,
 // P*Q >= 8 or the tile index space pads planes to a multiple of 8.
 template <typename T>
 __device__ __forceinline__ void store_block128t(const f32x16_t (&acc)[1][4], float* stage_f, const EpiArgs& e,
-                                                int row0, int col0, int g, int split) {
+                                                int row0, int col0, int g, int split, bool bias_in_acc = false) {
   const int lane = threadIdx.x & 63;
   const int l32 = lane & 31, h = lane >> 5;
   const int PQ = e.PQ;
@@ -336,7 +337,8 @@ __device__ __forceinline__ void store_block128t(const f32x16_t (&acc)[1][4], flo
   auto run_at = [&](int px) { return run128t(e, row0, col0, g, px); };
 
   if (e.splits <= 1) {
-    const T* bias = reinterpret_cast<const T*>(e.b);
+    // (bias_in_acc: the accumulators started from the bias.)
+    const T* bias = bias_in_acc ? nullptr : reinterpret_cast<const T*>(e.b);
     const int i_own = row0 + l32;
     const float bv = (bias && i_own < e.Kg) ? elem<T>::load(bias + g * e.Kg + i_own) : 0.f;
     // Channel l32, pixels px0 .. px0 + 3 (8 bytes of T = bf16; fp32 goes
@@ -382,6 +384,24 @@ __device__ __forceinline__ void store_block128t(const f32x16_t (&acc)[1][4], flo
       d[it] = *reinterpret_cast<const uint4*>(stage + row * 256 + ((u ^ (row & 15)) << 4));
     }
     T* y = reinterpret_cast<T*>(e.y);
+    // Common case: no residual, every lane's run is whole and the launch's
+    // output fits a buffer resource.  Then each row is one buffer store
+    // whose scalar offset steps by four channel rows, and rows past Kg get
+    // an offset past the buffer (the store is dropped): no per-row address
+    // arithmetic and no branches.
+    if (!e.res && e.y_bytes != 0 && __builtin_amdgcn_ballot_w64(!r.full) == 0) {
+      const __amdgpu_buffer_rsrc_t yr = make_rsrc(e.y, e.y_bytes);
+      const uint32_t vo = static_cast<uint32_t>((r.o + static_cast<int64_t>(rrow) * PQ) * 2);
+      const uint32_t step = static_cast<uint32_t>(4 * PQ * 2);
+      const int rows_left = e.Kg - row0 - rrow;  // rows of this lane below Kg: it < ceil(rows_left / 4)
+#pragma unroll
+      for (int it = 0; it < 8; ++it) {
+        const uint32_t v = 4 * it < rows_left ? vo : 0x80000000u;
+        __builtin_amdgcn_raw_buffer_store_b128(*reinterpret_cast<const u32x4_t*>(&d[it]), yr, v, step * it, 0);
+      }
+      __builtin_amdgcn_wave_barrier();
+      return;
+    }
     if (e.res) {  // uniform: residual add (and the ReLU after it), then the same stores
       // Whole runs: all eight rows are requested before any is used, so the
       // loads overlap (one memory round trip per tile, not one per row).

@@ -801,11 +801,26 @@ __global__ __launch_bounds__((4 + NL) * 64) void pointwise_dma_kernel(PwArgs a) 
     a_swz[mi] = (row >> 1) & 7;
   }
 
+  // Without a split the accumulators start from the bias of the lane's
+  // output channel (row kt * BM + 32 lw + l32 of the unit), so the epilogue
+  // does not add it; the next unit's bias is loaded while this one's
+  // epilogue runs.
+  const uint16_t* bias = a.e.splits == 1 ? reinterpret_cast<const uint16_t*>(a.e.b) : nullptr;
+  auto bias_of = [&](int u) -> float {
+    const int kt = (u / a.e.splits) % a.ktiles;
+    const int row = kt * BM + lw * 32 + l32;
+    return (bias && row < a.e.Kg) ? bf16_to_f32(bias[row]) : 0.f;
+  };
   f32x16_t acc[MI][NJ];
+  {
+    const float b0 = bias_of(u_first);
 #pragma unroll
-  for (int mi = 0; mi < MI; ++mi)
+    for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-    for (int nj = 0; nj < NJ; ++nj) acc[mi][nj] = zero16();
+      for (int nj = 0; nj < NJ; ++nj)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[mi][nj][v] = b0;
+  }
 
   int cu = u_first, cch = chunk_begin(u_first), cstage = 0;
   for (;;) {
@@ -838,12 +853,15 @@ __global__ __launch_bounds__((4 + NL) * 64) void pointwise_dma_kernel(PwArgs a) 
       // Tile done: each compute wave stages its part in its own region.
       const int tile = cu / a.e.splits;
       const int pt = tile / a.ktiles, kt = tile - pt * a.ktiles;
+      const float bn = cu + slots < u_end ? bias_of(cu + slots) : 0.f;
       store_block128t<bf16_t>(acc, reinterpret_cast<float*>(staging) + lw * 32 * 64, a.e, kt * BM + lw * 32, pt * BN,
-                              0, cu % a.e.splits);
+                              0, cu % a.e.splits, true);
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-        for (int nj = 0; nj < NJ; ++nj) acc[mi][nj] = zero16();
+        for (int nj = 0; nj < NJ; ++nj)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) acc[mi][nj][v] = bn;
       cu += slots;
       if (cu >= u_end) break;
       cch = chunk_begin(cu);
@@ -1255,6 +1273,8 @@ hipError_t pw_main_typed(const Shape& s, const void* x, const void* w, const voi
     a.e.b = b;
     a.e.partial = reinterpret_cast<float*>(ws + align256(cur.repack_bytes));
     a.e.vec = store_piece(s, a.e.y);
+    const int64_t y_bytes = cnt * out_elems * s.esize();
+    a.e.y_bytes = y_bytes < ((int64_t)1 << 31) ? (uint32_t)y_bytes : 0u;
     hipError_t e;
     if (cur.dma) {
       if (cur.repack) {
