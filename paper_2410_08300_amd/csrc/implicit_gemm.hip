@@ -736,10 +736,12 @@ __global__ __launch_bounds__((4 + NL) * 64) void pointwise_dma_kernel(PwArgs a) 
           __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, dst, 4, vo, xso, 0, 0);
       }
     };
-    // Fetch cursor (fu, fch).  All NS stages are filled up front; after that
-    // the stage freed at barrier B of item k-1 is refilled right after
-    // barrier A of item k, while the compute waves multiply item k, so the
-    // issue never delays the barrier.  `later` counts the items issued after
+    // Fetch cursor (fu, fch).  NS - 1 stages are filled up front and the
+    // last right after barrier A of the first item (the first item's data
+    // arrives a little sooner than behind a full queue); after that the
+    // stage freed at barrier B of item k-1 is refilled right after barrier A
+    // of item k, while the compute waves multiply item k, so the issue never
+    // delays the barrier.  `later` counts the items issued after
     // the one being waited for (this wave issues nothing else, so that is
     // the vmcnt to wait for).
     int fu = u_first, fch = chunk_begin(u_first), fstage = 0;
@@ -754,10 +756,9 @@ __global__ __launch_bounds__((4 + NL) * 64) void pointwise_dma_kernel(PwArgs a) 
       return true;
     };
     int later = -1;
-    for (int s = 0; s < NS; ++s)
+    for (int s = 0; s < NS - 1; ++s)
       if (fetch_next()) ++later;
     int cu = u_first, cch = chunk_begin(u_first);
-    bool first = true;
     for (;;) {
       static_for<NS>([&](auto m) {
         if (later == decltype(m)::value) CONVSEL_WAIT_VMCNT(decltype(m)::value * INS);
@@ -765,8 +766,7 @@ __global__ __launch_bounds__((4 + NL) * 64) void pointwise_dma_kernel(PwArgs a) 
       // Plain barriers: the wait above already covers the item's DMA, and an
       // LDS fence here would also wait for the later items still in flight.
       __builtin_amdgcn_s_barrier();  // A: item visible to the compute waves
-      if (!first && fetch_next()) ++later;  // refill the stage freed at the previous B
-      first = false;
+      if (fetch_next()) ++later;  // the last stage, then the one freed at the previous B
       __builtin_amdgcn_s_barrier();  // B: compute waves are done with this item's stage
       --later;                       // the next item to wait for is one further on
       if (++cch >= chunk_end(cu)) {
