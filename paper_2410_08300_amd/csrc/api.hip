@@ -541,7 +541,7 @@ conv_status_t conv2d_describe(const conv2d_desc_t* desc, conv_algo_t algo, char*
   std::string d;
   switch (algo) {
     case CONV_ALGO_DIRECT:
-      d = s.Cg == 1 ? "direct kernels=direct_depthwise_kernel" : "direct kernels=direct_tile_kernel";
+      d = direct_describe(s);
       break;
     case CONV_ALGO_IMPLICIT_GEMM:
       d = convsel::implicit_gemm_describe(s);

@@ -14,9 +14,20 @@
 //    depthwise layers).  A workgroup owns one image's rows of several output
 //    planes, stages the input rows once, and sums the R*S taps per output.
 //    These layers are bound by HBM traffic, not arithmetic.
+//  * direct_dw3_kernel<T, S>: depthwise 3x3 (one input channel per output
+//    channel), stride S = 1 or 2, dilation 1, padding 0 or 1, the shape of
+//    MobileNet-style networks.  Bound by HBM traffic: a workgroup stages a
+//    band of input rows of one or several whole planes in LDS with 16-byte
+//    loads (the rows a band reads are contiguous in NCHW), then each thread
+//    computes strips of 4 consecutive outputs of a row from LDS and stores
+//    them as one vector.  Planes are independent, so the grid is
+//    (row bands) x (groups of planes) with no halo exchange.
 //  * direct_naive_kernel: one thread per output reading global memory, used
 //    only when a halo tile would not fit in LDS (very large dilated filters).
+#include <string>
+
 #include "common.hpp"
+#include "igemm_common.hpp"
 #include "kernels.hpp"
 
 namespace convsel {
@@ -173,6 +184,150 @@ __global__ __launch_bounds__(256) void direct_depthwise_kernel(DirectArgs a) {
   }
 }
 
+constexpr int kDwLoads = 4;  // chunk loads in flight per thread (depthwise staging)
+
+struct Dw3Args {
+  const void* x;
+  const void* w;
+  const void* b;
+  void* y;
+  uint32_t x_bytes;
+  int NC, C, H, W, P, Q, ph, pw, relu;
+  int TB, PB;        // output rows per band, planes per workgroup
+  int HB, LP;        // staged rows per plane (for a full band), LDS floats per staged row
+};
+
+// LDS: [PB planes][HB rows][LP floats] of input, input column x at x + 4
+// (LP a multiple of 4, so that a row's 16-byte-aligned chunks stay aligned;
+// columns 0-3 and those past W + 3 stay zero, as do rows outside the image),
+// then the PB planes' 9 taps.
+constexpr int kDwCol0 = 4;
+
+template <typename T, int S>
+__global__ __launch_bounds__(256) void direct_dw3_kernel(Dw3Args a) {
+  extern __shared__ __align__(16) float smem[];
+  constexpr int VE = elem<T>::per16;  // elements per 16-byte load
+  const int p0 = blockIdx.x * a.TB;
+  const int tb = min(a.TB, a.P - p0);
+  const int plane0 = blockIdx.y * a.PB;
+  const int pb = min(a.PB, a.NC - plane0);
+  const int ih0 = p0 * S - a.ph;
+  const int hb = (tb - 1) * S + 3;  // rows this band reads
+  const int per_plane = a.HB * a.LP;
+  float* ws = smem + a.PB * per_plane;
+  const int tid = threadIdx.x;
+
+  for (int i = tid; i < pb * per_plane / 4; i += 256)
+    reinterpret_cast<float4*>(smem)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int i = tid; i < pb * 9; i += 256) {
+    const int c = (plane0 + i / 9) % a.C;
+    ws[i] = elem<T>::load(reinterpret_cast<const T*>(a.w) + c * 9 + i % 9);
+  }
+  __syncthreads();
+
+  // The rows of the band inside the image are one contiguous span per
+  // plane, read in aligned 16-byte chunks (a chunk at either end may hold
+  // elements of the neighbouring rows or planes, which are not written;
+  // reads past the tensor return zeros through the buffer range).  All the
+  // block's planes' chunks form one loop (at most cmax per plane), and a
+  // thread issues kDwLoads loads before it consumes any.  When W is a
+  // multiple of the chunk, every chunk lies inside one row and lands as
+  // 16-byte LDS writes.
+  const int rlo = max(ih0, 0), rhi = min(ih0 + hb, a.H);
+  if (rhi > rlo) {
+    const __amdgpu_buffer_rsrc_t xr = igemm::make_rsrc(a.x, a.x_bytes);
+    const int span = (rhi - rlo) * a.W;
+    const int cmax = (span + 2 * VE - 2) / VE;
+    const int total = pb * cmax;
+    const bool rowwise = a.W % VE == 0;
+    for (int base = 0; base < total; base += 256 * kDwLoads) {
+      igemm::u32x4_t v[kDwLoads];
+      int64_t c0s[kDwLoads];
+#pragma unroll
+      for (int k = 0; k < kDwLoads; ++k) {
+        const int idx = base + k * 256 + tid;
+        const int pi = idx / cmax, t = idx - pi * cmax;
+        const int64_t g0 = (static_cast<int64_t>(plane0 + pi) * a.H + rlo) * a.W;
+        c0s[k] = (g0 & ~static_cast<int64_t>(VE - 1)) + static_cast<int64_t>(t) * VE;
+        // chunks past the block's planes read past the buffer (zeros, unused)
+        const uint32_t off = idx < total ? static_cast<uint32_t>(c0s[k] * sizeof(T)) : a.x_bytes;
+        v[k] = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0);
+      }
+#pragma unroll
+      for (int k = 0; k < kDwLoads; ++k) {
+        const int idx = base + k * 256 + tid;
+        if (idx >= total) continue;
+        const int pi = idx / cmax;
+        const int64_t g0 = (static_cast<int64_t>(plane0 + pi) * a.H + rlo) * a.W;
+        const int rel = static_cast<int>(c0s[k] - g0);  // span element at the chunk's first lane element
+        if (rel >= span) continue;
+        float* dst = smem + pi * per_plane + (rlo - ih0) * a.LP + kDwCol0;
+        float f[VE];
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          if constexpr (sizeof(T) == 4) f[e] = __uint_as_float(v[k][e]);
+          else f[e] = __uint_as_float((v[k][e >> 1] >> (16 * (e & 1))) << 16);
+        }
+        if (rowwise) {
+          const int row = rel / a.W, col = rel - row * a.W;
+#pragma unroll
+          for (int e = 0; e < VE; e += 4)
+            *reinterpret_cast<float4*>(dst + row * a.LP + col + e) = make_float4(f[e], f[e + 1], f[e + 2], f[e + 3]);
+        } else {
+          int row = rel >= 0 ? rel / a.W : -1;
+          int col = rel - row * a.W;
+#pragma unroll
+          for (int e = 0; e < VE; ++e) {
+            if (rel + e >= 0 && rel + e < span) dst[row * a.LP + col] = f[e];
+            if (++col == a.W) {
+              col = 0;
+              ++row;
+            }
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // Work items: 4 output rows (a vertical strip) of one column; consecutive
+  // threads take consecutive columns, so that LDS reads and global stores
+  // of a wave are contiguous.  A strip reads 4 S + 2 rows of 3 columns.
+  constexpr int NR = 3 * S + 3;
+  const int rg = (tb + 3) / 4;
+  const int items = pb * rg * a.Q;
+  const T* bias = reinterpret_cast<const T*>(a.b);
+  T* y = reinterpret_cast<T*>(a.y);
+  for (int it = tid; it < items; it += 256) {
+    const int pi = it / (rg * a.Q), rem = it - pi * rg * a.Q;
+    const int g = rem / a.Q, q = rem - g * a.Q;
+    const int pl0 = 4 * g;
+    const float* wp = ws + pi * 9;
+    const float* xp = smem + pi * per_plane + (pl0 * S) * a.LP + q * S + kDwCol0 - a.pw;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < NR; ++j) {
+      const float v0 = xp[j * a.LP], v1 = xp[j * a.LP + 1], v2 = xp[j * a.LP + 2];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int r = j - t * S;  // tap row of output row pl0 + t
+        if (r >= 0 && r < 3) acc[t] = fmaf(v0, wp[r * 3], fmaf(v1, wp[r * 3 + 1], fmaf(v2, wp[r * 3 + 2], acc[t])));
+      }
+    }
+    const int plane = plane0 + pi;
+    const float bv = bias ? elem<T>::load(bias + plane % a.C) : 0.f;
+    T* yp = y + (static_cast<int64_t>(plane) * a.P + p0 + pl0) * a.Q + q;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      if (pl0 + t < tb) {
+        float o = acc[t] + bv;
+        if (a.relu) o = fmaxf(o, 0.f);
+        elem<T>::store(yp + t * a.Q, o);
+      }
+    }
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void direct_naive_kernel(DirectArgs a, int64_t total) {
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
@@ -205,6 +360,38 @@ __global__ __launch_bounds__(256) void direct_naive_kernel(DirectArgs a, int64_t
 
 constexpr int kLdsBudget = 64 * 1024;
 
+// Plan of the depthwise 3x3 kernel: bands of TB output rows of PB planes,
+// about 2048 outputs per workgroup, within 32 KiB of LDS (several
+// workgroups per CU overlap one's loads with another's arithmetic).
+bool dw3_plan(const Shape& s, Dw3Args& a) {
+  if (s.Cg != 1 || s.Kg != 1 || s.R != 3 || s.S != 3 || s.dh != 1 || s.dw != 1) return false;
+  if (s.sh != s.sw || (s.sh != 1 && s.sh != 2) || s.ph > 1 || s.pw > 1) return false;
+  const int64_t x_bytes = s.N * s.C * s.H * s.W * s.esize();
+  if (x_bytes + 16 >= ((int64_t)1 << 31) || s.N * s.C >= ((int64_t)1 << 31)) return false;
+  a.NC = (int)(s.N * s.C); a.C = (int)s.C; a.H = (int)s.H; a.W = (int)s.W;
+  a.P = (int)s.P; a.Q = (int)s.Q; a.ph = s.ph; a.pw = s.pw; a.relu = s.relu ? 1 : 0;
+  a.x_bytes = (uint32_t)x_bytes;
+  a.LP = ((int)s.W + kDwCol0 + 1 + 3) & ~3;
+  const int PQ = (int)(s.P * s.Q);
+  if (PQ >= 2048) {
+    a.PB = 1;
+    a.TB = 2048 / (int)s.Q > 1 ? 2048 / (int)s.Q : 1;
+    if (a.TB > s.P) a.TB = (int)s.P;
+  } else {
+    a.TB = (int)s.P;
+    a.PB = 2048 / PQ > 1 ? 2048 / PQ : 1;
+  }
+  // Rows staged per plane: those of a band rounded up to whole 4-row strips
+  // (the rows past the band stay zero; the last strip reads them).
+  auto rows = [&](int tb) { return (((tb + 3) / 4) * 4 - 1) * s.sh + 3; };
+  auto lds = [&](int tb, int pb) { return (size_t)pb * ((size_t)rows(tb) * a.LP + 9) * 4; };
+  while (a.PB > 1 && lds(a.TB, a.PB) > 32 * 1024) a.PB = (a.PB + 1) / 2;
+  while (a.TB > 1 && lds(a.TB, a.PB) > 32 * 1024) a.TB = (a.TB + 1) / 2;
+  if (lds(a.TB, a.PB) > 32 * 1024) return false;
+  a.HB = rows(a.TB);
+  return true;
+}
+
 template <typename T>
 hipError_t launch_direct_typed(const Shape& s, const void* x, const void* w, const void* b, void* y,
                                hipStream_t stream) {
@@ -217,6 +404,17 @@ hipError_t launch_direct_typed(const Shape& s, const void* x, const void* w, con
   a.CC = a.HT = a.WT = a.XS = a.TPo = a.PB = 0;
   const int RS = a.R * a.S;
 
+  Dw3Args d3;
+  if (dw3_plan(s, d3)) {
+    d3.x = x; d3.w = w; d3.b = b; d3.y = y;
+    const dim3 grid((unsigned)((d3.P + d3.TB - 1) / d3.TB), (unsigned)((d3.NC + d3.PB - 1) / d3.PB));
+    const size_t lds = (size_t)d3.PB * ((size_t)d3.HB * d3.LP + 9) * 4;
+    if (s.sh == 1)
+      hipLaunchKernelGGL((direct_dw3_kernel<T, 1>), grid, dim3(256), lds, stream, d3);
+    else
+      hipLaunchKernelGGL((direct_dw3_kernel<T, 2>), grid, dim3(256), lds, stream, d3);
+    return hipGetLastError();
+  }
   if (a.Cg == 1) {
     // Depthwise-style: one input channel per group.
     const int WT = (a.Q - 1) * a.sw + (a.S - 1) * a.dw + 1;
@@ -265,6 +463,17 @@ hipError_t launch_direct_typed(const Shape& s, const void* x, const void* w, con
 }
 
 }  // namespace
+
+std::string direct_describe(const Shape& s) {
+  Dw3Args d3;
+  if (dw3_plan(s, d3)) {
+    char buf[256];
+    snprintf(buf, sizeof(buf), "direct kernels=direct_dw3_kernel<%s,%d> rows_per_band=%d planes_per_block=%d",
+             s.dtype == DT_F32 ? "f32" : "bf16", s.sh, d3.TB, d3.PB);
+    return buf;
+  }
+  return s.Cg == 1 ? "direct kernels=direct_depthwise_kernel" : "direct kernels=direct_tile_kernel";
+}
 
 hipError_t launch_direct(const Shape& s, const void* x, const void* w, const void* b, void* y,
                          hipStream_t stream) {

@@ -88,6 +88,7 @@ hipError_t ws_main(const Shape& s, const void* x, const void* wp, const void* b,
 std::string ws_describe(const Shape& s);
 
 // direct convolution (VALU), all N images.
+std::string direct_describe(const Shape& s);
 hipError_t launch_direct(const Shape& s, const void* x, const void* w, const void* b, void* y,
                          hipStream_t stream);
 
