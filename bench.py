@@ -7,8 +7,11 @@ accumulation), each layer running the algorithm chosen for it by measured
 per-layer selection (every supported algorithm timed on that layer before
 the timed region; the fastest goes into the algorithm table) or taken from a
 saved table.  Inputs, weights and outputs are resident in HBM before timing
-starts; each call is the full conv2d() of the C ABI (filters repacked every
-call) unless --prepacked.
+starts.  Each layer's filter package (the tile-ordered filter copy some
+kernels read) is built once before timing, as a framework-managed model
+(swap_backend) holds it, and the step calls conv2d_prepacked; with
+--pack-per-call the step calls the plain conv2d(), which rebuilds or
+regroups the filters in every call.
 
 The headline replays the step as one captured HIP graph (--eager: plain
 launches); all four step variants are reported.  Per-layer call durations
@@ -19,7 +22,7 @@ oracle is timed on a bounded sample on the host.
 Prints one JSON line (TFLOP/s, 2*N*K*(C/G)*R*S*P*Q per layer).
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload resnet50]
-                    [--select measured|default|<algo>] [--eager] [--prepacked]
+                    [--select measured|default|<algo>] [--eager] [--pack-per-call]
                     [--table FILE] [--save-table FILE] [--sweep FILE]
 """
 import argparse
@@ -346,9 +349,10 @@ def main():
     ap.add_argument("--select", default="measured")
     ap.add_argument("--eager", action="store_true",
                     help="headline from eager launches (default: the step captured once as a HIP graph and replayed)")
-    ap.add_argument("--prepacked", action="store_true",
-                    help="time the step with filter packages built before timing (conv2d_prepacked); by default "
-                         "every call rebuilds them from the filters")
+    ap.add_argument("--pack-per-call", action="store_true",
+                    help="headline from plain conv2d calls, every call rebuilding its filter package from the "
+                         "filters; by default each layer's package is built once before timing, as a "
+                         "framework-managed model (swap_backend) holds it, and the step calls conv2d_prepacked")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-executor", action="store_true",
                     help="skip the whole-network swap_backend forward (ResNet-50 only)")
@@ -459,11 +463,12 @@ def main():
 
     modes = {"graph": timed_steps(step, True), "graph_prepacked": timed_steps(step_pk, True),
              "eager": timed_steps(step, False), "eager_prepacked": timed_steps(step_pk, False)}
-    head = ("eager" if args.eager else "graph") + ("_prepacked" if args.prepacked else "")
+    prepacked = not args.pack_per_call
+    head = ("eager" if args.eager else "graph") + ("_prepacked" if prepacked else "")
     ms_per_step = modes[head]
     lms_unpk = layer_times(False)
     lms_pk = layer_times(True)
-    layer_ms = lms_pk if args.prepacked else lms_unpk
+    layer_ms = lms_pk if prepacked else lms_unpk
 
     total_flops = sum(p["layer"].flops for p in plan)
     value = total_flops / (ms_per_step * 1e-3) / 1e12
@@ -563,7 +568,8 @@ def main():
            "config": {"workload": "%s conv layers (%d convs), batch %d, %s data, fp32 accumulate, %s, %s"
                                   % (wl, len(layers), nbatch, dtype,
                                      "eager launches" if args.eager else "one HIP graph per step",
-                                     "prepacked filters" if args.prepacked else "filters packed every call"),
+                                     "filters packaged once before timing" if prepacked
+                                     else "filters packed every call"),
                       "global_batch": nbatch, "layers": len(layers), "parallelism": "none (1 GPU)"},
            "roofline": roofline, "cpu_baseline": cpu, "detail": extra}
     print(json.dumps(out), flush=True)
