@@ -43,6 +43,10 @@ struct GemmArgs {
   int relu;
   int out_f32;
   int b_kmajor;
+  // Set inside launch_gemm_nt only: with jspan > 0, column j of C is column
+  // j % jspan of batch item j / jspan (sCj apart), for a batch folded into N.
+  int jspan = 0;
+  int64_t sCj = 0;
 };
 
 hipError_t launch_gemm_nt(int dtype, const GemmArgs& g, hipStream_t stream);
