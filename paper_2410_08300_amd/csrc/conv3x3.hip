@@ -385,6 +385,17 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
         hcol[t] = ws + a.pw;
       }
     }
+    // LDS byte offset (within a stage) of each pixel unit of each item: the
+    // same in every chunk.
+    uint32_t hoff[HS][UPX];
+#pragma unroll
+    for (int t = 0; t < HS; ++t)
+#pragma unroll
+      for (int px = 0; px < UPX; ++px) {
+        const int pc = hcol[t] + px;
+        const int slot = S2 ? hrow[t] + (pc & 1) * a.PS + (pc >> 1) : hrow[t] + pc;
+        hoff[t][px] = static_cast<uint32_t>(slot * (CH * 2) + ((hg[t] ^ k3_swz<UP>(slot)) * 16));
+      }
     constexpr int HD = UPX / 2;  // dwords per channel of a window
     using S0 = std::integral_constant<int, 0>;
     using S1 = std::integral_constant<int, 1>;
@@ -471,16 +482,14 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
           if (hrow[t] >= 0) {
 #pragma unroll
             for (int px = 0; px < UPX; ++px) {
+              // pixel px of the window: channels 8g .. 8g+7, the px-th bf16 of
+              // each channel's loaded dword pair, as one 16-byte unit
               u32x4_t o;
 #pragma unroll
-              for (int m = 0; m < 4; ++m) {
-                const uint32_t d0 = hd[SET][t][2 * m][px >> 1], d1 = hd[SET][t][2 * m + 1][px >> 1];
-                o[m] = (px & 1) ? ((d0 >> 16) | (d1 & 0xFFFF0000u)) : ((d0 & 0xFFFFu) | (d1 << 16));
-              }
-              const int pc = hcol[t] + px;
-              const int slot = S2 ? hrow[t] + (pc & 1) * a.PS + (pc >> 1) : hrow[t] + pc;
-              const int unit_ = hg[t] ^ k3_swz<UP>(slot);
-              *reinterpret_cast<u32x4_t*>(Hs + slot * (CH * 2) + unit_ * 16) = o;
+              for (int m = 0; m < 4; ++m)
+                o[m] = __builtin_amdgcn_perm(hd[SET][t][2 * m + 1][px >> 1], hd[SET][t][2 * m][px >> 1],
+                                             (px & 1) ? 0x07060302u : 0x05040100u);
+              *reinterpret_cast<u32x4_t*>(Hs + hoff[t][px]) = o;
             }
           }
         }
@@ -573,26 +582,28 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
             // pixel px of the window: channels 8g .. 8g+7 as one 16-byte unit
             u32x4_t o;
 #pragma unroll
-            for (int m = 0; m < 4; ++m) {
-              const uint32_t d0 = hd[SET][t][2 * m][px >> 1], d1 = hd[SET][t][2 * m + 1][px >> 1];
-              o[m] = (px & 1) ? ((d0 >> 16) | (d1 & 0xFFFF0000u)) : ((d0 & 0xFFFFu) | (d1 << 16));
-            }
-            const int pc = hcol[t] + px;
-            const int slot = S2 ? hrow[t] + (pc & 1) * a.PS + (pc >> 1) : hrow[t] + pc;
-            const int unit_ = hg[t] ^ k3_swz<UP>(slot);
-            *reinterpret_cast<u32x4_t*>(Hs + slot * (CH * 2) + unit_ * 16) = o;
+            for (int m = 0; m < 4; ++m)
+              o[m] = __builtin_amdgcn_perm(hd[SET][t][2 * m + 1][px >> 1], hd[SET][t][2 * m][px >> 1],
+                                           (px & 1) ? 0x07060302u : 0x05040100u);
+            *reinterpret_cast<u32x4_t*>(Hs + hoff[t][px]) = o;
           }
         }
       }
       if (f_on) {
-        // element i = c * 9 + tap of the 72 loaded values (c = 0..7)
-        auto el = [&](int i) -> uint32_t { return (fd[SET][i >> 3][(i >> 1) & 3] >> (16 * (i & 1))) & 0xFFFFu; };
+        // element i = c * 9 + tap of the 72 loaded values (c = 0..7): the
+        // (i & 1) half of dword (i >> 1) & 3 of load i >> 3.  Output dword m
+        // of a tap unit pairs elements 2m * 9 + tap and (2m + 1) * 9 + tap.
         const int unit_ = fg ^ k3_swz<UP>(kl);
 #pragma unroll
         for (int tap = 0; tap < kK3Taps; ++tap) {
           u32x4_t o;
 #pragma unroll
-          for (int m = 0; m < 4; ++m) o[m] = el(2 * m * kK3Taps + tap) | (el((2 * m + 1) * kK3Taps + tap) << 16);
+          for (int m = 0; m < 4; ++m) {
+            const int i0 = 2 * m * kK3Taps + tap, i1 = (2 * m + 1) * kK3Taps + tap;
+            const uint32_t sel = (2u * (i0 & 1)) | ((2u * (i0 & 1) + 1u) << 8) | ((4u + 2u * (i1 & 1)) << 16) |
+                                 ((5u + 2u * (i1 & 1)) << 24);
+            o[m] = __builtin_amdgcn_perm(fd[SET][i1 >> 3][(i1 >> 1) & 3], fd[SET][i0 >> 3][(i0 >> 1) & 3], sel);
+          }
           *reinterpret_cast<u32x4_t*>(Fs + (tap * TK + kl) * (CH * 2) + unit_ * 16) = o;
         }
       }
