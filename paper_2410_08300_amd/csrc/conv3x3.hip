@@ -33,7 +33,11 @@
 //     filter tensor, each (chunk, channel tile) filter tile stored in its
 //     LDS order: two loader waves copy it by LDS DMA with no register
 //     traffic while the other two transpose the halo, over three LDS stages
-//     (the DMA of chunk i+2 goes out while chunk i is multiplied).
+//     (the DMA of chunk i+2 goes out while chunk i is multiplied);
+//   * prepacked into registers (BG = true), from the same package: each
+//     compute wave loads the 16-byte fragments it multiplies straight into
+//     registers, a chunk ahead, and all four loader waves stage only the
+//     halo (two LDS stages).
 //
 // Compute waves form a WP x WK grid; each holds MB x NB blocks of 32 x 32
 // accumulators (32 MB pixels x 32 NB channels), so that each operand read
@@ -309,7 +313,7 @@ __device__ __forceinline__ void k3_epilogue(const f32x16_t (&acc)[MB][NB], char*
   }
 }
 
-template <int CH, int WP, int WK, int MB, int NB, bool S2, int UPX, int HS, bool PK>
+template <int CH, int WP, int WK, int MB, int NB, bool S2, int UPX, int HS, bool PK, bool BG>
 __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Args a) {
   constexpr int NC = WP * WK;                 // compute waves
   constexpr int TP = WP * MB * 32, TK = WK * NB * 32;
@@ -317,6 +321,8 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
   constexpr int KS = CH / 16;                 // MFMA steps per tap and chunk
   static_assert(CH == 16 || CH == 32, "channel chunk");
   static_assert(UPX == 8 || UPX == 4, "column window");
+  static_assert(!(PK && BG), "one filter path");
+  constexpr bool FL = !PK && !BG;             // the loader waves stage the filters from KCRS
   extern __shared__ __align__(16) vec16 smem[];
   char* lds = reinterpret_cast<char*>(smem);
 
@@ -538,10 +544,12 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
     const uint32_t fvo = (f_on && k0 + kl < a.K)
                              ? static_cast<uint32_t>(((k0 + kl) * a.C + 8 * fg) * kK3Taps) * 2
                              : a.w_bytes;
-    // Every chunk issues the same HS * 8 + 9 loads per lane (unused halo
-    // slots read zeros past the buffer), so the compiler's own count of the
-    // loads in flight matches the explicit waits below.
-    constexpr int PER = HS * 8 + kK3Taps;
+    // Every chunk issues the same HS * 8 (+ 9 filter) loads per lane (unused
+    // halo slots read zeros past the buffer), so the compiler's own count of
+    // the loads in flight matches the explicit waits below.  With BG the
+    // compute waves read the filters themselves and the loaders only stage
+    // the halo.
+    constexpr int PER = HS * 8 + (FL ? kK3Taps : 0);
     static_assert(2 * PER <= 63, "vmcnt range");
     // Two register sets, by chunk parity: chunk i+2's loads stay in flight
     // while chunk i+1 is written to LDS.
@@ -565,10 +573,12 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
           }
         }
       }
-      const uint32_t fso = static_cast<uint32_t>(c0 * kK3Taps * 2);
+      if constexpr (FL) {
+        const uint32_t fso = static_cast<uint32_t>(c0 * kK3Taps * 2);
 #pragma unroll
-      for (int q = 0; q < kK3Taps; ++q)
-        fd[SET][q] = __builtin_amdgcn_raw_buffer_load_b128(wr, fvo, fso + 16 * q, 0);
+        for (int q = 0; q < kK3Taps; ++q)
+          fd[SET][q] = __builtin_amdgcn_raw_buffer_load_b128(wr, fvo, fso + 16 * q, 0);
+      }
     };
     auto write = [&](int st, auto set_c) {
       constexpr int SET = decltype(set_c)::value;
@@ -589,7 +599,7 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
           }
         }
       }
-      if (f_on) {
+      if (FL && f_on) {
         // element i = c * 9 + tap of the 72 loaded values (c = 0..7): the
         // (i & 1) half of dword (i >> 1) & 3 of load i >> 3.  Output dword m
         // of a tap unit pairs elements 2m * 9 + tap and (2m + 1) * 9 + tap.
@@ -685,13 +695,39 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = zero16();
 
+  // BG: every filter fragment of a chunk lives in registers, read straight
+  // from the package ([chunk][channel tile][tap][TK][CH] units) by the wave
+  // that multiplies it: the fragment of step S is reloaded with the next
+  // chunk's right after its last MFMA, a whole chunk ahead of its use, and
+  // the LDS carries only the halo.  (The last chunk reloads itself.)
+  constexpr int NSTEP_ALL = kK3Taps * KS;
+  constexpr int NBG = BG ? NSTEP_ALL : 1;
+  bf16x8_t bq[NBG][NB];
+  uint32_t bvo[NB];
+  const __amdgpu_buffer_rsrc_t pr = make_rsrc(a.w, a.w_bytes);
+  if constexpr (BG) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) bvo[nb] = static_cast<uint32_t>(((wk * NB + nb) * 32 + l32) * UP + half) * 16;
+  }
+  auto bload = [&](int ch, auto s_c) {
+    constexpr int S = decltype(s_c)::value;
+    constexpr int t = S / KS, u = S % KS;
+    const uint32_t so = static_cast<uint32_t>((((ch_begin + ch) * a.ktiles + ktile) * kK3Taps + t) * TK * UP + 2 * u) * 16;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(pr, bvo[nb], so, 0);
+      __builtin_memcpy(&bq[S][nb], &v, 16);
+    }
+  };
+  if constexpr (BG) static_for<NSTEP_ALL>([&](auto s_c) { bload(0, s_c); });
+
   // A chunk is 9 KS steps (tap t, 16-channel slice u), each MB pixel and NB
   // filter fragment reads and MB x NB MFMAs.  The reads run D steps ahead of
   // the MFMAs (at most 15 LDS reads in flight per wave), and a wave with a
   // single 32 x 32 block alternates two accumulators by step parity, so that
   // neither an LDS round trip nor a dependent MFMA sits between two MFMAs.
   constexpr int NSTEP = kK3Taps * KS;
-  constexpr int RD = MB + NB;                 // reads per step
+  constexpr int RD = MB + (BG ? 0 : NB);      // LDS reads per step
   constexpr int D0 = 15 / RD - 1;
   constexpr int D = D0 < 1 ? 1 : (D0 > NSTEP - 1 ? NSTEP - 1 : D0);
   constexpr int NACC = MB * NB == 1 ? 2 : 1;
@@ -714,10 +750,12 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
         fa[slot][mb] =
             *reinterpret_cast<const bf16x8_t*>(Hs + pos * (CH * 2) + (((2 * u + half) ^ k3_swz<UP>(pos)) * 16));
       }
+      if constexpr (!BG)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        fb[slot][nb] = *reinterpret_cast<const bf16x8_t*>(Fs + t * (TK * CH * 2) + boff[nb][u]);
+        for (int nb = 0; nb < NB; ++nb)
+          fb[slot][nb] = *reinterpret_cast<const bf16x8_t*>(Fs + t * (TK * CH * 2) + boff[nb][u]);
     };
+    const int nxt = i + 1 < nchunks ? i + 1 : i;
     static_for<D>([&](auto s_c) { read(s_c); });
     static_for<NSTEP>([&](auto s_c) {
       constexpr int S = decltype(s_c)::value;
@@ -726,15 +764,17 @@ __global__ __launch_bounds__((WP * WK + kLoaders) * 64) void conv3x3_kernel(K3Ar
       // next to its MFMA.
       __builtin_amdgcn_sched_barrier(0);
       constexpr int slot = S % (D + 1);
+      auto bfrag = [&](int nb) -> const bf16x8_t& { return BG ? bq[BG ? S : 0][nb] : fb[slot][nb]; };
       if constexpr (NACC == 2 && (S & 1)) {
-        acc2[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][0], fb[slot][0], acc2[0], 0, 0, 0);
+        acc2[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][0], bfrag(0), acc2[0], 0, 0, 0);
       } else {
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb)
-            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][mb], fb[slot][nb], acc[mb][nb], 0, 0, 0);
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][mb], bfrag(nb), acc[mb][nb], 0, 0, 0);
       }
+      if constexpr (BG) bload(nxt, s_c);
       __builtin_amdgcn_sched_barrier(0);
     });
     lds_sync();  // B(i)
@@ -776,7 +816,8 @@ constexpr int kNumK3Configs = sizeof(kK3Configs) / sizeof(kK3Configs[0]);
 
 struct K3Plan {
   int cfg;
-  bool pk;   // filters from the tile-ordered package by DMA (three LDS stages)
+  bool pk;   // filters from the tile-ordered package (by DMA, three LDS stages; or, with bg, into registers)
+  bool bg;   // the compute waves read their filter fragments from the package into registers
   bool aligned;  // pixel layout with bank-aligned rows (E >= Q), else E = Q
   int nsplit;    // ways the channel reduction is split
   bool s2;
@@ -853,11 +894,17 @@ void k3_layout(const Shape& s, bool aligned, int& E, int& RS, int& PS, int& Hp) 
     }
 }
 
-bool make_k3_plan_cfg(const Shape& s, int cfg, K3Plan& pl, int64_t N1, bool pk, bool aligned, int nsplit) {
+bool make_k3_plan_cfg(const Shape& s, int cfg, K3Plan& pl, int64_t N1, bool pk, bool aligned, int nsplit,
+                      bool bg = false) {
   const K3Config c = kK3Configs[cfg];
   if (s.C % c.CH != 0) return false;
+  // The register copy of a chunk's filter fragments fits next to the
+  // accumulators only for the tiles with at most 72 fragment registers and
+  // 32 or 64 accumulators.
+  if (bg && (!pk || kK3Taps * (c.CH / 16) * c.NB * 4 > 72 || c.MB * c.NB > 4)) return false;
   pl.cfg = cfg;
   pl.pk = pk;
+  pl.bg = bg;
   pl.aligned = aligned;
   pl.s2 = s.sh == 2;
   pl.upx = s.W >= 8 ? 8 : 4;
@@ -876,13 +923,14 @@ bool make_k3_plan_cfg(const Shape& s, int cfg, K3Plan& pl, int64_t N1, bool pk, 
   a.VR = k3_halo_rows(s, N1, a.Hp, c.tp(), a.E);
   a.NG = (int)((s.W + pl.upx - 1) / pl.upx);
   a.halo_items = a.VR * a.NG * (c.CH / 8);
-  if (a.halo_items > kHSMax * (pk ? 128 : 256)) return false;
+  const int halo_lanes = pk && !bg ? 128 : 256;
+  if (a.halo_items > kHSMax * halo_lanes) return false;
   // 16 spare zero slots after the last row: taps of the last row's final
   // pixels (and of padding pixels) read past it.
   a.halo_bytes = (int)((((size_t)a.VR * a.RS + 16) * c.CH * 2 + 255) / 256 * 256);
-  const size_t filt = (size_t)kK3Taps * c.tk() * c.CH * 2;
+  const size_t filt = bg ? 0 : (size_t)kK3Taps * c.tk() * c.CH * 2;
   a.stage_bytes = (int)(a.halo_bytes + filt);
-  pl.lds = (size_t)(pk ? 3 : 2) * a.stage_bytes;
+  pl.lds = (size_t)(pk && !bg ? 3 : 2) * a.stage_bytes;
   // The epilogue stages each compute wave's fp32 or bf16 rows in LDS.
   const size_t staging = (size_t)c.nc() * c.MB * 32 * 32 * 4;
   if (pl.lds < staging) pl.lds = staging;
@@ -917,22 +965,27 @@ bool make_k3_plan_cfg(const Shape& s, int cfg, K3Plan& pl, int64_t N1, bool pk, 
 // (relative error) to measured times of the bf16 3x3 layers of ResNet-50 at
 // batch 32 over every tile shape and split of 1, 2 and 4; one set for the
 // per-call kernel (filters regrouped by the loaders), one for the package
-// kernel (filters by DMA).  Median error about 6% (per call) and 12%
-// (package).
+// kernel with filters by DMA, one for the package kernel with filters in
+// the compute waves' registers (the loaders then stage only the halo, with
+// all 256 lanes).  Median error about 6% (per call), 12% (DMA) and 5%
+// (registers).  The register path wins where the halo is the loaders'
+// bottleneck (the stride-2 layers: their halo holds four input pixels per
+// output pixel).
 struct K3CostParams {
   double a, b[kNumK3Configs], c, d, e, f, g;
 };
 constexpr K3CostParams kK3CostCall = {7.18, {0.0180, 0.0252, 0.0307, 0.0534}, 0.500, 0.0, 2.99, 0.168, 4.85};
 constexpr K3CostParams kK3CostPack = {4.90, {0.0180, 0.0278, 0.0175, 0.0094}, 0.315, 0.0, 0.90, 0.204, 4.39};
+constexpr K3CostParams kK3CostBg = {4.41, {1.0, 0.0226, 0.0333, 0.0482}, 0.543, 0.0, 3.29, 0.128, 4.59};
 
 double k3_cost(const K3Plan& pl, const Shape& s) {
-  const K3CostParams& m = pl.pk ? kK3CostPack : kK3CostCall;
+  const K3CostParams& m = pl.bg ? kK3CostBg : pl.pk ? kK3CostPack : kK3CostCall;
   const K3Config c = kK3Configs[pl.cfg];
   const K3Args& a = pl.a;
   const int64_t wgs = (int64_t)a.ptiles * a.ktiles * a.e.splits;
   const double rounds = (double)((wgs + kCUs - 1) / kCUs);
   const double mfma = (double)kK3Taps * (c.CH / 16) * c.MB * c.NB;
-  const int HL = pl.pk ? 128 : 256;
+  const int HL = pl.pk && !pl.bg ? 128 : 256;
   const double hs = (double)((a.halo_items + HL - 1) / HL);
   const double filt = pl.pk ? 0.0 : (double)c.tk() * c.CH / 1024.0;
   const double chunk = std::max(m.b[pl.cfg] * mfma, m.c * hs * c.CH / 16.0 + m.d * filt);
@@ -959,9 +1012,10 @@ bool make_k3_plan(const Shape& s, K3Plan& pl, int64_t N1 = -1, bool prepacked = 
   // remainder launch (N not a multiple of the images per launch) must fit the
   // same choice.
   const int64_t r = s.N % N1;
-  auto build = [&](int cfg, bool pk, bool al, int S, K3Plan& out) {
+  auto build = [&](int cfg, bool pk, bool al, int S, K3Plan& out, bool bg = false) {
     K3Plan rest;
-    return make_k3_plan_cfg(s, cfg, out, N1, pk, al, S) && (r == 0 || make_k3_plan_cfg(s, cfg, rest, r, pk, al, S));
+    return make_k3_plan_cfg(s, cfg, out, N1, pk, al, S, bg) &&
+           (r == 0 || make_k3_plan_cfg(s, cfg, rest, r, pk, al, S, bg));
   };
   bool found = false;
   double best = 0;
@@ -975,10 +1029,15 @@ bool make_k3_plan(const Shape& s, K3Plan& pl, int64_t N1 = -1, bool prepacked = 
         al = false;
         if (!build(cfg, false, false, S, call)) continue;
       }
-      // The package kernel: not for the 512-pixel tile, where the register
-      // path measured as fast.
-      K3Plan pack;
-      const bool has_pack = cfg != 0 && build(cfg, true, al, S, pack);
+      // The package kernels: filters by DMA (not for the 512-pixel tile,
+      // where the register path measured as fast) or read into registers by
+      // the compute waves, whichever is estimated faster.
+      K3Plan pack, pack_bg;
+      bool has_pack = cfg != 0 && build(cfg, true, al, S, pack);
+      if (build(cfg, true, al, S, pack_bg, true) && (!has_pack || k3_cost(pack_bg, s) < k3_cost(pack, s))) {
+        pack = pack_bg;
+        has_pack = true;
+      }
       const double t = k3_cost(call, s) + (has_pack ? k3_cost(pack, s) : k3_cost(call, s));
       if (!found || t < best) {
         best = t;
@@ -1006,7 +1065,7 @@ bool k3_plan_for_launch(const Shape& s, const K3Plan& pl, int64_t cnt, K3Plan& c
     cur = pl;
     return true;
   }
-  return make_k3_plan_cfg(s, pl.cfg, cur, cnt, pl.pk, pl.aligned, pl.nsplit);
+  return make_k3_plan_cfg(s, pl.cfg, cur, cnt, pl.pk, pl.aligned, pl.nsplit, pl.bg);
 }
 
 // Filter package: for chunk cg (CH channels) and channel tile kt, the LDS
@@ -1051,9 +1110,9 @@ __global__ __launch_bounds__(kK3PackThreads) void k3_pack_kernel(const uint16_t*
   }
 }
 
-template <int CH, int WP, int WK, int MB, int NB, bool S2, int UPX, int HS, bool PK>
+template <int CH, int WP, int WK, int MB, int NB, bool S2, int UPX, int HS, bool PK, bool BG>
 hipError_t k3_launch(const K3Plan& pl, const K3Args& a, hipStream_t stream) {
-  const auto kern = conv3x3_kernel<CH, WP, WK, MB, NB, S2, UPX, HS, PK>;
+  const auto kern = conv3x3_kernel<CH, WP, WK, MB, NB, S2, UPX, HS, PK, BG>;
   static std::atomic<int> lds_limit{64 * 1024};
   if ((int)pl.lds > lds_limit.load()) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -1075,11 +1134,18 @@ hipError_t k3_launch(const K3Plan& pl, const K3Args& a, hipStream_t stream) {
 
 template <int CH, int WP, int WK, int MB, int NB, bool S2, int UPX>
 hipError_t k3_dispatch_hs(const K3Plan& pl, const K3Args& a, hipStream_t st) {
+  if (pl.bg) {
+    // only the tiles whose fragments fit in registers (make_k3_plan_cfg)
+    if constexpr (kK3Taps * (CH / 16) * NB * 4 <= 72 && MB * NB <= 4)
+      return a.halo_items > 256 ? k3_launch<CH, WP, WK, MB, NB, S2, UPX, 2, false, true>(pl, a, st)
+                                : k3_launch<CH, WP, WK, MB, NB, S2, UPX, 1, false, true>(pl, a, st);
+    return hipErrorInvalidValue;
+  }
   if (pl.pk)
-    return a.halo_items > 128 ? k3_launch<CH, WP, WK, MB, NB, S2, UPX, 2, true>(pl, a, st)
-                              : k3_launch<CH, WP, WK, MB, NB, S2, UPX, 1, true>(pl, a, st);
-  return a.halo_items > 256 ? k3_launch<CH, WP, WK, MB, NB, S2, UPX, 2, false>(pl, a, st)
-                            : k3_launch<CH, WP, WK, MB, NB, S2, UPX, 1, false>(pl, a, st);
+    return a.halo_items > 128 ? k3_launch<CH, WP, WK, MB, NB, S2, UPX, 2, true, false>(pl, a, st)
+                              : k3_launch<CH, WP, WK, MB, NB, S2, UPX, 1, true, false>(pl, a, st);
+  return a.halo_items > 256 ? k3_launch<CH, WP, WK, MB, NB, S2, UPX, 2, false, false>(pl, a, st)
+                            : k3_launch<CH, WP, WK, MB, NB, S2, UPX, 1, false, false>(pl, a, st);
 }
 
 template <int CH, int WP, int WK, int MB, int NB>
@@ -1177,17 +1243,19 @@ std::string k3_describe(const Shape& s, bool prepacked) {
   const K3Config c = kK3Configs[pl.cfg];
   char buf[512];
   snprintf(buf, sizeof(buf),
-           "implicit_gemm kernels=%sconv3x3_kernel<%d,%d,%d,%d,%d,%d,%d,%d,%d>%s tile=%dx%d grid=%dx%d chunk=%d "
+           "implicit_gemm kernels=%sconv3x3_kernel<%d,%d,%d,%d,%d,%d,%d,%d,%d,%d>%s tile=%dx%d grid=%dx%d chunk=%d "
            "halo_rows=%d halo_items=%d row_slots=%d cols=%d lds=%zu images_per_launch=%lld (loader waves: halo "
            "rows transposed to pixel-major LDS, %s; compute waves: MFMA %dx%d per wave)",
            pl.pk ? "k3_pack_kernel;" : "", c.CH, c.WP, c.WK, c.MB, c.NB, pl.s2 ? 1 : 0, pl.upx,
-           pl.a.halo_items > (pl.pk ? 128 : 256) ? 2 : 1, pl.pk ? 1 : 0,
+           pl.a.halo_items > (pl.pk && !pl.bg ? 128 : 256) ? 2 : 1, pl.pk && !pl.bg ? 1 : 0, pl.bg ? 1 : 0,
            pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "",
            c.tp(), c.tk(), pl.a.ptiles * pl.a.ktiles, pl.a.e.splits, c.CH, pl.a.VR, pl.a.halo_items, pl.a.RS,
            pl.a.E, pl.lds,
            (long long)pl.images_per_launch,
-           pl.pk ? "filter tiles copied by DMA from the package, three LDS stages"
-                 : "KCRS filters regrouped to tap-major LDS, two LDS stages",
+           pl.bg   ? "filter fragments read from the package into the compute waves' registers, halo only in "
+                     "LDS, two LDS stages"
+           : pl.pk ? "filter tiles copied by DMA from the package, three LDS stages"
+                   : "KCRS filters regrouped to tap-major LDS, two LDS stages",
            32 * c.MB, 32 * c.NB);
   return buf;
 }

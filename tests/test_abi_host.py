@@ -117,9 +117,12 @@ def test_workspace_sizes():
     # implicit GEMM, bf16 3x3 (stride 1 or 2, C a multiple of 16): conv2d()
     # reads the filters as given (the workspace sizes a copy or package, used
     # only for unaligned filter pointers), plus fp32 split partial sums when
-    # the plan splits the channels.  Prepacked calls copy each filter tile by
-    # DMA from a tile-ordered package ([chunk][channel tile][tap][TK][CH])
-    # where three LDS stages fit.  Output rows are padded to a multiple of 8
+    # the plan splits the channels.  Prepacked calls read a tile-ordered
+    # package ([chunk][channel tile][tap][TK][CH]): each filter tile copied
+    # by DMA where three LDS stages fit, or each compute wave's fragments
+    # loaded into its registers, whichever the planner estimates faster.
+    # The last template argument is that register path.  Output rows are
+    # padded to a multiple of 8
     # pixels in the tile enumeration (row_slots, cols).
     # 64 -> 64 channels, 56x56, batch 32: 196 tiles of 512 x 64, no split;
     # the package is a plain copy (the register path for this tile).
@@ -127,7 +130,7 @@ def test_workspace_sizes():
     assert _lib.workspace_bytes(large, "implicit_gemm") == 64 * 64 * 9 * 2
     assert _lib.prepacked_workspace_bytes(large, "implicit_gemm") == 0
     d = _lib.describe(large, "implicit_gemm")
-    assert "conv3x3_kernel<16,4,1,4,2,0,8,1,0> tile=512x64 grid=196x1" in d and "prepacked_kernel" not in d
+    assert "conv3x3_kernel<16,4,1,4,2,0,8,1,0,0> tile=512x64 grid=196x1" in d and "prepacked_kernel" not in d
     assert "row_slots=72 cols=56" in d
     # 256 -> 256 channels, 14x14, batch 32: rows of 14 enumerated as 16, so
     # 56 x 4 tiles of 128 x 64, no split; the package holds 16 chunks x 4
@@ -136,27 +139,30 @@ def test_workspace_sizes():
     assert _lib.packed_filter_bytes(mid, "implicit_gemm") == 256 * 256 * 9 * 2
     assert _lib.prepacked_workspace_bytes(mid, "implicit_gemm") == 0
     d = _lib.describe(mid, "implicit_gemm")
-    assert "conv3x3_kernel<32,2,2,2,1,0,8,1,0> tile=128x64 grid=224x1" in d and "row_slots=16 cols=16" in d
-    assert "prepacked_kernel=conv3x3_kernel<32,2,2,2,1,0,8,1,1>" in d
+    assert "conv3x3_kernel<32,2,2,2,1,0,8,1,0,0> tile=128x64 grid=224x1" in d and "row_slots=16 cols=16" in d
+    assert "prepacked_kernel=conv3x3_kernel<32,2,2,2,1,0,8,1,1,0>" in d
     # 512 -> 512 channels, 14x14 -> 7x7 (stride 2): rows of 7 enumerated as
     # 8, 56 x 4 tiles of 128 x 128, the 32 chunks split four ways.
     s4 = _lib.make_desc(32, 512, 14, 14, 512, 3, 3, 2, 1, 1, 1, "bf16")
     assert _lib.prepacked_workspace_bytes(s4, "implicit_gemm") == 4 * 32 * 512 * 49 * 4
-    assert "conv3x3_kernel<16,2,2,2,2,1,8,1,0>;splitk_reduce_kernel tile=128x128 grid=56x4" in \
+    assert "conv3x3_kernel<16,2,2,2,2,1,8,1,0,0>;splitk_reduce_kernel tile=128x128 grid=56x4" in \
         _lib.describe(s4, "implicit_gemm")
     # 512 -> 512 channels, 7x7: 64 x 64 tiles, no split; halo rows share
     # their padding columns (8 slots per row).
     s7 = _lib.make_desc(32, 512, 7, 7, 512, 3, 3, 1, 1, 1, 1, "bf16")
     assert _lib.prepacked_workspace_bytes(s7, "implicit_gemm") == 0
-    assert "conv3x3_kernel<32,2,2,1,1,0,4,1,0> tile=64x64 grid=224x1" in _lib.describe(s7, "implicit_gemm")
+    assert "conv3x3_kernel<32,2,2,1,1,0,4,1,0,0> tile=64x64 grid=224x1" in _lib.describe(s7, "implicit_gemm")
     assert "row_slots=8 cols=8" in _lib.describe(s7, "implicit_gemm")
-    # Stride 2 splits rows into column-parity planes (here too large a halo
-    # for three stages: no package); 7-wide rows load in 4-pixel windows.
+    # Stride 2 splits rows into column-parity planes; its halo is the
+    # loaders' bottleneck, so prepacked calls read the filter fragments into
+    # the compute waves' registers and the loaders stage only the halo.
+    # 7-wide rows load in 4-pixel windows.
     s2 = _lib.make_desc(32, 128, 56, 56, 128, 3, 3, 2, 1, 1, 1, "bf16")
     d = _lib.describe(s2, "implicit_gemm")
-    assert "conv3x3_kernel<16,2,2,2,2,1,8,1,0> tile=128x128 grid=224x1" in d and "prepacked_kernel" not in d
+    assert "conv3x3_kernel<16,2,2,2,2,1,8,1,0,0> tile=128x128 grid=224x1" in d
+    assert "prepacked_kernel=conv3x3_kernel<16,2,2,2,2,1,8,1,0,1>" in d
     small = _lib.make_desc(32, 64, 7, 7, 128, 3, 3, 1, 1, 1, 1, "bf16")
-    assert "conv3x3_kernel<32,2,2,1,1,0,4,1,0> tile=64x64" in _lib.describe(small, "implicit_gemm")
+    assert "conv3x3_kernel<32,2,2,1,1,0,4,1,0,0> tile=64x64" in _lib.describe(small, "implicit_gemm")
     # Other bf16 3x3 layers (channels not a multiple of 16, dilation, planes
     # below 8 pixels) keep the loader/compute-wave kernel and its package
     # [16-channel chunk][K padded to the tile][19 units of 8 channels].

@@ -117,17 +117,17 @@ RESIDUAL = [
     ("bf16", 5, 64, 2, 3, 96, 1, 1, 0, True, "repack_plane_kernel;pointwise_dma_kernel<16,4,4>"),
     ("bf16", 4, 1024, 7, 7, 256, 1, 1, 0, True, "repack_plane_kernel;pointwise_dma_kernel<16,4,4>;splitk_reduce_kernel"),
     ("bf16", 3, 64, 3, 3, 64, 1, 1, 0, False, "repack_plane_kernel;pointwise_dma_kernel<16,4,4>"),
-    ("bf16", 2, 64, 28, 28, 64, 3, 1, 1, True, "conv3x3_kernel<32,2,2,1,1,0,8,1,1>"),
-    ("bf16", 3, 32, 8, 8, 32, 3, 1, 1, False, "conv3x3_kernel<32,2,2,1,1,0,8,1,1>"),
-    ("bf16", 2, 256, 7, 7, 256, 3, 1, 1, True, "conv3x3_kernel<32,2,2,1,1,0,4,1,1>;splitk_reduce_kernel"),
+    ("bf16", 2, 64, 28, 28, 64, 3, 1, 1, True, "conv3x3_kernel<32,2,2,1,1,0,8,1,1,0>"),
+    ("bf16", 3, 32, 8, 8, 32, 3, 1, 1, False, "conv3x3_kernel<32,2,2,1,1,0,8,1,1,0>"),
+    ("bf16", 2, 256, 7, 7, 256, 3, 1, 1, True, "conv3x3_kernel<32,2,2,1,1,0,4,1,1,0>;splitk_reduce_kernel"),
     ("bf16", 2, 24, 9, 9, 40, 3, 1, 1, True, "implicit_ws_kernel<64,0,1>"),
-    ("bf16", 32, 256, 14, 14, 256, 3, 1, 1, True, "conv3x3_kernel<32,2,2,2,1,0,8,1,1>"),
-    ("bf16", 32, 128, 28, 28, 128, 3, 1, 1, False, "conv3x3_kernel<16,2,2,2,2,0,8,1,1>"),
-    ("bf16", 32, 64, 56, 56, 64, 3, 1, 1, True, "conv3x3_kernel<16,4,1,4,2,0,8,1,0>"),
-    ("bf16", 32, 128, 56, 56, 128, 3, 2, 1, True, "conv3x3_kernel<16,2,2,2,2,1,8,1,0>"),
-    ("bf16", 2, 128, 112, 112, 64, 3, 1, 1, False, "conv3x3_kernel<32,2,2,2,1,0,8,1,0>"),
-    ("bf16", 2, 256, 28, 28, 256, 3, 2, 1, True, "conv3x3_kernel<32,2,2,1,1,1,8,1,0>;splitk_reduce_kernel"),
-    ("bf16", 4, 256, 14, 14, 256, 3, 1, 1, False, "conv3x3_kernel<32,2,2,1,1,0,8,1,1>;splitk_reduce_kernel"),
+    ("bf16", 32, 256, 14, 14, 256, 3, 1, 1, True, "conv3x3_kernel<32,2,2,2,1,0,8,1,1,0>"),
+    ("bf16", 32, 128, 28, 28, 128, 3, 1, 1, False, "conv3x3_kernel<16,2,2,2,2,0,8,1,0,1>"),
+    ("bf16", 32, 64, 56, 56, 64, 3, 1, 1, True, "conv3x3_kernel<16,4,1,4,2,0,8,1,0,0>"),
+    ("bf16", 32, 128, 56, 56, 128, 3, 2, 1, True, "conv3x3_kernel<16,2,2,2,2,1,8,1,0,1>"),
+    ("bf16", 2, 128, 112, 112, 64, 3, 1, 1, False, "conv3x3_kernel<32,2,2,2,1,0,8,1,0,1>"),
+    ("bf16", 2, 256, 28, 28, 256, 3, 2, 1, True, "conv3x3_kernel<32,2,2,1,1,1,8,1,0,1>;splitk_reduce_kernel"),
+    ("bf16", 4, 256, 14, 14, 256, 3, 1, 1, False, "conv3x3_kernel<32,2,2,1,1,0,8,1,1,0>;splitk_reduce_kernel"),
     ("bf16", 7, 48, 2, 2, 64, 3, 1, 1, True, "implicit_gemm_kernel<bf16,64,2,9>;splitk_reduce_kernel"),
     ("bf16", 2, 3, 32, 32, 16, 3, 1, 1, False, "implicit_gemm_kernel<bf16,64,1,9>"),
     ("bf16", 2, 3, 64, 64, 64, 7, 2, 3, True, "implicit_rows_kernel"),
