@@ -180,6 +180,52 @@ def calibration_copy(mib, device):
     log("calibration copy: %d bytes read, %d bytes written" % (w.numel() * 2, w.numel() * 2))
 
 
+def measured_peaks(device):
+    """What this machine delivers, beside the nominal peaks: the MFMA rate of a
+    register-only probe (bf16 and fp32) and the HBM rate of a plain 16-byte
+    copy of 1 GiB (bytes read plus bytes written per second), each the best of
+    five timed launches after one warm-up."""
+    import torch
+    from paper_2410_08300_amd import _lib
+    stream = torch.cuda.current_stream(device)
+    out = {}
+    blocks, iters = 1024, 2000
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device=device)
+    for dt, flops_per in (("bf16", 32768), ("f32", 4096)):
+        its = iters if dt == "bf16" else iters // 4
+        best = None
+        for rep in range(6):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            _lib.probe_mfma(dt, blocks, its, sink.data_ptr(), stream.cuda_stream)
+            e1.record(stream)
+            e1.synchronize()
+            ms = e0.elapsed_time(e1)
+            if rep and (best is None or ms < best):
+                best = ms
+        tf = blocks * 4 * its * 8 * flops_per / (best * 1e-3) / 1e12
+        out["mfma_%s_tflops" % dt] = {"measured": tf, "nominal": PEAKS_TFLOPS[dt], "frac_of_nominal": tf / PEAKS_TFLOPS[dt]}
+    nbytes = 1 << 30
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device=device)
+    src.fill_(1.0)
+    dst = torch.empty_like(src)
+    best = None
+    for rep in range(6):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        _lib.probe_copy(src.data_ptr(), dst.data_ptr(), nbytes, stream.cuda_stream)
+        e1.record(stream)
+        e1.synchronize()
+        ms = e0.elapsed_time(e1)
+        if rep and (best is None or ms < best):
+            best = ms
+    gbs = 2 * nbytes / (best * 1e-3) / 1e9
+    out["hbm_copy_gbs"] = {"measured": gbs, "nominal": HBM_GBS, "frac_of_nominal": gbs / HBM_GBS}
+    del src, dst, sink
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(workload, budget_s=20.0):
     """The fp64 CPU oracle on a bounded sample of the same layers: all layers
     of the workload at batch 1 (one image), repeated while the time budget
@@ -555,6 +601,7 @@ def main():
 
     if args.calibrate_copy > 0:
         calibration_copy(args.calibrate_copy, dev)
+    extra["measured_peaks"] = measured_peaks(dev)
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -216,6 +216,20 @@ conv_status_t conv2d_winograd_filter_transform(const void* w, void* u, const con
 conv_status_t conv2d_winograd_input_transform(const void* x, void* v, const conv2d_desc_t* desc,
                                               void* stream);
 
+/* Measurement probes for the roofline denominators (no convolution):
+ *  - conv2d_probe_mfma launches `blocks` workgroups of four waves; every
+ *    wave issues `iters` rounds of eight independent 32x32 MFMAs with the
+ *    operands in registers (CONV_BF16: v_mfma_f32_32x32x16_bf16, 32768
+ *    flops each; CONV_F32: v_mfma_f32_32x32x2_f32, 4096 flops each), then
+ *    writes one float per lane to sink (device memory of blocks * 256
+ *    floats, owned by the caller).  INVALID_ARG for a NULL sink, a
+ *    non-positive count or another dtype.
+ *  - conv2d_probe_copy copies `bytes` from src to dst (device memory, not
+ *    overlapping) with 16-byte loads and stores when src is 16-byte aligned.
+ * Both are asynchronous on `stream`: the caller times them with events. */
+conv_status_t conv2d_probe_mfma(int32_t dtype, int32_t blocks, int32_t iters, float* sink, void* stream);
+conv_status_t conv2d_probe_copy(const void* src, void* dst, size_t bytes, void* stream);
+
 /* Static strings; never NULL ("unknown" for values outside the enums). */
 const char* conv2d_status_string(conv_status_t status);
 const char* conv2d_algo_name(conv_algo_t algo);

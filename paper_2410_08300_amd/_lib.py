@@ -25,7 +25,8 @@ EXPORTED = ("conv2d_output_shape", "conv2d_check", "conv2d_workspace_bytes", "co
             "conv2d", "conv2d_packed_filter_bytes", "conv2d_pack_filters", "conv2d_prepacked_workspace_bytes",
             "conv2d_prepacked", "conv2d_describe", "conv2d_im2col", "conv2d_winograd_filter_transform",
             "conv2d_winograd_input_transform", "conv2d_status_string", "conv2d_algo_name",
-            "conv2d_algo_from_name", "conv2d_static_scratch", "conv2d_static_scratch_capacity")
+            "conv2d_algo_from_name", "conv2d_static_scratch", "conv2d_static_scratch_capacity",
+            "conv2d_probe_mfma", "conv2d_probe_copy")
 
 
 EXPORTED_MODEL = ("convsel_model_create", "convsel_model_destroy", "convsel_model_conv", "convsel_model_linear",
@@ -105,6 +106,10 @@ def lib():
         L.conv2d_algo_name.restype = ctypes.c_char_p
         L.conv2d_algo_from_name.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int)]
         L.conv2d_algo_from_name.restype = i32
+        L.conv2d_probe_mfma.argtypes = [i32, i32, i32, vp, vp]
+        L.conv2d_probe_mfma.restype = i32
+        L.conv2d_probe_copy.argtypes = [vp, vp, ctypes.c_size_t, vp]
+        L.conv2d_probe_copy.restype = i32
         # model executor (include/convsel_model.h)
         mp = ctypes.c_void_p
         i64 = ctypes.c_int64
@@ -196,6 +201,22 @@ def packed_filter_bytes(desc, algo):
     if st != CONV_OK:
         raise Conv2dError(st, "conv2d_packed_filter_bytes")
     return out.value
+
+
+def probe_mfma(dtype, blocks, iters, sink_ptr, stream_ptr):
+    """Launches the MFMA-rate probe (conv2d_probe_mfma); dtype "bf16" or "f32"."""
+    st = lib().conv2d_probe_mfma(1 if dtype == "bf16" else 0, int(blocks), int(iters), ctypes.c_void_p(sink_ptr),
+                                 ctypes.c_void_p(stream_ptr))
+    if st != CONV_OK:
+        raise Conv2dError(st, "conv2d_probe_mfma")
+
+
+def probe_copy(src_ptr, dst_ptr, nbytes, stream_ptr):
+    """Launches the 16-byte copy probe (conv2d_probe_copy)."""
+    st = lib().conv2d_probe_copy(ctypes.c_void_p(src_ptr), ctypes.c_void_p(dst_ptr), ctypes.c_size_t(nbytes),
+                                 ctypes.c_void_p(stream_ptr))
+    if st != CONV_OK:
+        raise Conv2dError(st, "conv2d_probe_copy")
 
 
 def prepacked_workspace_bytes(desc, algo):
