@@ -869,6 +869,265 @@ __global__ __launch_bounds__((4 + NL) * 64) void pointwise_dma_kernel(PwArgs a) 
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 1x1 layers, stride 1, no padding, on planes of P*Q = 4 (mod 8) pixels
+// (14 x 14): a tile is 128 output channels of one whole image.  Channel rows
+// of such a plane are 8-byte aligned, so 16-byte units of one row do not
+// exist in memory, but two consecutive rows (c even, c+1) are 4*P*Q bytes,
+// 16-byte aligned and contiguous: the chunk's input, 64 channels of the
+// image, is copied as 32 row pairs with 16-byte LDS DMA exactly as it lies,
+// each pair PU = P*Q/4 units, PU+1 units apart in LDS (the extra unit reads
+// zero).  Row c of the chunk starts at pair(c)*(PU+1)*16 + (c&1)*2*P*Q bytes,
+// 8-byte aligned, which is all the transposing read ds_read_b64_tr_b16
+// needs: the compute waves read pixel fragments as in the kernel above, from
+// these row addresses.  Tile pixels past P*Q read the next row (or the zero
+// unit) and land in output columns that are not stored.
+//
+// The tile spans NJ*32 >= P*Q pixels (7 blocks for 196): each compute wave
+// holds 32 channels x NJ*32 pixels.  Its epilogue stages 16 channel rows at
+// a time as bf16 (after the bias and, without a residual, the ReLU) and
+// stores them as one contiguous run of 16*P*Q*2 bytes (the rows of one image
+// are contiguous, 16-byte aligned when K is even), adding the residual, if
+// any, to the rounded values as the other epilogues do.  K must be a multiple
+// of 32, so a wave's rows are all real or all past K.
+//
+// Units (image, channel tile), channel tiles innermost, walked as in the
+// kernel above; three 41 KiB stages.
+// ---------------------------------------------------------------------------
+constexpr int kImgStages = 3;
+constexpr int kImgMaxPU = 49;                                   // P*Q <= 196
+constexpr int kImgStageBytes = 16384 + 32 * (kImgMaxPU + 1) * 16;  // 41,984
+
+template <int NJ>
+__global__ __launch_bounds__(8 * 64) void pointwise_img_kernel(PwArgs a) {
+  constexpr int BM = 128, CC = 64, NS = kImgStages;
+  constexpr int A_INS = 4;  // filter DMA instructions per loader wave per chunk
+  extern __shared__ __align__(16) vec16 smem[];
+  char* lds = reinterpret_cast<char*>(smem);
+  const int HW = a.H * a.W, PU = HW / 4, pitch = (PU + 1) * 16;
+  const int NBI = (32 * (PU + 1) + 63) / 64;  // input DMA instructions per chunk (all loader waves)
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool loader = wave >= 4;
+  const int lw = loader ? wave - 4 : wave;
+  const int half = lane >> 5, l32 = lane & 31;
+
+  const int units = a.ptiles * a.ktiles;  // ptiles = images of this launch
+  const int per_xcd = (units + 7) >> 3;
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3, slots = gridDim.x >> 3;
+  const int u_end = min(units, (xcd + 1) * per_xcd);
+  const int u_first = xcd * per_xcd + slot;
+  if (u_first >= u_end) return;  // uniform
+
+  if (loader) {
+    const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
+    const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
+    // Filters as in the kernel above: instruction i fills rows
+    // (lw*4 + i)*8 + lane/8, stored unit lane%8, global unit
+    // (lane%8) ^ ((row >> 1) & 7).
+    int a_unit[A_INS];
+    uint32_t a_vo[A_INS];
+#pragma unroll
+    for (int i = 0; i < A_INS; ++i) a_unit[i] = (lane & 7) ^ ((((lw * A_INS + i) * 8 + (lane >> 3)) >> 1) & 7);
+    // Input instruction j (this wave: j = lw, lw+4, ...) fills LDS units
+    // j*64 + lane: pair i = unit / (PU+1), unit k of the pair (k == PU: the
+    // zero unit).  Byte offset within the chunk: i*4*HW + 16k.
+    const int nb = (NBI - lw + 3) / 4;  // this wave's input instructions
+    const int ins = A_INS + nb;
+    auto b_pair = [&](int q) { return ((lw + 4 * q) * 64 + lane) / (PU + 1); };
+    auto b_off = [&](int q) -> uint32_t {
+      const int U = (lw + 4 * q) * 64 + lane, i = U / (PU + 1), k = U - i * (PU + 1);
+      return (i < 32 && k < PU) ? static_cast<uint32_t>(i * 4 * HW + 16 * k) : a.x_bytes;
+    };
+    int tile_u = -1;
+    uint32_t xbase = 0;
+    int fu = u_first, fch = 0, fstage = 0;
+    auto fetch_next = [&]() -> bool {
+      if (fu >= u_end) return false;
+      const int u = __builtin_amdgcn_readfirstlane(fu);
+      const int c0 = __builtin_amdgcn_readfirstlane(fch) * CC;
+      if (u != tile_u) {
+        tile_u = u;
+        const int n = u / a.ktiles, k0 = (u - n * a.ktiles) * BM;
+#pragma unroll
+        for (int i = 0; i < A_INS; ++i)
+          a_vo[i] = static_cast<uint32_t>(((k0 + (lw * A_INS + i) * 8 + (lane >> 3)) * a.C + a_unit[i] * 8) * 2);
+        xbase = static_cast<uint32_t>(n) * a.C * HW * 2;
+      }
+      const bool tail = c0 + CC > a.C;  // uniform
+      char __attribute__((address_space(3)))* base =
+          (char __attribute__((address_space(3)))*)(lds + fstage * kImgStageBytes);
+      const uint32_t wso = static_cast<uint32_t>(c0 * 2);
+#pragma unroll
+      for (int i = 0; i < A_INS; ++i) {
+        const uint32_t vo = (!tail || c0 + a_unit[i] * 8 < a.C) ? a_vo[i] : a.w_bytes;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void_t*)(base + (lw * A_INS + i) * 1024), 16, vo, wso, 0,
+                                                 0);
+      }
+      const uint32_t xso = xbase + static_cast<uint32_t>(c0) * HW * 2;
+      for (int q = 0; q < nb; ++q) {
+        const uint32_t vo = (!tail || c0 + 2 * b_pair(q) < a.C) ? b_off(q) : a.x_bytes;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void_t*)(base + 16384 + (lw + 4 * q) * 1024), 16, vo, xso,
+                                                 0, 0);
+      }
+      fstage = fstage + 1 == NS ? 0 : fstage + 1;
+      if (++fch >= a.nch) {
+        fu += slots;
+        fch = 0;
+      }
+      return true;
+    };
+    // As in the kernel above: NS-1 items ahead, the wave's DMA counted in
+    // order (`later` items issued after the one waited for).
+    int later = -1;
+    for (int s = 0; s < NS - 1; ++s)
+      if (fetch_next()) ++later;
+    int cu = u_first, cch = 0;
+    for (;;) {
+      wait_vmcnt(later * ins);
+      __builtin_amdgcn_s_barrier();  // A: item visible to the compute waves
+      if (fetch_next()) ++later;
+      __builtin_amdgcn_s_barrier();  // B: compute waves are done with this item's stage
+      --later;
+      if (++cch >= a.nch) {
+        cu += slots;
+        if (cu >= u_end) break;
+        cch = 0;
+      }
+    }
+    return;
+  }
+
+  // ---- compute waves: 32 channels (rows lw*32 ..) x NJ*32 pixels ----
+  // Transposing reads: group g = lane/16 covers pixels 16*(g&1) of a block
+  // and channels 8*(g>>1) of the 16-channel step; lane r = lane%16 reads
+  // channel row cr = 8*(g>>1) + r/4 (and cr + 4), pixels 4*(r%4) .. +3.
+  int b_lane;
+  {
+    const int g = lane >> 4, r = lane & 15;
+    const int cr = 8 * (g >> 1) + (r >> 2);
+    b_lane = (cr >> 1) * pitch + (cr & 1) * HW * 2 + (16 * (g & 1) + 4 * (r & 3)) * 2;
+  }
+  const int a_off = (lw * 32 + l32) * 8, a_swz = ((lw * 32 + l32) >> 1) & 7;
+  const uint16_t* bias = reinterpret_cast<const uint16_t*>(a.e.b);
+  uint16_t* y = reinterpret_cast<uint16_t*>(a.e.y);
+  const uint16_t* res = reinterpret_cast<const uint16_t*>(a.e.res);
+  char* staging = lds + NS * kImgStageBytes + lw * (16 * HW * 2);  // 16 rows of this wave
+  const int run_units = 16 * HW * 2 / 16;                          // 16-byte units of 16 rows
+
+  // The bias of a unit's channel is read when the unit starts, long before
+  // its epilogue needs it.
+  auto bias_of = [&](int u) -> float {
+    const int kb = (u % a.ktiles) * BM + lw * 32 + l32;
+    return (bias && kb < a.e.K) ? bf16_to_f32(bias[kb]) : 0.f;
+  };
+  float bv = bias_of(u_first);
+  f32x16_t acc[NJ];
+#pragma unroll
+  for (int nj = 0; nj < NJ; ++nj) acc[nj] = zero16();
+  int cu = u_first, cch = 0, cstage = 0;
+  for (;;) {
+    lds_sync();  // A
+    const char* As = lds + cstage * kImgStageBytes;
+    const char* Bs = As + 16384;
+    // Step kst (16 channels: pairs 8 kst .., the second read 4 channels = 2
+    // pairs on): its fragments are read while the previous step's MFMAs run.
+    bf16x8_t af[2], bfr[2][NJ];
+    auto load_step = [&](int kst, auto set_c) {
+      constexpr int SET = decltype(set_c)::value;
+      const int u = 2 * kst + half;
+      af[SET] = *reinterpret_cast<const bf16x8_t*>(As + (a_off + (u ^ a_swz)) * 16);
+      const char* p0 = Bs + kst * 8 * pitch + b_lane;
+#pragma unroll
+      for (int nj = 0; nj < NJ; ++nj) {
+        const char* p = p0 + nj * 64;
+        const v4s_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)(p));
+        const v4s_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)(p + 2 * pitch));
+        bfr[SET][nj] = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+    };
+    // (Scheduling barriers keep each step's reads together ahead of the
+    // previous step's MFMAs; left alone, the compiler interleaves one read
+    // per MFMA and waits for it.)
+    load_step(0, std::integral_constant<int, 0>{});
+    static_for<CC / 16>([&](auto k_c) {
+      constexpr int KST = decltype(k_c)::value, SET = KST & 1;
+      if constexpr (KST + 1 < CC / 16) load_step(KST + 1, std::integral_constant<int, SET ^ 1>{});
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int nj = 0; nj < NJ; ++nj)
+        acc[nj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[SET][nj], af[SET], acc[nj], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    lds_sync();  // B: the stage may be refilled
+    cstage = cstage + 1 == NS ? 0 : cstage + 1;
+    if (++cch < a.nch) continue;
+
+    // Unit done: image n, channels k0 + lw*32 ...
+    const int n = cu / a.ktiles, kw = (cu - n * a.ktiles) * BM + lw * 32;
+    if (kw < a.e.K) {  // uniform per wave (K is a multiple of 32)
+      const bool relu_now = a.e.relu && !res;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        // Stage rows 16h .. 16h+15 (lanes whose channel is among them).
+        if ((l32 >> 4) == h) {
+          char* row = staging + (l32 - 16 * h) * HW * 2;
+#pragma unroll
+          for (int nj = 0; nj < NJ; ++nj)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const int px = nj * 32 + 8 * g + 4 * half;
+              if (px < HW) {
+                float v[4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                  v[t] = acc[nj][4 * g + t] + bv;
+                  if (relu_now) v[t] = fmaxf(v[t], 0.f);
+                }
+                uint2 w;
+                w.x = f32x2_to_bf16x2(v[0], v[1]);
+                w.y = f32x2_to_bf16x2(v[2], v[3]);
+                *reinterpret_cast<uint2*>(row + px * 2) = w;
+              }
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's staging writes
+        __builtin_amdgcn_wave_barrier();
+        // The 16 rows are one contiguous run of y (and of the residual).
+        const int64_t o = (static_cast<int64_t>(n) * a.e.K + kw + 16 * h) * HW;  // elements
+        for (int q = lane; q < run_units; q += 64) {
+          uint4 d = *reinterpret_cast<const uint4*>(staging + q * 16);
+          if (res) {
+            uint4 rr;
+            __builtin_memcpy(&rr, res + o + q * 8, 16);
+            const uint32_t dw[4] = {d.x, d.y, d.z, d.w}, rw[4] = {rr.x, rr.y, rr.z, rr.w};
+            uint32_t ow[4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+              float lo = __uint_as_float(dw[m] << 16) + __uint_as_float(rw[m] << 16);
+              float hi = __uint_as_float(dw[m] & 0xFFFF0000u) + __uint_as_float(rw[m] & 0xFFFF0000u);
+              if (a.e.relu) {
+                lo = fmaxf(lo, 0.f);
+                hi = fmaxf(hi, 0.f);
+              }
+              ow[m] = f32x2_to_bf16x2(lo, hi);
+            }
+            d = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+          }
+          __builtin_memcpy(y + o + q * 8, &d, 16);
+        }
+        __builtin_amdgcn_wave_barrier();  // the next rows reuse the staging
+      }
+    }
+#pragma unroll
+    for (int nj = 0; nj < NJ; ++nj) acc[nj] = zero16();
+    cu += slots;
+    if (cu >= u_end) break;
+    cch = 0;
+    bv = bias_of(cu);
+  }
+}
+
 // Input of the 1x1 DMA kernel for layers whose plane is not a multiple of 8
 // pixels, or that are strided or padded: xr[n][c][pix] = the input pixel
 // that output pixel pix = p*Q + q reads (zero outside the image), and zero
@@ -1133,6 +1392,7 @@ struct PwPlan {
   bool dma;              // bf16: the LDS-DMA kernel
   bool repack;           // ... on a repacked input (see repack_plane_kernel)
   bool ub4;              // ... reading pixel pairs in place (4-byte DMA units)
+  bool img;              // ... or, 14 x 14 planes with enough images, whole-image tiles (pointwise_img_kernel)
   int span;              // pixels per image of the tile index space
   size_t repack_bytes;   // repacked input of one launch
   int64_t images_per_launch;
@@ -1142,7 +1402,7 @@ struct PwPlan {
 };
 
 template <typename T>
-bool make_pw_plan(const Shape& s, PwPlan& pl, int64_t N1 = -1, bool allow_dma = true) {
+bool make_pw_plan(const Shape& s, PwPlan& pl, int64_t N1 = -1, bool allow_dma = true, bool allow_img = true) {
   constexpr int UE = elem<T>::per16;
   if (s.R != 1 || s.S != 1 || s.G != 1 || s.C % UE != 0) return false;
   // bf16: the DMA kernel, on the input as it is when the layer is
@@ -1200,6 +1460,17 @@ bool make_pw_plan(const Shape& s, PwPlan& pl, int64_t N1 = -1, bool allow_dma = 
   } else {
     split_chunks((int64_t)a.ptiles * a.ktiles, a.nch, &a.e.splits, &a.chunks_per_split);
   }
+  // 14 x 14 planes: whole-image tiles when the images and channel tiles
+  // fill most of the CUs in one unsplit round (ResNet-50's 256 -> 1024
+  // layers at batch 32: 256 units of 4 chunks, against 392 units of the
+  // pixel-pair kernel); the rows of one image's 128 channels are then one
+  // contiguous run of the output.
+  pl.img = allow_img && pl.ub4 && s.H * s.W == 196 && s.K % 32 == 0 && N1 * a.ktiles >= 192 && N1 * a.ktiles <= 2 * kCUs;
+  if (pl.img) {
+    a.ptiles = (int)N1;
+    a.e.splits = 1;
+    a.chunks_per_split = a.nch;
+  }
   a.e.K = (int)s.K; a.e.Kg = (int)s.K; a.e.PQ = (int)(s.P * s.Q); a.e.relu = s.relu ? 1 : 0;
   a.e.NPQ = a.NPQ;
   a.e.span = pl.dma ? pl.span : (int)(s.P * s.Q);
@@ -1209,6 +1480,7 @@ bool make_pw_plan(const Shape& s, PwPlan& pl, int64_t N1 = -1, bool allow_dma = 
   const size_t stage = (size_t)4 * 32 * (BN / 2) * sizeof(float);  // epilogue staging
   pl.lds = tiles > stage ? tiles : stage;
   if (pl.dma) pl.lds = (size_t)(kDmaStages + 1) * kDmaStageBytes;
+  if (pl.img) pl.lds = (size_t)kImgStages * kImgStageBytes + (size_t)4 * 16 * 196 * 2;
   return true;
 }
 
@@ -1255,6 +1527,20 @@ hipError_t pw_dma_launch(const PwPlan& pl, const PwArgs& a, hipStream_t stream) 
   return hipGetLastError();
 }
 
+hipError_t pw_img_launch(const PwPlan& pl, const PwArgs& a, hipStream_t stream) {
+  const auto kern = pointwise_img_kernel<7>;
+  static std::atomic<int> lds_raised{0};
+  if (!lds_raised.load()) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsLimit);
+    if (e != hipSuccess) return e;
+    lds_raised.store(1);
+  }
+  const int g = (a.ptiles * a.ktiles + 7) / 8 * 8;
+  hipLaunchKernelGGL(kern, dim3((unsigned)(g < kCUs ? g : kCUs)), dim3(8 * 64), pl.lds, stream, a);
+  return hipGetLastError();
+}
+
 template <typename T, int BM, bool GATHER>
 hipError_t pw_launch(const PwPlan& pl, const PwArgs& a, hipStream_t stream) {
   const dim3 grid((unsigned)pw_grid(a, BM));
@@ -1279,12 +1565,17 @@ hipError_t pw_main_typed(const Shape& s, const void* x, const void* w, const voi
   if (pl.dma && !pl.repack && reinterpret_cast<uintptr_t>(x) % (pl.ub4 ? 4 : 16) != 0 &&
       !make_pw_plan<T>(s, pl, -1, false))
     return hipErrorInvalidValue;
+  // Whole-image tiles store 16-byte runs and read the input by 16-byte DMA:
+  // other alignments take the pixel-pair kernel.
+  const bool img_ok = reinterpret_cast<uintptr_t>(x) % 16 == 0 && reinterpret_cast<uintptr_t>(y) % 16 == 0 &&
+                      reinterpret_cast<uintptr_t>(res) % 16 == 0;
+  if (pl.img && !img_ok && !make_pw_plan<T>(s, pl, -1, true, false)) return hipErrorInvalidValue;
   char* ws = reinterpret_cast<char*>(part_ws);
   const int64_t img_elems = s.C * s.H * s.W, out_elems = s.K * s.P * s.Q;
   for (int64_t n0 = 0; n0 < s.N; n0 += pl.images_per_launch) {
     const int64_t cnt = s.N - n0 < pl.images_per_launch ? s.N - n0 : pl.images_per_launch;
     PwPlan cur = pl;
-    if (cnt != pl.images_per_launch && !make_pw_plan<T>(s, cur, cnt, pl.dma)) return hipErrorInvalidValue;
+    if (cnt != pl.images_per_launch && !make_pw_plan<T>(s, cur, cnt, pl.dma, img_ok)) return hipErrorInvalidValue;
     if ((cur.repack || cur.a.e.splits > 1) && !ws) return hipErrorInvalidValue;
     PwArgs a = cur.a;
     a.x = reinterpret_cast<const T*>(x) + n0 * img_elems;
@@ -1311,7 +1602,8 @@ hipError_t pw_main_typed(const Shape& s, const void* x, const void* w, const voi
         a.x = ws;
         a.x_bytes = (uint32_t)(cnt * s.C * cur.span * s.esize());
       }
-      e = cur.ub4 ? pw_dma_launch<4>(cur, a, stream) : pw_dma_launch<16>(cur, a, stream);
+      e = cur.img ? pw_img_launch(cur, a, stream)
+                  : cur.ub4 ? pw_dma_launch<4>(cur, a, stream) : pw_dma_launch<16>(cur, a, stream);
     } else {
       // Pixel-quad loads need the input aligned to 4 elements.
       const bool gather = cur.gather || reinterpret_cast<uintptr_t>(a.x) % (4 * s.esize()) != 0;
@@ -1345,6 +1637,18 @@ size_t pw_split_bytes(const Shape& s) {
   // input) use their own split count.
   PwPlan alt;
   if (make_pw_plan<T>(s, alt, -1, false) && alt.part_bytes > need) need = alt.part_bytes;
+  // ... and calls whose operands do not allow whole-image tiles.
+  if (pl.img && make_pw_plan<T>(s, alt, -1, true, false)) {
+    size_t n2 = (alt.repack_bytes ? align256(alt.repack_bytes) : 0) + alt.part_bytes;
+    if (rem) {
+      PwPlan last;
+      if (make_pw_plan<T>(s, last, rem, true, false)) {
+        const size_t n3 = (last.repack_bytes ? align256(last.repack_bytes) : 0) + last.part_bytes;
+        if (n3 > n2) n2 = n3;
+      }
+    }
+    if (n2 > need) need = n2;
+  }
   return need;
 }
 
@@ -1354,6 +1658,15 @@ std::string pw_describe(const Shape& s) {
   make_pw_plan<T>(s, pl);
   char buf[512];
   const char* tn = sizeof(T) == 2 ? "bf16" : "f32";
+  if (pl.img) {
+    snprintf(buf, sizeof(buf),
+             "implicit_gemm kernels=pointwise_img_kernel<7> tile=128x196 units=%dx%d grid=%d chunk=64 lds=%zu "
+             "images_per_launch=%lld (1x1: filters used as given; whole-image tiles, channel-row pairs by 16-byte "
+             "DMA)",
+             pl.a.ptiles, pl.a.ktiles, std::min(kCUs, (pl.a.ptiles * pl.a.ktiles + 7) / 8 * 8), pl.lds,
+             (long long)pl.images_per_launch);
+    return buf;
+  }
   if (pl.dma) {
     snprintf(buf, sizeof(buf),
              "implicit_gemm kernels=%spointwise_dma_kernel<%d,%d,%d>%s tile=128x%d units=%dx%dx%d grid=%d chunk=64 "

@@ -192,9 +192,18 @@ def test_workspace_sizes():
     assert "pointwise_dma_kernel<16,4,4>" in _lib.describe(pw, "implicit_gemm")
     # A 14x14 plane (even, not a multiple of 8) is read in place as pixel
     # pairs: no repack, 4-byte DMA units.
-    pw14 = _lib.make_desc(32, 256, 14, 14, 1024, 1, 1, 1, 0, 1, 1, "bf16")
+    pw14 = _lib.make_desc(16, 256, 14, 14, 1024, 1, 1, 1, 0, 1, 1, "bf16")
     assert "kernels=pointwise_dma_kernel<4,4,4>" in _lib.describe(pw14, "implicit_gemm")
     assert _lib.prepacked_workspace_bytes(pw14, "implicit_gemm") == 0
+    # With enough images for most of the CUs (N x channel tiles >= 192),
+    # whole-image tiles: 32 images x 8 channel tiles, one round.
+    img = _lib.make_desc(32, 256, 14, 14, 1024, 1, 1, 1, 0, 1, 1, "bf16")
+    assert "kernels=pointwise_img_kernel<7> tile=128x196 units=32x8 grid=256" in _lib.describe(img, "implicit_gemm")
+    assert _lib.prepacked_workspace_bytes(img, "implicit_gemm") == 0
+    # ... not when K is not a multiple of 32, or with too few units.
+    assert "pointwise_img_kernel" not in _lib.describe(_lib.make_desc(32, 256, 14, 14, 1000, 1, 1, 1, 0, 1, 1, "bf16"),
+                                                       "implicit_gemm")
+    assert "pointwise_img_kernel" not in _lib.describe(pw14, "implicit_gemm")
     # The 7x7 stride-2 stem (bf16, 3 channels) takes the filter-row kernel:
     # its package is the LDS image of each 64-filter tile, 64 x 23 units of
     # 16 bytes (21 filter rows, rounded up to an odd count); no other

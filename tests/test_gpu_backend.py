@@ -114,6 +114,8 @@ RESIDUAL = [
     ("bf16", 4, 64, 14, 14, 256, 1, 1, 0, True, "pointwise_dma_kernel<4,4,4>"),
     ("bf16", 4, 256, 14, 14, 64, 1, 1, 0, False, "pointwise_dma_kernel<4,4,4> "),
     ("bf16", 4, 1024, 14, 14, 64, 1, 1, 0, False, "pointwise_dma_kernel<4,4,4>;splitk_reduce_kernel"),
+    ("bf16", 24, 256, 14, 14, 1024, 1, 1, 0, True, "kernels=pointwise_img_kernel<7>"),
+    ("bf16", 32, 256, 14, 14, 1024, 1, 1, 0, False, "kernels=pointwise_img_kernel<7>"),
     ("bf16", 5, 64, 2, 3, 96, 1, 1, 0, True, "repack_plane_kernel;pointwise_dma_kernel<16,4,4>"),
     ("bf16", 4, 1024, 7, 7, 256, 1, 1, 0, True, "repack_plane_kernel;pointwise_dma_kernel<16,4,4>;splitk_reduce_kernel"),
     ("bf16", 3, 64, 3, 3, 64, 1, 1, 0, False, "repack_plane_kernel;pointwise_dma_kernel<16,4,4>"),

@@ -310,6 +310,9 @@ POINTWISE = [
     (2, 40, 9, 12, 40, 1, 0, "f32", False, False, "K <= 64 tile"),
     (4, 24, 28, 28, 64, 1, 0, "bf16", False, False, "single partial chunk"),
     (3, 256, 14, 14, 300, 1, 0, "bf16", True, False, "14x14 plane read in place as pixel pairs, tiles cross images"),
+    (24, 256, 14, 14, 1024, 1, 0, "bf16", True, False, "14x14 whole-image tiles, 192 units"),
+    (24, 200, 14, 14, 1024, 1, 0, "bf16", False, True, "14x14 whole-image tiles, channel tail"),
+    (40, 256, 14, 14, 1024, 1, 0, "bf16", True, True, "14x14 whole-image tiles, 320 units: two per workgroup"),
 ]
 
 
@@ -349,6 +352,32 @@ def test_pointwise_unaligned_operands(which, side):
     y = cs.conv2d(xd, wd, None, algo="implicit_gemm")
     torch.cuda.synchronize()
     assert rel_err(f64(y), ref) <= tolerance("bf16", "implicit_gemm")
+
+
+def test_pointwise_whole_image_tiles_fall_back_for_unaligned_output():
+    """A 14 x 14 layer that would take whole-image tiles (16-byte stores of
+    each image's rows) with the output one element past a 16-byte boundary:
+    the call takes the pixel-pair kernel and is still correct."""
+    from paper_2410_08300_amd import _lib
+    N, C, H, Wd, K = 24, 256, 14, 14, 1024
+    g = torch.Generator().manual_seed(W.seed_for(12, 7))
+    x = torch.randn(N, C, H, Wd, generator=g).to(torch.bfloat16)
+    w = (torch.randn(K, C, 1, 1, generator=g) * (2.0 / C) ** 0.5).to(torch.bfloat16)
+    desc = _lib.make_desc(N, C, H, Wd, K, 1, 1, 1, 0, 1, 1, "bf16")
+    assert "pointwise_img_kernel" in _lib.describe(desc, "implicit_gemm")
+    ref = oracle.conv2d(f64(x), f64(w), None, 1, 0, 1, 1, False)
+    xd, wd = x.to(DEV), w.to(DEV)
+    ybuf = torch.zeros(N * K * H * Wd + 1, dtype=torch.bfloat16, device=DEV)
+    y = ybuf[1:]
+    assert y.data_ptr() % 16 != 0
+    nws = _lib.workspace_bytes(desc, "implicit_gemm")
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=DEV)
+    say("case whole-image tiles, unaligned y")
+    st = _lib.conv2d_raw(xd.data_ptr(), wd.data_ptr(), None, y.data_ptr(), desc, "implicit_gemm", ws.data_ptr(), nws,
+                         torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert st == _lib.CONV_OK
+    assert rel_err(f64(y.view(N, K, H, Wd)), ref) <= tolerance("bf16", "implicit_gemm")
 
 
 # Wide-filter, few-channel bf16 layers (5 <= S <= 8, even column stride,
