@@ -463,6 +463,7 @@ GUARDED = [
     # N, C, H, W, K, R, stride, pad, dtype, algos
     (1, 1024, 14, 14, 512, 1, 1, 0, "bf16", ("implicit_gemm", "im2col_gemm")),
     (2, 2048, 7, 7, 512, 1, 1, 0, "bf16", ("implicit_gemm",)),
+    (24, 256, 14, 14, 1024, 1, 1, 0, "bf16", ("implicit_gemm",)),
     (3, 64, 56, 56, 256, 1, 1, 0, "bf16", ("implicit_gemm",)),
     (2, 256, 15, 15, 128, 1, 2, 0, "bf16", ("implicit_gemm", "im2col_gemm")),
     (2, 512, 7, 7, 512, 3, 1, 1, "bf16", ("implicit_gemm", "winograd", "im2col_gemm")),
