@@ -121,6 +121,7 @@ KERNEL_SOURCES = {
     "implicit_gemm_kernel": ("implicit_gemm.hip", "igemm_common.hpp"),
     "pointwise_": ("implicit_gemm.hip", "igemm_common.hpp"),
     "repack_plane_kernel": ("implicit_gemm.hip", "igemm_common.hpp"),
+    "repack_s2_rows_kernel": ("implicit_gemm.hip", "igemm_common.hpp"),
     "splitk_reduce_kernel": ("igemm_common.hpp",),
     "implicit_rows_kernel": ("implicit_rows.hip", "igemm_common.hpp"),
     "conv3x3_kernel": ("conv3x3.hip", "igemm_common.hpp"),

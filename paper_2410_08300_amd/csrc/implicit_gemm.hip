@@ -1206,6 +1206,59 @@ __global__ __launch_bounds__(256) void repack_plane_kernel(const uint16_t* __res
   *reinterpret_cast<uint4*>(xr + static_cast<int64_t>(plane) * span + pix0) = o;
 }
 
+// The same repack for stride 2 on both axes without padding (the ResNet
+// projections), one thread per 8-pixel group of one output row: output row p
+// reads input row 2p, so a group is the even elements of 16 consecutive
+// input values, two 16-byte loads issued together.  Groups never cross an
+// output row (rows of 28, 14 or 7 pixels end in a shorter group, stored in
+// 8-, 4- and 2-byte pieces), so no thread takes the element-by-element path
+// of the kernel above except where the loads would run past the end of x.
+// The thread holding a plane's last group also zeroes the span's tail.
+__global__ __launch_bounds__(256) void repack_s2_rows_kernel(const uint16_t* __restrict__ x, uint16_t* __restrict__ xr,
+                                                             int planes, int H, int W, int P, int Q, int span) {
+  const int G = (Q + 7) / 8;  // groups per output row
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= planes * P * G) return;
+  const int plane = t / (P * G), rem = t - plane * (P * G);
+  const int p = rem / G, q0 = (rem - p * G) * 8;
+  const int n = Q - q0 < 8 ? Q - q0 : 8;  // pixels of this group
+  const int HW = H * W;
+  const uint16_t* src = x + static_cast<int64_t>(plane) * HW;
+  const int64_t left = static_cast<int64_t>(planes - plane) * HW;  // elements from src to the end of x
+  const int64_t in0 = static_cast<int64_t>(2 * p) * W + 2 * q0;
+  uint32_t v[8];
+  if (in0 + 16 <= left) {
+    uint4 ua, ub;
+    __builtin_memcpy(&ua, src + in0, 16);
+    __builtin_memcpy(&ub, src + in0 + 8, 16);
+    v[0] = ua.x & 0xFFFFu; v[1] = ua.y & 0xFFFFu; v[2] = ua.z & 0xFFFFu; v[3] = ua.w & 0xFFFFu;
+    v[4] = ub.x & 0xFFFFu; v[5] = ub.y & 0xFFFFu; v[6] = ub.z & 0xFFFFu; v[7] = ub.w & 0xFFFFu;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = e < n ? src[in0 + 2 * e] : 0u;
+  }
+  uint16_t* dst = xr + static_cast<int64_t>(plane) * span + p * Q + q0;
+  if (n == 8) {
+    const uint4 o = make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
+    __builtin_memcpy(dst, &o, 16);
+  } else {
+    int e = 0;
+    if (n - e >= 4) {
+      const uint2 o = make_uint2(v[0] | (v[1] << 16), v[2] | (v[3] << 16));
+      __builtin_memcpy(dst, &o, 8);
+      e = 4;
+    }
+    if (n - e >= 2) {
+      const uint32_t o = v[e] | (v[e + 1] << 16);
+      __builtin_memcpy(dst + e, &o, 4);
+      e += 2;
+    }
+    if (n - e >= 1) dst[e] = static_cast<uint16_t>(v[e]);
+  }
+  if (p == P - 1 && q0 + n == Q)
+    for (int e = P * Q; e < span; ++e) xr[static_cast<int64_t>(plane) * span + e] = 0;
+}
+
 // Wp[g][ch][kp][tap][cg][e] = w[g*Kg + kp][ch*Cc + cg*UE + e][tap], zero past
 // Kg rows or Cg channels.  One workgroup per packed row (g, ch, kp); its
 // threads write the row's RS*NG*UE elements consecutively.
@@ -1593,10 +1646,17 @@ hipError_t pw_main_typed(const Shape& s, const void* x, const void* w, const voi
     if (cur.dma) {
       if (cur.repack) {
         const int planes = (int)(cnt * s.C);
-        const int threads = planes * (cur.span / 8);
-        hipLaunchKernelGGL(repack_plane_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream,
-                           reinterpret_cast<const uint16_t*>(a.x), reinterpret_cast<uint16_t*>(ws), planes,
-                           (int)s.H, (int)s.W, (int)s.P, (int)s.Q, s.sh, s.sw, s.ph, s.pw, cur.span);
+        if (s.sh == 2 && s.sw == 2 && s.ph == 0 && s.pw == 0) {
+          const int threads = planes * (int)s.P * (int)((s.Q + 7) / 8);
+          hipLaunchKernelGGL(repack_s2_rows_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream,
+                             reinterpret_cast<const uint16_t*>(a.x), reinterpret_cast<uint16_t*>(ws), planes,
+                             (int)s.H, (int)s.W, (int)s.P, (int)s.Q, cur.span);
+        } else {
+          const int threads = planes * (cur.span / 8);
+          hipLaunchKernelGGL(repack_plane_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream,
+                             reinterpret_cast<const uint16_t*>(a.x), reinterpret_cast<uint16_t*>(ws), planes,
+                             (int)s.H, (int)s.W, (int)s.P, (int)s.Q, s.sh, s.sw, s.ph, s.pw, cur.span);
+        }
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         a.x = ws;
@@ -1671,7 +1731,10 @@ std::string pw_describe(const Shape& s) {
     snprintf(buf, sizeof(buf),
              "implicit_gemm kernels=%spointwise_dma_kernel<%d,%d,%d>%s tile=128x%d units=%dx%dx%d grid=%d chunk=64 "
              "span=%d lds=%zu images_per_launch=%lld (1x1: filters used as given)",
-             pl.repack ? "repack_plane_kernel;" : "", pl.ub4 ? 4 : 16, kDmaStages, kDmaLoaders,
+             !pl.repack ? ""
+             : s.sh == 2 && s.sw == 2 && s.ph == 0 && s.pw == 0 ? "repack_s2_rows_kernel;"
+                                                                 : "repack_plane_kernel;",
+             pl.ub4 ? 4 : 16, kDmaStages, kDmaLoaders,
              pl.a.e.splits > 1 ? ";splitk_reduce_kernel" : "",
              BN, pl.a.ptiles, pl.a.ktiles, pl.a.e.splits, pw_dma_grid(pl.a), pl.span, pl.lds,
              (long long)pl.images_per_launch);

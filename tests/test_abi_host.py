@@ -186,6 +186,10 @@ def test_workspace_sizes():
     assert _lib.workspace_bytes(pws, "implicit_gemm") == 512 * 2048 * 2 + repack + 4 * 32 * 512 * 49 * 4
     assert _lib.prepacked_workspace_bytes(pws, "implicit_gemm") == repack + 4 * 32 * 512 * 49 * 4
     assert "repack_plane_kernel;pointwise_dma_kernel<16,4,4>;splitk_reduce_kernel" in _lib.describe(pws, "implicit_gemm")
+    # Stride-2 projections are repacked one output row at a time.
+    ds = _lib.make_desc(32, 256, 56, 56, 512, 1, 1, 2, 0, 1, 1, "bf16")
+    assert "kernels=repack_s2_rows_kernel;pointwise_dma_kernel<16,4,4> " in _lib.describe(ds, "implicit_gemm")
+    assert _lib.prepacked_workspace_bytes(ds, "implicit_gemm") == 32 * 256 * 784 * 2
     # fp32 1x1 layers keep the register-transposing kernel.
     pwf = _lib.make_desc(32, 256, 56, 56, 64, 1, 1, 1, 0, 1, 1, "f32")
     assert "pointwise_gemm_kernel<f32,64,0,2>" in _lib.describe(pwf, "implicit_gemm")

@@ -313,6 +313,10 @@ POINTWISE = [
     (24, 256, 14, 14, 1024, 1, 0, "bf16", True, False, "14x14 whole-image tiles, 192 units"),
     (24, 200, 14, 14, 1024, 1, 0, "bf16", False, True, "14x14 whole-image tiles, channel tail"),
     (40, 256, 14, 14, 1024, 1, 0, "bf16", True, True, "14x14 whole-image tiles, 320 units: two per workgroup"),
+    (3, 64, 56, 56, 96, 2, 0, "bf16", True, False, "stride 2, rows of 28 (row-aligned repack)"),
+    (4, 128, 28, 28, 64, 2, 0, "bf16", False, True, "stride 2, rows of 14, span tail"),
+    (5, 96, 14, 14, 80, 2, 0, "bf16", True, True, "stride 2, rows of 7"),
+    (3, 48, 15, 13, 40, 2, 0, "bf16", False, False, "stride 2, odd plane, last loads element by element"),
 ]
 
 
