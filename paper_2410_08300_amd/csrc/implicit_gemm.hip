@@ -1483,7 +1483,12 @@ bool make_pw_plan(const Shape& s, PwPlan& pl, int64_t N1 = -1, bool allow_dma = 
   a.HW = pl.dma ? pl.span : (int)(s.H * s.W);
   a.P = (int)s.P; a.Q = (int)s.Q; a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw;
   a.NPQ = (int)(N1 * (pl.dma ? pl.span : s.P * s.Q));
-  pl.BM = pl.dma || s.K > 64 ? 128 : 64;
+  // fp32 takes the 64-row tile at every K: its matrix cores run at a
+  // sixteenth of the bf16 rate, so rows past K in a 128-row tile (K = 144,
+  // 160, 192, 320 in MobileNetV2) cost more than the 64-row tile's extra
+  // input reads, and two of its workgroups share a CU (MobileNetV2's 1x1
+  // layers at N = 64: 1246 -> 1084 us over the unique layers).
+  pl.BM = pl.dma || (sizeof(T) == 2 && s.K > 64) ? 128 : 64;
   a.ktiles = (int)((s.K + pl.BM - 1) / pl.BM);
   a.ptiles = (a.NPQ + BN - 1) / BN;
   a.nch = (int)((s.C + kPwUnits * UE - 1) / (kPwUnits * UE));

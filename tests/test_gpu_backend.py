@@ -135,9 +135,9 @@ RESIDUAL = [
     ("bf16", 2, 3, 64, 64, 64, 7, 2, 3, True, "implicit_rows_kernel"),
     ("f32", 2, 64, 28, 28, 64, 3, 1, 1, True, "implicit_gemm_kernel<f32,64,2,9>;splitk_reduce_kernel"),
     ("f32", 3, 16, 16, 16, 16, 3, 1, 1, False, "implicit_gemm_kernel<f32,64,2,9>"),
-    ("f32", 5, 64, 2, 3, 96, 1, 1, 0, True, "pointwise_gemm_kernel<f32,128,1,2>"),
-    ("f32", 4, 1024, 7, 7, 256, 1, 1, 0, False, "pointwise_gemm_kernel<f32,128,1,2>;splitk_reduce_kernel"),
-    ("f32", 4, 64, 56, 56, 256, 1, 1, 0, True, "pointwise_gemm_kernel<f32,128,0,2>"),
+    ("f32", 5, 64, 2, 3, 96, 1, 1, 0, True, "pointwise_gemm_kernel<f32,64,1,2>"),
+    ("f32", 4, 1024, 7, 7, 256, 1, 1, 0, False, "pointwise_gemm_kernel<f32,64,1,2>;splitk_reduce_kernel"),
+    ("f32", 4, 64, 56, 56, 256, 1, 1, 0, True, "pointwise_gemm_kernel<f32,64,0,2>"),
     ("f32", 2, 3, 64, 64, 64, 7, 2, 3, False, "implicit_gemm_kernel<f32,64,1,0>"),
 ]
 
