@@ -272,8 +272,8 @@ def summary(rows, nets, st):
             lines.append("| %s | %s | n/a | %s |" % (n["network"], n["table"], n["reason"]))
     lines.append("")
     for s in st:
-        lines.append("oracle, one thread: %s %s at batch 1: %.3f s (%.2f GFLOP/s)" %
-                     (s["workload"], s["layer"], s["seconds"], s["gflops"]))
+        lines.append("oracle, one thread: %s %s at batch 1: %.3f ms (%.2f GFLOP/s)" %
+                     (s["workload"], s["layer"], s["seconds"] * 1e3, s["gflops"]))
     return "\n".join(lines) + "\n"
 
 
